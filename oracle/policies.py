@@ -1,0 +1,114 @@
+"""Integer policies of the stage runtime, written independently -- TEST INFRASTRUCTURE.
+
+The HIP runtime must reproduce these bit-exactly (block tables, slot log,
+residency changes).  Each is a reading of the paper where it leaves the detail
+open; the readings are:
+
+* Paged KV allocation.  One pool of blocks of ``block`` tokens shared by all
+  sequences of the stage (one block id addresses the same block in every
+  layer's pool).  Free blocks are handed out lowest id first.  A sequence takes
+  a new block when it writes a position that is a multiple of ``block``.  Within
+  a call, sequences allocate in call order (micro-batch ids in the order given,
+  then batch rows ascending), each taking all blocks its new tokens need before
+  the next.  A call that would exhaust the pool changes nothing.
+* Slot assignment (Section III-C: a reusable loading buffer is refilled once the
+  GPU signals it is done with the previous layer).  The k-th layer load of the
+  stage's life (k = 0, 1, ...) goes to slot k mod S.  Each call loads each
+  streamed layer once, in ascending layer order, and runs it for every
+  micro-batch of the call before its slot is reused.
+* Residency schedule (Section III-E, online memory-aware planner: progressive
+  offloading at token-length thresholds TS^j).  Before a call, let c be the
+  longest sequence length in the stage once the call's tokens are appended.
+  Every threshold TS^j <= c not yet applied demotes one resident layer, the
+  highest id first, so a prefix of layers stays resident.
+"""
+from __future__ import annotations
+
+import heapq
+from typing import Dict, Hashable, Iterable, List, Sequence, Tuple
+
+
+class BlockAllocator:
+    def __init__(self, n_blocks: int, block: int = 16):
+        self.block = block
+        self.free: List[int] = list(range(n_blocks))
+        heapq.heapify(self.free)
+        self.tables: Dict[Hashable, List[int]] = {}
+        self.lengths: Dict[Hashable, int] = {}
+
+    def _blocks_for(self, length: int) -> int:
+        return -(-length // self.block)
+
+    def need(self, key: Hashable, n_new: int) -> int:
+        length = self.lengths.get(key, 0)
+        return self._blocks_for(length + n_new) - len(self.tables.get(key, []))
+
+    def call(self, keys_and_counts: Sequence[Tuple[Hashable, int]]) -> Dict[Hashable, List[int]]:
+        """Append n tokens to each listed sequence, in the order given.  Returns new block ids."""
+        total = sum(self.need(k, n) for k, n in keys_and_counts)
+        if total > len(self.free):
+            raise MemoryError("KV pool exhausted")
+        new = {}
+        for key, n in keys_and_counts:
+            got = [heapq.heappop(self.free) for _ in range(self.need(key, n))]
+            self.tables.setdefault(key, []).extend(got)
+            self.lengths[key] = self.lengths.get(key, 0) + n
+            new[key] = got
+        return new
+
+    def truncate(self, key: Hashable, n_drop: int) -> None:
+        """Drop the last n_drop tokens; blocks left empty return to the pool."""
+        length = self.lengths[key] - n_drop
+        assert length >= 0
+        keep = self._blocks_for(length)
+        for b in self.tables[key][keep:]:
+            heapq.heappush(self.free, b)
+        self.tables[key] = self.tables[key][:keep]
+        self.lengths[key] = length
+
+    def release(self, key: Hashable) -> None:
+        for b in self.tables.pop(key, []):
+            heapq.heappush(self.free, b)
+        self.lengths.pop(key, None)
+
+    def table(self, key: Hashable) -> List[int]:
+        return list(self.tables.get(key, []))
+
+
+class SlotSchedule:
+    """Which HBM slot each streamed-layer load goes to."""
+
+    def __init__(self, n_slots: int):
+        self.n_slots = n_slots
+        self.loads = 0
+        self.log: List[Tuple[int, int, int]] = []   # (call number, layer, slot)
+
+    def call(self, call_no: int, streamed_layers: Iterable[int]) -> None:
+        for layer in sorted(streamed_layers):
+            self.log.append((call_no, layer, self.loads % self.n_slots))
+            self.loads += 1
+
+
+class ResidencySchedule:
+    """Resident set of layers and its threshold-driven shrinking."""
+
+    def __init__(self, n_layers: int, resident: Iterable[int], thresholds: Sequence[int] = ()):
+        self.n_layers = n_layers
+        self.resident = set(resident)
+        self.thresholds = list(thresholds)
+        self.applied = 0
+        self.log: List[Tuple[int, int]] = []        # (call number, demoted layer)
+
+    def before_call(self, call_no: int, longest_after_call: int) -> List[int]:
+        demoted = []
+        while self.applied < len(self.thresholds) and self.thresholds[self.applied] <= longest_after_call:
+            self.applied += 1
+            if self.resident:
+                layer = max(self.resident)
+                self.resident.remove(layer)
+                demoted.append(layer)
+                self.log.append((call_no, layer))
+        return demoted
+
+    def streamed(self) -> List[int]:
+        return [l for l in range(self.n_layers) if l not in self.resident]
