@@ -1,0 +1,195 @@
+/*
+ * stage.h -- C ABI of one pipeline stage of the offloading-based interleaved
+ * pipeline (arXiv 2512.21835), on one MI355X (gfx950) GPU.
+ *
+ * A stage is a contiguous block of LLaMA-style decoder layers (Section III-A:
+ * every device holds stages of consecutive layers and runs micro-batches
+ * through them in turn).  Some layers are *resident* in HBM; the others are
+ * *offloaded* to pinned host memory and streamed, layer by layer, into a few
+ * reusable HBM slots while resident layers compute (Section III-A: retained and
+ * offloaded layers per stage; Section III-B: weight memory is the retained
+ * layers plus one stage's worth of offloaded layers; Section III-C: a reusable
+ * loading buffer refilled once the GPU signals it has finished with it).
+ * Streaming changes where the weights are, never the arithmetic: outputs are
+ * bit-identical whichever layers are resident (lossless inference, abstract and
+ * Section IV-A).
+ *
+ * Conventions for every function:
+ *  - Return 0 (STAGE_OK) or a negative stage_status.  Nothing throws or aborts.
+ *  - All arguments are validated before any state changes; on an error the
+ *    handle is unchanged and still usable (except STAGE_EHIP, see below).
+ *  - STAGE_EHIP reports a failed HIP call, possibly an asynchronous error of
+ *    earlier work surfacing now; stage_last_error() gives the HIP message.
+ *  - A handle is not thread-safe: use it from one host thread at a time.
+ *  - Compute is enqueued on the compute stream and returns before it runs,
+ *    unless stated otherwise.  Device buffers passed in must stay valid until
+ *    the compute stream has passed the call (stage_sync or a stream sync).
+ *  - Matrices are row-major.  Weights are [out, in] (each output row is
+ *    contiguous).  bf16 is passed as its 16-bit pattern.
+ *  - Sequences are addressed by (micro-batch id mb, batch row b), 0 <= mb <
+ *    max_microbatches, 0 <= b < max_batch.  Each has its own KV cache and
+ *    positions; a sequence starts empty and its positions continue from its
+ *    current length.
+ */
+#ifndef PAPER_2512_21835_STAGE_H
+#define PAPER_2512_21835_STAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct stage stage; /* opaque; one per stage per GPU */
+
+typedef enum {
+    STAGE_OK = 0,
+    STAGE_EINVAL = -1, /* bad argument */
+    STAGE_ENOMEM = -2, /* HBM budget, device/pinned allocation or KV block pool exhausted */
+    STAGE_EHIP = -3,   /* a HIP runtime call failed */
+    STAGE_ESTATE = -4, /* not valid now (layer not loaded, sequence empty, ...) */
+    STAGE_ERANGE = -5  /* a sequence would exceed max_context */
+} stage_status;
+
+#define STAGE_MAX_THRESHOLDS 32
+#define STAGE_MAX_SEQS_PER_CALL 64
+
+/* Timing flags (stage_config.timing). */
+#define STAGE_TIME_CALLS 1   /* events around each prefill/decode call and each slot copy */
+#define STAGE_TIME_GATEUP 2  /* events around each gate/up projection kernel (the largest GEMV) */
+
+typedef struct {
+    /* Layer shape.  hidden, head_dim, ffn and n_q_heads*head_dim must be multiples of 8;
+       head_dim even and <= 256; n_q_heads a multiple of n_kv_heads. */
+    int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn;
+    float rope_theta; /* RoPE base; angle of pair i at position p is p * theta^(-2i/head_dim) */
+    float rms_eps;    /* RMSNorm epsilon, added to mean(x^2) inside the square root */
+    /* Sequence capacity.  max_microbatches * max_batch <= STAGE_MAX_SEQS_PER_CALL. */
+    int32_t max_microbatches, max_batch, max_context;
+    int32_t kv_block_tokens; /* tokens per KV block; must be 16 */
+    int32_t kv_pool_blocks;  /* blocks in the pool; 0 = every sequence can reach max_context */
+    int32_t kv_fp32;         /* KV element type: 0 = bf16 (rounded to nearest even), 1 = fp32 */
+    /* Weight memory: at most n_resident_max layers resident in HBM (the HBM weight budget, in
+       layers); every other layer streams through n_stream_slots reusable HBM slots. */
+    int32_t n_resident_max;
+    int32_t n_stream_slots;
+    /* Residency schedule (Section III-E, online memory-aware planner): before a prefill or
+       decode call, every threshold not yet applied that is <= the longest sequence length
+       the stage will hold after the call demotes one resident layer, highest id first.
+       Ascending; n_thresholds <= STAGE_MAX_THRESHOLDS. */
+    int32_t n_thresholds;
+    int32_t thresholds[STAGE_MAX_THRESHOLDS];
+    int32_t device;       /* HIP device ordinal */
+    void *compute_stream; /* hipStream_t for kernels; NULL = the library creates one */
+    void *copy_stream;    /* hipStream_t for slot copies; NULL = the library creates one */
+    int32_t timing;       /* STAGE_TIME_* flags; 0 = no events */
+} stage_config;
+
+/* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
+   the call.  wq [Hq*d, H], wk [Hkv*d, H], wv [Hkv*d, H], wo [H, Hq*d], wg [F, H], wu [F, H],
+   wd [H, F], g1 [H] (attention RMSNorm gain), g2 [H] (MLP RMSNorm gain). */
+typedef struct {
+    const void *wq, *wk, *wv, *wo, *wg, *wu, *wd, *g1, *g2;
+} stage_layer_weights;
+
+/* Fills *cfg with defaults: theta 10000, eps 1e-5, kv_block_tokens 16, n_stream_slots 2,
+   device 0, everything else zero. */
+void stage_config_default(stage_config *cfg);
+
+/* Creates a stage on cfg->device.  Allocates the KV pool, the block tables and the
+   RoPE tables in HBM.  No layer is loaded yet.
+   EINVAL: inconsistent shape or capacity; ENOMEM: the KV pool does not fit; EHIP. */
+int stage_init(const stage_config *cfg, stage **out);
+
+/* Frees everything the stage owns after waiting for its streams.  NULL is a no-op. */
+int stage_destroy(stage *s);
+
+/* Loads layer `layer` (0 <= layer < n_layers) and sets its residency (Section III-A:
+   retained vs offloaded layers).  w != NULL: copy the weights into library storage -- an HBM
+   blob if resident, a pinned host blob (hipHostMalloc) if not; the caller may free w on return
+   (the call synchronises its copies).  w == NULL: change the residency of an already loaded
+   layer (demotion copies the HBM blob to pinned host memory; promotion copies it back), which
+   is the planner's offload action (Section III-E).
+   EINVAL: bad layer; ENOMEM: more than n_resident_max resident layers, or allocation failed;
+   ESTATE: w == NULL for a layer never loaded. */
+int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int32_t resident);
+
+/* Prefill: runs T new tokens of each of B rows of each listed micro-batch through all layers.
+   x_in, x_out: device fp32 [n_mb][B][T][hidden] (x_out may not alias x_in).  Row r of x_out is
+   the hidden state after the stage's last layer (no final norm).  The k-th micro-batch of the
+   call is mb_ids[k] (distinct).  Streamed layers are loaded once per call, in ascending order,
+   and run for all rows of the call before their slot is reused (Section III-A: loading
+   overlapped with computation of other layers; the bursty pattern serves several micro-batches
+   per load).  KV blocks are taken in call order (mb_ids order, then b ascending).
+   EINVAL: bad ids/sizes or a layer not loaded; ERANGE: a sequence would exceed max_context;
+   ENOMEM: KV pool exhausted. */
+int stage_prefill(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, int32_t T,
+                  const float *x_in, float *x_out);
+
+/* Decode: one new token for each of B rows of each listed micro-batch; x_in, x_out: device
+   fp32 [n_mb][B][hidden].  Same rules as stage_prefill with T = 1.  Every listed sequence
+   must already hold at least one token (ESTATE otherwise). */
+int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                 float *x_out);
+
+/* Appends n_tokens positions of already-rotated K and V to sequence (mb, b) without compute:
+   the concatenation of a received KV-cache tail in the KV transfer protocol (Section III-E,
+   Alg. 2).  k, v: [n_layers][n_tokens][n_kv_heads][head_dim] in the KV element type (bf16 bits
+   or fp32), host or device memory; the call returns once they have been read.
+   ERANGE / ENOMEM as for prefill. */
+int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k,
+                    const void *v);
+
+/* Copies the stored K and V of the last n_tokens positions of sequence (mb, b) into k, v
+   (layout and type as stage_kv_append; host or device memory; synchronous), and if drop != 0
+   removes them from the sequence, returning emptied blocks to the pool: the tail a device ships
+   to its peer in Alg. 2 (Section III-E).  ESTATE: fewer than n_tokens stored. */
+int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void *k, void *v,
+                         int32_t drop);
+
+/* Forgets sequence (mb, b): its blocks return to the pool and its length becomes 0. */
+int stage_reset_sequence(stage *s, int32_t mb, int32_t b);
+
+/* Waits for the compute and copy streams; reports asynchronous HIP errors. */
+int stage_sync(stage *s);
+
+/* --- introspection (tests, metrics) --- */
+
+/* Block ids of sequence (mb, b) in position order (block j holds positions 16j..16j+15);
+   writes min(cap, count) ids, *n = count. */
+int stage_get_block_table(stage *s, int32_t mb, int32_t b, int32_t *blocks, int32_t cap,
+                          int32_t *n);
+
+/* Current length (tokens stored) of sequence (mb, b). */
+int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length);
+
+/* Residency of every layer: 1 resident, 0 streamed, -1 not loaded; out has n_layers entries. */
+int stage_get_residency(stage *s, int32_t *out);
+
+/* Slot log: one (call number, layer, slot) triple per streamed-layer load since init, in
+   load order; call numbers count prefill and decode calls from 0.  Writes min(cap, count)
+   triples (3*cap ints), *n = count. */
+int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
+
+/* Demotions made by the residency schedule: (call number, layer) pairs, like the slot log. */
+int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
+
+/* Timeline recorded under stage_config.timing, then cleared.  Synchronises.  Each record is
+   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel), layer (-1 for a call), start and
+   end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
+int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
+
+/* JSON object with counters: calls, tokens, layer loads, bytes streamed, HBM bytes in use. */
+int stage_get_stats(stage *s, char *buf, int32_t cap);
+
+/* Message of the last error on this handle ("" if none); valid until the next call. */
+const char *stage_last_error(stage *s);
+
+/* Static description of a status code. */
+const char *stage_strerror(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAPER_2512_21835_STAGE_H */

@@ -1,0 +1,246 @@
+// Causal grouped-query attention over the paged KV cache, fp32 arithmetic.
+//
+// One workgroup handles one (row, KV head, key split): the G = Hq/Hkv query heads that share the
+// KV head, over a range of keys.  Keys are walked in chunks of 64.  Inside a chunk, 128-bit loads
+// fetch one K row per D/8 lanes (a 16-token block of one head is 4 KiB contiguous in the pool);
+// the lanes of a key reduce their partial dot products with shuffles, scores go to LDS, one
+// wavefront per head takes the chunk maximum and exponentials (online softmax across chunks), and
+// the same lanes then accumulate P.V from V rows fetched the same way.
+//
+// Decode (split_keys > 0): the context is cut into splits of split_keys keys so that one token's
+// attention still fills the GPU; each split writes its unnormalised output with its max and sum,
+// and a combine pass merges the splits in ascending order.  Prefill (split_keys == 0): one split
+// per row spanning all of its keys writes the normalised output directly.
+#include "stage_kernels.h"
+
+namespace stg {
+namespace {
+
+constexpr int kChunk = 64;
+
+__device__ __forceinline__ float bf16lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+template <bool F32KV>
+__device__ __forceinline__ void load8(const void *pool, size_t elem, float f[8]) {
+    if (F32KV) {
+        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(pool) + elem);
+        const float4 a = p[0], b = p[1];
+        f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+        f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+    } else {
+        const uint4 v = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(pool) + elem);
+        f[0] = bf16lo(v.x); f[1] = bf16hi(v.x);
+        f[2] = bf16lo(v.y); f[3] = bf16hi(v.y);
+        f[4] = bf16lo(v.z); f[5] = bf16hi(v.z);
+        f[6] = bf16lo(v.w); f[7] = bf16hi(v.w);
+    }
+}
+
+template <int G, int D, bool F32KV>
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+    constexpr int LPK = D / 8;        // lanes per key row
+    constexpr int KPW = 64 / LPK;     // keys per wavefront per step
+    constexpr int KPS = 4 * KPW;      // keys per workgroup per step
+    static_assert(kChunk % KPS == 0, "chunk must be a multiple of keys per step");
+    const int split = blockIdx.x, g = blockIdx.y, row = blockIdx.z;
+    const int sidx = row / a.meta.rows_per_seq;
+    const int pos = a.meta.pos0[sidx] + row % a.meta.rows_per_seq;
+    const int slot = a.meta.seq_slot[sidx];
+    const int ctx = pos + 1;
+    const bool final_out = (a.split_keys == 0);
+    const int kbeg = final_out ? 0 : split * a.split_keys;
+    if (kbeg >= ctx) return;
+    const int kend = final_out ? ctx : min(ctx, kbeg + a.split_keys);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kl = lane / LPK;        // key slot of this lane within the wavefront step
+    const int sub = lane % LPK;
+    const int c0 = sub * 8;
+    const int hq_total = a.n_q_heads;
+    const size_t q_ld = (size_t)hq_total * D;
+    const int hkv = a.kv.n_kv_heads;
+    const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
+    const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
+
+    __shared__ float s_p[G][kChunk];
+    __shared__ float s_m[G], s_l[G], s_alpha[G];
+    __shared__ float s_o[4][G][D];
+
+    const float scale = 1.f / sqrtf((float)D);
+    float q[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const float *qp = a.q + row * q_ld + (size_t)(g * G + h) * D + c0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) q[h][j] = qp[j] * scale;
+    }
+    if (tid < G) { s_m[tid] = -INFINITY; s_l[tid] = 0.f; }
+    float o[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[h][j] = 0.f;
+    __syncthreads();
+
+    for (int kc = kbeg; kc < kend; kc += kChunk) {
+        const int n = min(kChunk, kend - kc);
+        // scores of this chunk
+        for (int base = 0; base < kChunk; base += KPS) {
+            const int kk = base + wave * KPW + kl;
+            float part[G];
+#pragma unroll
+            for (int h = 0; h < G; ++h) part[h] = 0.f;
+            if (kk < n) {
+                const int key = kc + kk;
+                const size_t e = (size_t)table[key / kBlockTokens] * blk_stride +
+                                 ((size_t)g * kBlockTokens + key % kBlockTokens) * D + c0;
+                float kf[8];
+                load8<F32KV>(a.kv.pool, e, kf);
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) part[h] = fmaf(q[h][j], kf[j], part[h]);
+            }
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int o2 = LPK / 2; o2 >= 1; o2 >>= 1) part[h] += __shfl_xor(part[h], o2, 64);
+            if (kk < n && sub == 0) {
+#pragma unroll
+                for (int h = 0; h < G; ++h) s_p[h][kk] = part[h];
+            }
+        }
+        __syncthreads();
+        // online softmax update, one wavefront per head
+        for (int h = wave; h < G; h += 4) {
+            const float sv = lane < n ? s_p[h][lane] : -INFINITY;
+            float mx = sv;
+#pragma unroll
+            for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
+            const float m_old = s_m[h];
+            const float m_new = fmaxf(m_old, mx);
+            const float p = lane < n ? expf(sv - m_new) : 0.f;
+            float sum = p;
+#pragma unroll
+            for (int o2 = 32; o2 >= 1; o2 >>= 1) sum += __shfl_xor(sum, o2, 64);
+            s_p[h][lane] = p;
+            if (lane == 0) {
+                const float alpha = expf(m_old - m_new);  // 0 on the first chunk (m_old = -inf)
+                s_alpha[h] = alpha;
+                s_l[h] = s_l[h] * alpha + sum;
+                s_m[h] = m_new;
+            }
+        }
+        __syncthreads();
+        // P.V
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float al = s_alpha[h];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) o[h][j] *= al;
+        }
+        for (int base = 0; base < kChunk; base += KPS) {
+            const int kk = base + wave * KPW + kl;
+            if (kk < n) {
+                const int key = kc + kk;
+                const size_t e = (size_t)table[key / kBlockTokens] * blk_stride +
+                                 ((size_t)(hkv + g) * kBlockTokens + key % kBlockTokens) * D + c0;
+                float vf[8];
+                load8<F32KV>(a.kv.pool, e, vf);
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    const float p = s_p[h][kk];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) o[h][j] = fmaf(p, vf[j], o[h][j]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // reduce the key slots: lanes with equal `sub` inside a wavefront, then across wavefronts
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int o2 = 32; o2 >= LPK; o2 >>= 1) o[h][j] += __shfl_xor(o[h][j], o2, 64);
+    if (kl == 0) {
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s_o[wave][h][c0 + j] = o[h][j];
+    }
+    __syncthreads();
+    for (int i = tid; i < G * D; i += 256) {
+        const int h = i / D, c = i % D;
+        const float v = ((s_o[0][h][c] + s_o[1][h][c]) + s_o[2][h][c]) + s_o[3][h][c];
+        const int hq = g * G + h;
+        if (final_out) {
+            a.out[row * q_ld + (size_t)hq * D + c] = v / s_l[h];
+        } else {
+            const size_t pi = ((size_t)row * hq_total + hq) * a.max_splits + split;
+            a.part_o[pi * D + c] = v;
+            if (c == 0) {
+                a.part_ml[pi * 2 + 0] = s_m[h];
+                a.part_ml[pi * 2 + 1] = s_l[h];
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a, int D) {
+    const int hq = blockIdx.x, row = blockIdx.y;
+    const int sidx = row / a.meta.rows_per_seq;
+    const int ctx = a.meta.pos0[sidx] + row % a.meta.rows_per_seq + 1;
+    const int nsp = (ctx + a.split_keys - 1) / a.split_keys;
+    const size_t pi0 = ((size_t)row * a.n_q_heads + hq) * a.max_splits;
+    float mx = -INFINITY;
+    for (int s = 0; s < nsp; ++s) mx = fmaxf(mx, a.part_ml[(pi0 + s) * 2]);
+    for (int c = threadIdx.x; c < D; c += blockDim.x) {
+        float num = 0.f, den = 0.f;
+        for (int s = 0; s < nsp; ++s) {
+            const float w = expf(a.part_ml[(pi0 + s) * 2] - mx);
+            den = fmaf(w, a.part_ml[(pi0 + s) * 2 + 1], den);
+            num = fmaf(w, a.part_o[(pi0 + s) * D + c], num);
+        }
+        a.out[(size_t)row * a.n_q_heads * D + (size_t)hq * D + c] = num / den;
+    }
+}
+
+template <int G, int D>
+hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
+    const int hkv = a.kv.n_kv_heads;
+    const int splits = a.split_keys == 0 ? 1 : a.grid_splits;
+    dim3 grid(splits, hkv, a.rows);
+    if (a.kv_fp32)
+        hipLaunchKernelGGL((attn_kernel<G, D, true>), grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((attn_kernel<G, D, false>), grid, dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.split_keys == 0) return e;
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_q_heads, a.rows), dim3(D < 256 ? D : 256), 0,
+                       st, a, D);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnArgs &a, hipStream_t st) {
+    if (a.rows <= 0) return hipSuccess;
+    const int G = a.n_q_heads / a.kv.n_kv_heads;
+    const int D = a.kv.head_dim;
+#define STG_ATTN_CASE(GG, DD) \
+    if (G == GG && D == DD) return launch_gd<GG, DD>(a, st);
+    STG_ATTN_CASE(1, 64) STG_ATTN_CASE(2, 64) STG_ATTN_CASE(4, 64) STG_ATTN_CASE(8, 64)
+    STG_ATTN_CASE(1, 128) STG_ATTN_CASE(2, 128) STG_ATTN_CASE(4, 128) STG_ATTN_CASE(8, 128)
+#undef STG_ATTN_CASE
+    return hipErrorInvalidValue;
+}
+
+bool attention_supported(int group, int head_dim) {
+    return (group == 1 || group == 2 || group == 4 || group == 8) && (head_dim == 64 || head_dim == 128);
+}
+
+}  // namespace stg

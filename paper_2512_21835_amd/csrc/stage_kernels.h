@@ -1,0 +1,101 @@
+// Internal interface between the stage runtime (stage_runtime.cpp) and the HIP kernels.
+// Not part of the public ABI (include/stage.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace stg {
+
+constexpr int kMaxSeqs = 64;     // sequences in one call
+constexpr int kBlockTokens = 16; // tokens per paged-KV block
+
+// Rows of a call: sequence k of the call owns rows [k*rows_per_seq, (k+1)*rows_per_seq);
+// its row t sits at position pos0[k] + t and its block table is row seq_slot[k].
+struct CallMeta {
+    int n_seqs;
+    int rows_per_seq;
+    int seq_slot[kMaxSeqs];
+    int pos0[kMaxSeqs];
+};
+
+// Paged KV pool of one layer: block b holds K then V, each [n_kv_heads][16][head_dim].
+struct KvView {
+    void *pool;              // element type: bf16 bits or fp32 (kv_fp32)
+    const int *block_table;  // [n_seq_slots][max_blocks]
+    int max_blocks;
+    int n_kv_heads;
+    int head_dim;
+};
+
+enum GemvMode {
+    GEMV_NORM_STORE = 0,     // out = W (rmsnorm(act) * gain)
+    GEMV_PLAIN_RESIDUAL = 1, // out = res + W act
+    GEMV_NORM_SWIGLU = 2     // out = silu(Wg y) * (Wu y), y = rmsnorm(act) * gain
+};
+
+struct GemvArgs {
+    const uint16_t *w;    // [N, K] bf16
+    const uint16_t *w2;   // second [N, K] matrix (SWIGLU: up projection)
+    const float *act;     // [rows, K] with row stride act_ld
+    const uint16_t *gain; // [K] bf16 (NORM modes)
+    const float *res;     // [rows, N] with row stride out_ld (RESIDUAL)
+    float *out;           // [rows, N] with row stride out_ld
+    long act_ld, out_ld;
+    int N, K;
+    int rows;  // rows in this launch
+    float eps;
+};
+
+// y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).
+hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st);
+
+struct RopeKvArgs {
+    const float *qkv;  // [rows, (Hq + 2 Hkv) d]: q heads, then k heads, then v heads
+    float *q_out;      // [rows, Hq d] rotated queries
+    const float *cos_t, *sin_t;  // [max_context, d/2]
+    KvView kv;
+    int n_q_heads;
+    int kv_fp32;
+    int rows;
+    CallMeta meta;
+};
+hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st);
+
+struct AttnArgs {
+    const float *q;      // [rows, Hq d] rotated
+    float *out;          // [rows, Hq d]
+    float *part_o;       // [rows, Hq, max_splits, d] unnormalised partial outputs
+    float *part_ml;      // [rows, Hq, max_splits, 2] partial max and sum
+    KvView kv;
+    int n_q_heads;
+    int kv_fp32;
+    int rows;
+    int split_keys;      // keys per split; 0 = one split per row (final output directly)
+    int max_splits;      // stride of the partial buffers
+    int grid_splits;     // splits launched: ceil(longest context in the call / split_keys)
+    CallMeta meta;
+};
+hipError_t launch_attention(const AttnArgs &a, hipStream_t st);
+bool attention_supported(int group, int head_dim);
+
+// Writes table[idx[i]] = val[i] for i < n (any n; chunked).
+hipError_t launch_table_write(int *table, const int *idx, const int *val, int n, hipStream_t st);
+
+// Moves K/V between a dense buffer [n_layers][n][Hkv][d] and positions pos0..pos0+n-1 of the
+// sequence whose block table row is `slot`.  to_pool: dense -> pool, else pool -> dense.
+struct KvCopyArgs {
+    void *pool_base;        // layer 0 pool; layer l at pool_base + l * layer_stride bytes
+    size_t layer_stride;
+    const int *block_table;
+    int max_blocks;
+    int n_kv_heads, head_dim, kv_fp32;
+    int n_layers;
+    int slot, pos0, n;
+    void *k, *v;            // dense device buffers
+    int to_pool;
+};
+hipError_t launch_kv_copy(const KvCopyArgs &a, hipStream_t st);
+
+}  // namespace stg

@@ -1,0 +1,972 @@
+// Stage runtime: memory plan, paged KV allocation, weight streaming through reusable HBM slots,
+// residency schedule and the per-layer launch sequence.  Implements include/stage.h.
+//
+// Memory plan (one stage, one GPU):
+//   * every layer is one blob of bf16 tensors at 256-byte aligned offsets:
+//       Wqkv [(Hq + 2 Hkv) d, H] (q rows, then k rows, then v rows) | Wo [H, Hq d] |
+//       Wg [F, H] | Wu [F, H] | Wd [H, F] | g1 [H] | g2 [H]
+//     so a loaded layer is described once by fixed offsets (the paper's proxy modules,
+//     Section III-C: structure bound once, later loads only refill the bytes);
+//   * resident layers own an HBM blob; offloaded layers own a pinned host blob (hipHostMalloc)
+//     and are copied into one of n_stream_slots HBM slots when a call needs them;
+//   * the KV cache is one pool of 16-token blocks per layer, [block][K|V][Hkv][16][d], shared by
+//     all sequences through per-sequence block tables (one table row per sequence, the same block
+//     ids in every layer);
+//   * RoPE cos/sin tables [max_context][d/2] (fp32, computed in double on the host).
+//
+// Streaming (Section III-A/III-C): in each call the offloaded layers are loaded once, in
+// ascending order; load k of the stage's life goes to slot k mod S.  The copy stream waits on
+// the slot's "free" event (recorded by the compute stream after the last kernel that read the
+// slot's previous layer), copies the blob and records "ready"; the compute stream waits on
+// "ready" before the layer's first kernel.  With S slots the next S-1 loads proceed while a
+// layer computes, and the first loads of a call overlap the call's resident layers.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "stage.h"
+#include "stage_kernels.h"
+
+using namespace stg;
+
+namespace {
+
+constexpr int kDecodeSplitKeys = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layer {
+    int state = -1;       // -1 not loaded, 0 offloaded (pinned host blob), 1 resident (HBM blob)
+    void *dev = nullptr;  // HBM blob when resident
+    void *host = nullptr; // pinned host blob when offloaded
+};
+
+struct TimeRec {
+    int kind, layer;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct stage {
+    stage_config cfg{};
+    int H = 0, Hq = 0, Hkv = 0, D = 0, F = 0, L = 0;
+    int qkv_rows = 0;
+    hipStream_t cs = nullptr, xs = nullptr;
+    bool own_cs = false, own_xs = false;
+
+    size_t off_wqkv = 0, off_wo = 0, off_wg = 0, off_wu = 0, off_wd = 0, off_g1 = 0, off_g2 = 0;
+    size_t blob_bytes = 0;
+    std::vector<Layer> layers;
+
+    std::vector<void *> slots;
+    std::vector<hipEvent_t> slot_ready, slot_free;
+    long long loads = 0, calls = 0;
+    std::vector<int> slot_log, demotion_log;
+    int thresholds_applied = 0;
+
+    void *kv_pool = nullptr;
+    size_t kv_block_bytes = 0, kv_layer_stride = 0;
+    int n_blocks = 0, max_blocks = 0, n_seq_slots = 0;
+    int *d_table = nullptr;
+    std::vector<std::vector<int>> tables;
+    std::vector<int> lengths;
+    std::priority_queue<int, std::vector<int>, std::greater<int>> free_blocks;
+
+    float *d_cos = nullptr, *d_sin = nullptr;
+
+    size_t ws_rows = 0;
+    float *ws_qkv = nullptr, *ws_q = nullptr, *ws_attn = nullptr, *ws_h = nullptr;
+    size_t part_rows = 0;
+    int max_splits = 0;
+    float *ws_part_o = nullptr, *ws_part_ml = nullptr;
+    void *ws_dense = nullptr;
+    size_t ws_dense_bytes = 0;
+
+    std::vector<TimeRec> recs;
+    std::vector<hipEvent_t> ev_pool;
+
+    long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
+    std::string err;
+
+    int fail(int code, const char *fmt, ...) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        err = buf;
+        return code;
+    }
+    int fail_hip(hipError_t e, const char *what) {
+        return fail(STAGE_EHIP, "%s: %s", what, hipGetErrorString(e));
+    }
+};
+
+#define HIP_TRY(expr)                                              \
+    do {                                                           \
+        hipError_t e_ = (expr);                                    \
+        if (e_ != hipSuccess) return s->fail_hip(e_, #expr);       \
+    } while (0)
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) (void)hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+bool is_device_ptr(const void *p) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return attr.type == hipMemoryTypeDevice;
+}
+
+int seq_slot(const stage *s, int mb, int b) { return mb * s->cfg.max_batch + b; }
+
+hipEvent_t pooled_event(stage *s) {
+    if (!s->ev_pool.empty()) {
+        hipEvent_t e = s->ev_pool.back();
+        s->ev_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+int sync_all(stage *s) {
+    HIP_TRY(hipStreamSynchronize(s->cs));
+    HIP_TRY(hipStreamSynchronize(s->xs));
+    return STAGE_OK;
+}
+
+int ensure_slots(stage *s) {
+    if (!s->slots.empty()) return STAGE_OK;
+    const int S = s->cfg.n_stream_slots;
+    if (S < 1) return s->fail(STAGE_EINVAL, "a layer is offloaded but n_stream_slots is 0");
+    std::vector<void *> sl(S, nullptr);
+    std::vector<hipEvent_t> rd(S, nullptr), fr(S, nullptr);
+    for (int i = 0; i < S; ++i) {
+        if (hipMalloc(&sl[i], s->blob_bytes) != hipSuccess ||
+            hipEventCreateWithFlags(&rd[i], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&fr[i], hipEventDisableTiming) != hipSuccess) {
+            (void)hipGetLastError();
+            for (int j = 0; j <= i; ++j) {
+                if (sl[j]) (void)hipFree(sl[j]);
+                if (rd[j]) (void)hipEventDestroy(rd[j]);
+                if (fr[j]) (void)hipEventDestroy(fr[j]);
+            }
+            return s->fail(STAGE_ENOMEM, "cannot allocate %d stream slots of %zu bytes", S, s->blob_bytes);
+        }
+    }
+    s->slots = sl;
+    s->slot_ready = rd;
+    s->slot_free = fr;
+    return STAGE_OK;
+}
+
+int n_resident(const stage *s) {
+    int n = 0;
+    for (const Layer &l : s->layers) n += (l.state == 1);
+    return n;
+}
+
+// Moves a loaded layer between HBM and pinned host memory (the planner's offload action).
+int set_residency(stage *s, int layer, int resident) {
+    Layer &ly = s->layers[layer];
+    if (ly.state == resident) return STAGE_OK;
+    if (resident) {
+        if (n_resident(s) + 1 > s->cfg.n_resident_max)
+            return s->fail(STAGE_ENOMEM, "HBM weight budget of %d resident layers reached", s->cfg.n_resident_max);
+        void *dev = nullptr;
+        if (hipMalloc(&dev, s->blob_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+        }
+        int rc = sync_all(s);
+        if (rc) { (void)hipFree(dev); return rc; }
+        HIP_TRY(hipMemcpy(dev, ly.host, s->blob_bytes, hipMemcpyHostToDevice));
+        HIP_TRY(hipHostFree(ly.host));
+        ly.host = nullptr;
+        ly.dev = dev;
+        ly.state = 1;
+    } else {
+        int rc = ensure_slots(s);
+        if (rc) return rc;
+        void *host = nullptr;
+        if (hipHostMalloc(&host, s->blob_bytes, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+        }
+        rc = sync_all(s);
+        if (rc) { (void)hipHostFree(host); return rc; }
+        HIP_TRY(hipMemcpy(host, ly.dev, s->blob_bytes, hipMemcpyDeviceToHost));
+        HIP_TRY(hipFree(ly.dev));
+        ly.dev = nullptr;
+        ly.host = host;
+        ly.state = 0;
+    }
+    return STAGE_OK;
+}
+
+int ensure_workspace(stage *s, size_t rows, bool decode) {
+    const size_t need_part = decode ? rows : 0;
+    if (rows <= s->ws_rows && need_part <= s->part_rows) return STAGE_OK;
+    int rc = sync_all(s);
+    if (rc) return rc;
+    if (rows > s->ws_rows) {
+        for (float *p : {s->ws_qkv, s->ws_q, s->ws_attn, s->ws_h})
+            if (p) (void)hipFree(p);
+        s->ws_qkv = s->ws_q = s->ws_attn = s->ws_h = nullptr;
+        s->ws_rows = 0;
+        const size_t qd = (size_t)s->Hq * s->D;
+        if (hipMalloc(&s->ws_qkv, rows * s->qkv_rows * sizeof(float)) != hipSuccess ||
+            hipMalloc(&s->ws_q, rows * qd * sizeof(float)) != hipSuccess ||
+            hipMalloc(&s->ws_attn, rows * qd * sizeof(float)) != hipSuccess ||
+            hipMalloc(&s->ws_h, rows * (size_t)s->F * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "workspace for %zu rows does not fit", rows);
+        }
+        s->ws_rows = rows;
+    }
+    if (need_part > s->part_rows) {
+        if (s->ws_part_o) (void)hipFree(s->ws_part_o);
+        if (s->ws_part_ml) (void)hipFree(s->ws_part_ml);
+        s->ws_part_o = s->ws_part_ml = nullptr;
+        s->part_rows = 0;
+        const size_t n = need_part * s->Hq * (size_t)s->max_splits;
+        if (hipMalloc(&s->ws_part_o, n * s->D * sizeof(float)) != hipSuccess ||
+            hipMalloc(&s->ws_part_ml, n * 2 * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "attention partials for %zu rows do not fit", need_part);
+        }
+        s->part_rows = need_part;
+    }
+    return STAGE_OK;
+}
+
+int ensure_dense(stage *s, size_t bytes) {
+    if (bytes <= s->ws_dense_bytes) return STAGE_OK;
+    int rc = sync_all(s);
+    if (rc) return rc;
+    if (s->ws_dense) (void)hipFree(s->ws_dense);
+    s->ws_dense = nullptr;
+    s->ws_dense_bytes = 0;
+    if (hipMalloc(&s->ws_dense, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return s->fail(STAGE_ENOMEM, "staging buffer of %zu bytes does not fit", bytes);
+    }
+    s->ws_dense_bytes = bytes;
+    return STAGE_OK;
+}
+
+KvView kv_view(stage *s, int layer) {
+    KvView v;
+    v.pool = static_cast<char *>(s->kv_pool) + (size_t)layer * s->kv_layer_stride;
+    v.block_table = s->d_table;
+    v.max_blocks = s->max_blocks;
+    v.n_kv_heads = s->Hkv;
+    v.head_dim = s->D;
+    return v;
+}
+
+// Blocks a sequence of current length `len` needs to hold `n` more tokens.
+int blocks_needed(const stage *s, int slot, int n) {
+    const int len = s->lengths[slot];
+    const int have = (int)s->tables[slot].size();
+    const int want = (len + n + kBlockTokens - 1) / kBlockTokens;
+    return want - have;
+}
+
+// Takes blocks (lowest free id first) for the listed sequences in order and mirrors the new
+// table entries on the device.  The caller has checked that the pool suffices.
+int allocate_blocks(stage *s, const std::vector<int> &slots, int n) {
+    std::vector<int> idx, val;
+    for (int slot : slots) {
+        const int need = blocks_needed(s, slot, n);
+        for (int i = 0; i < need; ++i) {
+            const int blk = s->free_blocks.top();
+            s->free_blocks.pop();
+            idx.push_back(slot * s->max_blocks + (int)s->tables[slot].size());
+            val.push_back(blk);
+            s->tables[slot].push_back(blk);
+        }
+    }
+    if (!idx.empty()) HIP_TRY(launch_table_write(s->d_table, idx.data(), val.data(), (int)idx.size(), s->cs));
+    return STAGE_OK;
+}
+
+void release_tail_blocks(stage *s, int slot) {
+    const int keep = (s->lengths[slot] + kBlockTokens - 1) / kBlockTokens;
+    std::vector<int> &t = s->tables[slot];
+    while ((int)t.size() > keep) {
+        s->free_blocks.push(t.back());
+        t.pop_back();
+    }
+}
+
+int record_event(stage *s, hipStream_t st, hipEvent_t *out) {
+    hipEvent_t e = pooled_event(s);
+    if (!e) return s->fail(STAGE_EHIP, "hipEventCreate failed");
+    HIP_TRY(hipEventRecord(e, st));
+    *out = e;
+    return STAGE_OK;
+}
+
+int enqueue_copy(stage *s, int layer, int slot) {
+    TimeRec rec{1, layer, nullptr, nullptr};
+    HIP_TRY(hipStreamWaitEvent(s->xs, s->slot_free[slot], 0));
+    if (s->cfg.timing & STAGE_TIME_CALLS) {
+        int rc = record_event(s, s->xs, &rec.a);
+        if (rc) return rc;
+    }
+    HIP_TRY(hipMemcpyAsync(s->slots[slot], s->layers[layer].host, s->blob_bytes, hipMemcpyHostToDevice, s->xs));
+    HIP_TRY(hipEventRecord(s->slot_ready[slot], s->xs));
+    if (s->cfg.timing & STAGE_TIME_CALLS) {
+        int rc = record_event(s, s->xs, &rec.b);
+        if (rc) return rc;
+        s->recs.push_back(rec);
+    }
+    s->bytes_streamed += (long long)s->blob_bytes;
+    return STAGE_OK;
+}
+
+int run_layer(stage *s, int layer, const void *blob, int rows, int T, const CallMeta &meta,
+              int grid_splits, const float *x_src, float *x_dst) {
+    const uint16_t *base = static_cast<const uint16_t *>(blob);
+    const size_t qd = (size_t)s->Hq * s->D;
+
+    GemvArgs q{};
+    q.w = base + s->off_wqkv / 2;
+    q.act = x_src;
+    q.act_ld = s->H;
+    q.gain = base + s->off_g1 / 2;
+    q.out = s->ws_qkv;
+    q.out_ld = s->qkv_rows;
+    q.N = s->qkv_rows;
+    q.K = s->H;
+    q.rows = rows;
+    q.eps = s->cfg.rms_eps;
+    HIP_TRY(launch_gemv(GEMV_NORM_STORE, q, s->cs));
+
+    RopeKvArgs r{};
+    r.qkv = s->ws_qkv;
+    r.q_out = s->ws_q;
+    r.cos_t = s->d_cos;
+    r.sin_t = s->d_sin;
+    r.kv = kv_view(s, layer);
+    r.n_q_heads = s->Hq;
+    r.kv_fp32 = s->cfg.kv_fp32;
+    r.rows = rows;
+    r.meta = meta;
+    HIP_TRY(launch_rope_kv_store(r, s->cs));
+
+    AttnArgs at{};
+    at.q = s->ws_q;
+    at.out = s->ws_attn;
+    at.part_o = s->ws_part_o;
+    at.part_ml = s->ws_part_ml;
+    at.kv = kv_view(s, layer);
+    at.n_q_heads = s->Hq;
+    at.kv_fp32 = s->cfg.kv_fp32;
+    at.rows = rows;
+    at.split_keys = (T == 1) ? kDecodeSplitKeys : 0;
+    at.max_splits = s->max_splits;
+    at.grid_splits = grid_splits;
+    at.meta = meta;
+    HIP_TRY(launch_attention(at, s->cs));
+
+    GemvArgs o{};
+    o.w = base + s->off_wo / 2;
+    o.act = s->ws_attn;
+    o.act_ld = (long)qd;
+    o.res = x_src;
+    o.out = x_dst;
+    o.out_ld = s->H;
+    o.N = s->H;
+    o.K = (int)qd;
+    o.rows = rows;
+    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
+
+    GemvArgs gu{};
+    gu.w = base + s->off_wg / 2;
+    gu.w2 = base + s->off_wu / 2;
+    gu.act = x_dst;
+    gu.act_ld = s->H;
+    gu.gain = base + s->off_g2 / 2;
+    gu.out = s->ws_h;
+    gu.out_ld = s->F;
+    gu.N = s->F;
+    gu.K = s->H;
+    gu.rows = rows;
+    gu.eps = s->cfg.rms_eps;
+    TimeRec rec{2, layer, nullptr, nullptr};
+    const bool t_gu = (s->cfg.timing & STAGE_TIME_GATEUP) != 0;
+    if (t_gu) {
+        int rc = record_event(s, s->cs, &rec.a);
+        if (rc) return rc;
+    }
+    HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs));
+    if (t_gu) {
+        int rc = record_event(s, s->cs, &rec.b);
+        if (rc) return rc;
+        s->recs.push_back(rec);
+    }
+
+    GemvArgs dn{};
+    dn.w = base + s->off_wd / 2;
+    dn.act = s->ws_h;
+    dn.act_ld = s->F;
+    dn.res = x_dst;
+    dn.out = x_dst;
+    dn.out_ld = s->H;
+    dn.N = s->H;
+    dn.K = s->F;
+    dn.rows = rows;
+    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
+    return STAGE_OK;
+}
+
+// Shared body of prefill and decode.
+int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
+             bool decode) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    const stage_config &c = s->cfg;
+    if (n_mb < 1 || n_mb > c.max_microbatches || !mb_ids || B < 1 || B > c.max_batch || T < 1 ||
+        !x_in || !x_out)
+        return s->fail(STAGE_EINVAL, "bad call arguments (n_mb=%d B=%d T=%d)", n_mb, B, T);
+    std::vector<int> slots;
+    std::vector<char> seen(c.max_microbatches, 0);
+    for (int k = 0; k < n_mb; ++k) {
+        const int mb = mb_ids[k];
+        if (mb < 0 || mb >= c.max_microbatches || seen[mb])
+            return s->fail(STAGE_EINVAL, "micro-batch id %d out of range or repeated", mb);
+        seen[mb] = 1;
+        for (int b = 0; b < B; ++b) slots.push_back(seq_slot(s, mb, b));
+    }
+    for (int l = 0; l < s->L; ++l)
+        if (s->layers[l].state < 0) return s->fail(STAGE_EINVAL, "layer %d is not loaded", l);
+    int longest = 0;
+    for (int len : s->lengths) longest = std::max(longest, len);
+    int need_blocks = 0;
+    for (int sl : slots) {
+        if (decode && s->lengths[sl] < 1)
+            return s->fail(STAGE_ESTATE, "decode on an empty sequence (slot %d)", sl);
+        if (s->lengths[sl] + T > c.max_context)
+            return s->fail(STAGE_ERANGE, "sequence would exceed max_context %d", c.max_context);
+        need_blocks += blocks_needed(s, sl, T);
+        longest = std::max(longest, s->lengths[sl] + T);
+    }
+    if (need_blocks > (int)s->free_blocks.size())
+        return s->fail(STAGE_ENOMEM, "KV pool exhausted (%d blocks needed, %d free)", need_blocks,
+                       (int)s->free_blocks.size());
+    const size_t rows = (size_t)slots.size() * T;
+    DeviceGuard dg(c.device);
+    int rc = ensure_workspace(s, rows, decode);
+    if (rc) return rc;
+
+    const long long call_no = s->calls;
+    // residency schedule: thresholds reached by this call demote resident layers, highest first
+    while (s->thresholds_applied < c.n_thresholds && c.thresholds[s->thresholds_applied] <= longest) {
+        s->thresholds_applied++;
+        int victim = -1;
+        for (int l = s->L - 1; l >= 0; --l)
+            if (s->layers[l].state == 1) { victim = l; break; }
+        if (victim < 0) continue;
+        rc = set_residency(s, victim, 0);
+        if (rc) return rc;
+        s->demotion_log.push_back((int)call_no);
+        s->demotion_log.push_back(victim);
+    }
+
+    rc = allocate_blocks(s, slots, T);
+    if (rc) return rc;
+    CallMeta meta{};
+    meta.n_seqs = (int)slots.size();
+    meta.rows_per_seq = T;
+    int max_ctx = 0;
+    for (size_t i = 0; i < slots.size(); ++i) {
+        meta.seq_slot[i] = slots[i];
+        meta.pos0[i] = s->lengths[slots[i]];
+        s->lengths[slots[i]] += T;
+        max_ctx = std::max(max_ctx, s->lengths[slots[i]]);
+    }
+    const int grid_splits = (max_ctx + kDecodeSplitKeys - 1) / kDecodeSplitKeys;
+    s->calls++;
+    if (decode) s->tok_decode += (long long)rows; else s->tok_prefill += (long long)rows;
+
+    TimeRec call_rec{0, -1, nullptr, nullptr};
+    if (c.timing & STAGE_TIME_CALLS) {
+        rc = record_event(s, s->cs, &call_rec.a);
+        if (rc) return rc;
+    }
+
+    // streamed layers of this call, ascending; load j -> slot (loads + j) mod S
+    std::vector<int> streamed;
+    for (int l = 0; l < s->L; ++l)
+        if (s->layers[l].state == 0) streamed.push_back(l);
+    const int S = c.n_stream_slots;
+    const long long load0 = s->loads;
+    auto slot_of = [&](int j) { return (int)((load0 + j) % S); };
+    const int n_str = (int)streamed.size();
+    for (int j = 0; j < n_str; ++j) {
+        s->slot_log.push_back((int)call_no);
+        s->slot_log.push_back(streamed[j]);
+        s->slot_log.push_back(slot_of(j));
+    }
+    s->loads += n_str;
+    for (int j = 0; j < std::min(S, n_str); ++j) {
+        rc = enqueue_copy(s, streamed[j], slot_of(j));
+        if (rc) return rc;
+    }
+
+    int j = 0;
+    for (int l = 0; l < s->L; ++l) {
+        const float *src = (l == 0) ? x_in : x_out;
+        const Layer &ly = s->layers[l];
+        if (ly.state == 1) {
+            rc = run_layer(s, l, ly.dev, (int)rows, T, meta, grid_splits, src, x_out);
+            if (rc) return rc;
+            continue;
+        }
+        const int sl = slot_of(j);
+        HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[sl], 0));
+        rc = run_layer(s, l, s->slots[sl], (int)rows, T, meta, grid_splits, src, x_out);
+        if (rc) return rc;
+        HIP_TRY(hipEventRecord(s->slot_free[sl], s->cs));
+        if (j + S < n_str) {
+            rc = enqueue_copy(s, streamed[j + S], slot_of(j + S));
+            if (rc) return rc;
+        }
+        ++j;
+    }
+    if (c.timing & STAGE_TIME_CALLS) {
+        rc = record_event(s, s->cs, &call_rec.b);
+        if (rc) return rc;
+        s->recs.push_back(call_rec);
+    }
+    return STAGE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void stage_config_default(stage_config *cfg) {
+    if (!cfg) return;
+    std::memset(cfg, 0, sizeof *cfg);
+    cfg->rope_theta = 10000.f;
+    cfg->rms_eps = 1e-5f;
+    cfg->kv_block_tokens = kBlockTokens;
+    cfg->n_stream_slots = 2;
+}
+
+const char *stage_strerror(int32_t status) {
+    switch (status) {
+        case STAGE_OK: return "ok";
+        case STAGE_EINVAL: return "invalid argument";
+        case STAGE_ENOMEM: return "out of memory (HBM budget, allocation or KV pool)";
+        case STAGE_EHIP: return "HIP runtime error";
+        case STAGE_ESTATE: return "invalid state for this call";
+        case STAGE_ERANGE: return "sequence would exceed max_context";
+        default: return "unknown status";
+    }
+}
+
+const char *stage_last_error(stage *s) { return s ? s->err.c_str() : "null stage handle"; }
+
+int stage_init(const stage_config *cfg, stage **out) {
+    if (!cfg || !out) return STAGE_EINVAL;
+    *out = nullptr;
+    const stage_config &c = *cfg;
+    const bool shape_ok = c.n_layers >= 1 && c.hidden >= 8 && c.hidden % 8 == 0 && c.n_q_heads >= 1 &&
+                          c.n_kv_heads >= 1 && c.n_q_heads % c.n_kv_heads == 0 && c.head_dim >= 8 &&
+                          c.head_dim % 8 == 0 && c.head_dim <= 256 && c.ffn >= 8 && c.ffn % 8 == 0 &&
+                          attention_supported(c.n_q_heads / c.n_kv_heads, c.head_dim) &&
+                          c.rope_theta > 0.f && c.rms_eps >= 0.f;
+    const bool cap_ok = c.max_microbatches >= 1 && c.max_batch >= 1 &&
+                        (long)c.max_microbatches * c.max_batch <= kMaxSeqs && c.max_context >= 1 &&
+                        c.kv_block_tokens == kBlockTokens && c.kv_pool_blocks >= 0 &&
+                        (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
+                        c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
+                        c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
+                        (c.timing & ~(STAGE_TIME_CALLS | STAGE_TIME_GATEUP)) == 0;
+    if (!shape_ok || !cap_ok) return STAGE_EINVAL;
+    for (int i = 0; i < c.n_thresholds; ++i)
+        if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || c.device < 0 || c.device >= ndev) {
+        (void)hipGetLastError();
+        return STAGE_EINVAL;
+    }
+    DeviceGuard dg(c.device);
+
+    stage *s = new stage();
+    s->cfg = c;
+    s->L = c.n_layers; s->H = c.hidden; s->Hq = c.n_q_heads; s->Hkv = c.n_kv_heads;
+    s->D = c.head_dim; s->F = c.ffn;
+    s->qkv_rows = (s->Hq + 2 * s->Hkv) * s->D;
+    const size_t H = s->H, F = s->F, qd = (size_t)s->Hq * s->D;
+    size_t off = 0;
+    s->off_wqkv = off; off = align256(off + (size_t)s->qkv_rows * H * 2);
+    s->off_wo = off;   off = align256(off + H * qd * 2);
+    s->off_wg = off;   off = align256(off + F * H * 2);
+    s->off_wu = off;   off = align256(off + F * H * 2);
+    s->off_wd = off;   off = align256(off + H * F * 2);
+    s->off_g1 = off;   off = align256(off + H * 2);
+    s->off_g2 = off;   off = align256(off + H * 2);
+    s->blob_bytes = off;
+    s->layers.assign(s->L, Layer());
+
+    s->n_seq_slots = c.max_microbatches * c.max_batch;
+    s->max_blocks = (c.max_context + kBlockTokens - 1) / kBlockTokens;
+    s->n_blocks = c.kv_pool_blocks > 0 ? c.kv_pool_blocks : s->n_seq_slots * s->max_blocks;
+    s->kv_block_bytes = (size_t)2 * s->Hkv * kBlockTokens * s->D * (c.kv_fp32 ? 4 : 2);
+    s->kv_layer_stride = align256(s->kv_block_bytes * s->n_blocks);
+    s->max_splits = (c.max_context + kDecodeSplitKeys - 1) / kDecodeSplitKeys;
+    s->tables.assign(s->n_seq_slots, {});
+    s->lengths.assign(s->n_seq_slots, 0);
+    for (int b = 0; b < s->n_blocks; ++b) s->free_blocks.push(b);
+
+    auto cleanup = [&](int code) {
+        stage_destroy(s);
+        return code;
+    };
+    if (c.compute_stream) s->cs = static_cast<hipStream_t>(c.compute_stream);
+    else if (hipStreamCreateWithFlags(&s->cs, hipStreamNonBlocking) == hipSuccess) s->own_cs = true;
+    else return cleanup(STAGE_EHIP);
+    if (c.copy_stream) s->xs = static_cast<hipStream_t>(c.copy_stream);
+    else if (hipStreamCreateWithFlags(&s->xs, hipStreamNonBlocking) == hipSuccess) s->own_xs = true;
+    else return cleanup(STAGE_EHIP);
+
+    if (hipMalloc(&s->kv_pool, s->kv_layer_stride * s->L) != hipSuccess ||
+        hipMalloc(&s->d_table, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
+        hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
+        hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess) {
+        (void)hipGetLastError();
+        return cleanup(STAGE_ENOMEM);
+    }
+    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
+        return cleanup(STAGE_EHIP);
+    // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
+    const int half = s->D / 2;
+    std::vector<float> ct((size_t)c.max_context * half), st((size_t)c.max_context * half);
+    for (int p = 0; p < c.max_context; ++p)
+        for (int i = 0; i < half; ++i) {
+            const double ang = (double)p * std::pow((double)c.rope_theta, -2.0 * i / s->D);
+            ct[(size_t)p * half + i] = (float)std::cos(ang);
+            st[(size_t)p * half + i] = (float)std::sin(ang);
+        }
+    if (hipMemcpy(s->d_cos, ct.data(), ct.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(s->d_sin, st.data(), st.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess)
+        return cleanup(STAGE_EHIP);
+    *out = s;
+    return STAGE_OK;
+}
+
+int stage_destroy(stage *s) {
+    if (!s) return STAGE_OK;
+    DeviceGuard dg(s->cfg.device);
+    if (s->cs) (void)hipStreamSynchronize(s->cs);
+    if (s->xs) (void)hipStreamSynchronize(s->xs);
+    for (Layer &l : s->layers) {
+        if (l.dev) (void)hipFree(l.dev);
+        if (l.host) (void)hipHostFree(l.host);
+    }
+    for (void *p : s->slots) (void)hipFree(p);
+    for (hipEvent_t e : s->slot_ready) (void)hipEventDestroy(e);
+    for (hipEvent_t e : s->slot_free) (void)hipEventDestroy(e);
+    for (TimeRec &r : s->recs) {
+        if (r.a) (void)hipEventDestroy(r.a);
+        if (r.b) (void)hipEventDestroy(r.b);
+    }
+    for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_cos, (void *)s->d_sin,
+                    (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
+                    (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
+        if (p) (void)hipFree(p);
+    if (s->own_cs && s->cs) (void)hipStreamDestroy(s->cs);
+    if (s->own_xs && s->xs) (void)hipStreamDestroy(s->xs);
+    delete s;
+    return STAGE_OK;
+}
+
+int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int32_t resident) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (layer < 0 || layer >= s->L || (resident != 0 && resident != 1))
+        return s->fail(STAGE_EINVAL, "bad layer %d or residency %d", layer, resident);
+    DeviceGuard dg(s->cfg.device);
+    Layer &ly = s->layers[layer];
+    if (!w) {
+        if (ly.state < 0) return s->fail(STAGE_ESTATE, "layer %d was never loaded", layer);
+        return set_residency(s, layer, resident);
+    }
+    const void *src[9] = {w->wq, w->wk, w->wv, w->wo, w->wg, w->wu, w->wd, w->g1, w->g2};
+    for (const void *p : src)
+        if (!p) return s->fail(STAGE_EINVAL, "null weight pointer");
+    if (resident && ly.state != 1 && n_resident(s) + 1 > s->cfg.n_resident_max)
+        return s->fail(STAGE_ENOMEM, "HBM weight budget of %d resident layers reached", s->cfg.n_resident_max);
+    if (!resident) {
+        int rc = ensure_slots(s);
+        if (rc) return rc;
+    }
+    void *dst = nullptr;
+    if (resident) {
+        if (hipMalloc(&dst, s->blob_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+        }
+    } else if (hipHostMalloc(&dst, s->blob_bytes, hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+    }
+    int rc = sync_all(s);
+    if (rc) return rc;
+    const size_t H = s->H, F = s->F, qd = (size_t)s->Hq * s->D, kvd = (size_t)s->Hkv * s->D;
+    const size_t offs[9] = {s->off_wqkv, s->off_wqkv + qd * H * 2, s->off_wqkv + (qd + kvd) * H * 2,
+                            s->off_wo, s->off_wg, s->off_wu, s->off_wd, s->off_g1, s->off_g2};
+    const size_t bytes[9] = {qd * H * 2, kvd * H * 2, kvd * H * 2, H * qd * 2, F * H * 2,
+                             F * H * 2, H * F * 2, H * 2, H * 2};
+    for (int i = 0; i < 9; ++i) {
+        hipError_t e = hipMemcpy(static_cast<char *>(dst) + offs[i], src[i], bytes[i], hipMemcpyDefault);
+        if (e != hipSuccess) {
+            if (resident) (void)hipFree(dst); else (void)hipHostFree(dst);
+            return s->fail_hip(e, "copying layer weights");
+        }
+    }
+    if (ly.dev) (void)hipFree(ly.dev);
+    if (ly.host) (void)hipHostFree(ly.host);
+    ly.dev = resident ? dst : nullptr;
+    ly.host = resident ? nullptr : dst;
+    ly.state = resident;
+    return STAGE_OK;
+}
+
+int stage_prefill(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, int32_t T, const float *x_in,
+                  float *x_out) {
+    return run_call(s, n_mb, mb_ids, B, T, x_in, x_out, false);
+}
+
+int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in, float *x_out) {
+    return run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
+}
+
+int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k, const void *v) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch || n_tokens < 1 || !k || !v)
+        return s->fail(STAGE_EINVAL, "bad kv_append arguments");
+    const int slot = seq_slot(s, mb, b);
+    if (s->lengths[slot] + n_tokens > s->cfg.max_context)
+        return s->fail(STAGE_ERANGE, "sequence would exceed max_context");
+    if (blocks_needed(s, slot, n_tokens) > (int)s->free_blocks.size())
+        return s->fail(STAGE_ENOMEM, "KV pool exhausted");
+    DeviceGuard dg(s->cfg.device);
+    const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
+    const size_t bytes = (size_t)s->L * n_tokens * s->Hkv * s->D * elem;
+    const bool dev = is_device_ptr(k) && is_device_ptr(v);
+    if (!dev) {
+        int rc = ensure_dense(s, 2 * bytes);
+        if (rc) return rc;
+    }
+    int rc = allocate_blocks(s, {slot}, n_tokens);
+    if (rc) return rc;
+    KvCopyArgs a{};
+    a.pool_base = s->kv_pool;
+    a.layer_stride = s->kv_layer_stride;
+    a.block_table = s->d_table;
+    a.max_blocks = s->max_blocks;
+    a.n_kv_heads = s->Hkv;
+    a.head_dim = s->D;
+    a.kv_fp32 = s->cfg.kv_fp32;
+    a.n_layers = s->L;
+    a.slot = slot;
+    a.pos0 = s->lengths[slot];
+    a.n = n_tokens;
+    a.to_pool = 1;
+    if (dev) {
+        a.k = const_cast<void *>(k);
+        a.v = const_cast<void *>(v);
+    } else {
+        a.k = s->ws_dense;
+        a.v = static_cast<char *>(s->ws_dense) + bytes;
+        HIP_TRY(hipMemcpyAsync(a.k, k, bytes, hipMemcpyHostToDevice, s->cs));
+        HIP_TRY(hipMemcpyAsync(a.v, v, bytes, hipMemcpyHostToDevice, s->cs));
+    }
+    HIP_TRY(launch_kv_copy(a, s->cs));
+    s->lengths[slot] += n_tokens;
+    HIP_TRY(hipStreamSynchronize(s->cs));
+    return STAGE_OK;
+}
+
+int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void *k, void *v, int32_t drop) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch || n_tokens < 1 || !k || !v)
+        return s->fail(STAGE_EINVAL, "bad kv_export_tail arguments");
+    const int slot = seq_slot(s, mb, b);
+    if (n_tokens > s->lengths[slot])
+        return s->fail(STAGE_ESTATE, "sequence holds %d tokens, %d requested", s->lengths[slot], n_tokens);
+    DeviceGuard dg(s->cfg.device);
+    const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
+    const size_t bytes = (size_t)s->L * n_tokens * s->Hkv * s->D * elem;
+    const bool dev = is_device_ptr(k) && is_device_ptr(v);
+    if (!dev) {
+        int rc = ensure_dense(s, 2 * bytes);
+        if (rc) return rc;
+    }
+    KvCopyArgs a{};
+    a.pool_base = s->kv_pool;
+    a.layer_stride = s->kv_layer_stride;
+    a.block_table = s->d_table;
+    a.max_blocks = s->max_blocks;
+    a.n_kv_heads = s->Hkv;
+    a.head_dim = s->D;
+    a.kv_fp32 = s->cfg.kv_fp32;
+    a.n_layers = s->L;
+    a.slot = slot;
+    a.pos0 = s->lengths[slot] - n_tokens;
+    a.n = n_tokens;
+    a.to_pool = 0;
+    a.k = dev ? k : s->ws_dense;
+    a.v = dev ? v : static_cast<char *>(s->ws_dense) + bytes;
+    HIP_TRY(launch_kv_copy(a, s->cs));
+    if (!dev) {
+        HIP_TRY(hipMemcpyAsync(k, a.k, bytes, hipMemcpyDeviceToHost, s->cs));
+        HIP_TRY(hipMemcpyAsync(v, a.v, bytes, hipMemcpyDeviceToHost, s->cs));
+    }
+    HIP_TRY(hipStreamSynchronize(s->cs));
+    if (drop) {
+        s->lengths[slot] -= n_tokens;
+        release_tail_blocks(s, slot);
+    }
+    return STAGE_OK;
+}
+
+int stage_reset_sequence(stage *s, int32_t mb, int32_t b) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch)
+        return s->fail(STAGE_EINVAL, "bad sequence (%d, %d)", mb, b);
+    const int slot = seq_slot(s, mb, b);
+    s->lengths[slot] = 0;
+    release_tail_blocks(s, slot);
+    return STAGE_OK;
+}
+
+int stage_sync(stage *s) {
+    if (!s) return STAGE_EINVAL;
+    DeviceGuard dg(s->cfg.device);
+    int rc = sync_all(s);
+    if (rc) return rc;
+    HIP_TRY(hipGetLastError());
+    return STAGE_OK;
+}
+
+int stage_get_block_table(stage *s, int32_t mb, int32_t b, int32_t *blocks, int32_t cap, int32_t *n) {
+    if (!s || !n || cap < 0 || (cap > 0 && !blocks) || mb < 0 || mb >= s->cfg.max_microbatches || b < 0 ||
+        b >= s->cfg.max_batch)
+        return STAGE_EINVAL;
+    const std::vector<int> &t = s->tables[seq_slot(s, mb, b)];
+    *n = (int)t.size();
+    for (int i = 0; i < std::min<int>(cap, (int)t.size()); ++i) blocks[i] = t[i];
+    return STAGE_OK;
+}
+
+int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length) {
+    if (!s || !length || mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch)
+        return STAGE_EINVAL;
+    *length = s->lengths[seq_slot(s, mb, b)];
+    return STAGE_OK;
+}
+
+int stage_get_residency(stage *s, int32_t *out) {
+    if (!s || !out) return STAGE_EINVAL;
+    for (int l = 0; l < s->L; ++l) out[l] = s->layers[l].state;
+    return STAGE_OK;
+}
+
+static int copy_log(const std::vector<int> &log, int width, int32_t *entries, int32_t cap, int32_t *n) {
+    if (!n || cap < 0 || (cap > 0 && !entries)) return STAGE_EINVAL;
+    const int count = (int)log.size() / width;
+    *n = count;
+    for (int i = 0; i < std::min<int>(cap, count) * width; ++i) entries[i] = log[i];
+    return STAGE_OK;
+}
+
+int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n) {
+    if (!s) return STAGE_EINVAL;
+    return copy_log(s->slot_log, 3, entries, cap, n);
+}
+
+int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n) {
+    if (!s) return STAGE_EINVAL;
+    return copy_log(s->demotion_log, 2, entries, cap, n);
+}
+
+int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n) {
+    if (!s || !n || cap < 0 || (cap > 0 && !records)) return STAGE_EINVAL;
+    DeviceGuard dg(s->cfg.device);
+    int rc = sync_all(s);
+    if (rc) return rc;
+    *n = (int)s->recs.size();
+    if (!s->recs.empty()) {
+        // origin: the earliest start among the records
+        std::vector<float> start(s->recs.size()), end(s->recs.size());
+        for (size_t i = 0; i < s->recs.size(); ++i) {
+            HIP_TRY(hipEventElapsedTime(&start[i], s->recs[0].a, s->recs[i].a));
+            HIP_TRY(hipEventElapsedTime(&end[i], s->recs[0].a, s->recs[i].b));
+        }
+        const float t0 = *std::min_element(start.begin(), start.end());
+        for (int i = 0; i < std::min<int>(cap, (int)s->recs.size()); ++i) {
+            records[4 * i + 0] = (float)s->recs[i].kind;
+            records[4 * i + 1] = (float)s->recs[i].layer;
+            records[4 * i + 2] = start[i] - t0;
+            records[4 * i + 3] = end[i] - t0;
+        }
+    }
+    for (TimeRec &r : s->recs) {
+        s->ev_pool.push_back(r.a);
+        s->ev_pool.push_back(r.b);
+    }
+    s->recs.clear();
+    return STAGE_OK;
+}
+
+int stage_get_stats(stage *s, char *buf, int32_t cap) {
+    if (!s || !buf || cap < 1) return STAGE_EINVAL;
+    const int res = n_resident(s);
+    int streamed = 0;
+    for (const Layer &l : s->layers) streamed += (l.state == 0);
+    const size_t hbm_w = (size_t)res * s->blob_bytes + s->slots.size() * s->blob_bytes;
+    const int written = snprintf(
+        buf, cap,
+        "{\"calls\": %lld, \"prefill_tokens\": %lld, \"decode_tokens\": %lld, \"layer_loads\": %lld, "
+        "\"bytes_streamed\": %lld, \"layer_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
+        "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, \"kv_blocks\": %d, "
+        "\"kv_blocks_free\": %d}",
+        s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->blob_bytes, res, streamed,
+        s->slots.size(), hbm_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
+    return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
+}
+
+}  // extern "C"

@@ -1,0 +1,232 @@
+"""Drives one call sequence through the HIP stage (C ABI) and through the CPU oracle.
+
+Used by the GPU parity tests, bench.py's correctness-free timing helpers do not
+use it.  The oracle side never receives a value produced by the GPU: with
+feedback decoding, each side feeds back its own outputs.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Callable, Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+import synth
+
+_WEIGHTS: Dict[int, Dict[int, Dict[str, np.ndarray]]] = {}
+
+
+def weights_of(shape) -> Callable[[int], Dict[str, np.ndarray]]:
+    """Cached seeded bf16 weights of a stage shape, generated on first use per layer."""
+    cache = _WEIGHTS.setdefault(shape.shape_id, {})
+
+    def get(layer: int):
+        if layer not in cache:
+            cache[layer] = synth.layer_weights(shape, layer)
+        return cache[layer]
+    return get
+
+
+def drop_weights(shape) -> None:
+    _WEIGHTS.pop(shape.shape_id, None)
+
+
+@dataclass
+class Scenario:
+    """A call sequence on one stage.
+
+    prefill: tokens per sequence in the (single) prefill of each micro-batch.
+    decode_steps: decode rounds; each round visits every micro-batch.
+    calls: "one" = one micro-batch per call, round-robin (the interleaved pipeline's order);
+           "all" = one call carrying every micro-batch.
+    """
+    wl: synth.Workload
+    prefill: int
+    decode_steps: int
+    calls: str = "one"
+    kv_fp32: bool = False
+    n_resident: Optional[int] = None
+    slots: int = 2
+    thresholds: Tuple[int, ...] = ()
+    max_context: Optional[int] = None
+    timing: int = 0
+
+    @property
+    def shape(self):
+        return self.wl.shape
+
+    def resident_layers(self) -> int:
+        return self.shape.n_layers if self.n_resident is None else self.n_resident
+
+    def ctx(self) -> int:
+        return self.max_context or (self.prefill + self.decode_steps)
+
+    def call_plan(self) -> List[Tuple[str, List[int], int]]:
+        """[(kind, mb_ids, step)] in call order; step = decode step index (-1 for prefill)."""
+        mbs = list(range(self.wl.n_mb))
+        groups = [[m] for m in mbs] if self.calls == "one" else [mbs]
+        plan = [("prefill", g, -1) for g in groups]
+        for s in range(self.decode_steps):
+            plan += [("decode", g, s) for g in groups]
+        return plan
+
+
+@dataclass
+class RunResult:
+    outputs: List[np.ndarray] = field(default_factory=list)   # per call [n_mb, B, T, H]
+    inputs: List[np.ndarray] = field(default_factory=list)
+    block_tables: Dict[Tuple[int, int], List[int]] = field(default_factory=dict)
+    slot_log: List[Tuple[int, int, int]] = field(default_factory=list)
+    demotion_log: List[Tuple[int, int]] = field(default_factory=list)
+    residency: List[int] = field(default_factory=list)
+    stats: dict = field(default_factory=dict)
+    timeline: list = field(default_factory=list)
+
+    def flat_out(self) -> np.ndarray:
+        return np.concatenate([o.reshape(-1, o.shape[-1]) for o in self.outputs])
+
+    def flat_in(self) -> np.ndarray:
+        return np.concatenate([o.reshape(-1, o.shape[-1]) for o in self.inputs])
+
+
+def _inputs(sc: Scenario, kind: str, mbs: Sequence[int], step: int, prev: Dict) -> np.ndarray:
+    wl, B, H = sc.wl, sc.wl.batch, sc.shape.hidden
+    if kind == "prefill":
+        return np.stack([np.stack([synth.prefill_inputs(wl, m, b, sc.prefill) for b in range(B)]) for m in mbs])
+    if wl.feedback:
+        return np.stack([np.stack([prev[(m, b)] for b in range(B)]) for m in mbs])[:, :, None, :]
+    return np.stack([np.stack([synth.decode_input(wl, m, b, step) for b in range(B)]) for m in mbs])[:, :, None, :]
+
+
+class compute_stream:
+    """Context: a fresh (default-priority) torch stream made current, shared with the library.
+
+    torch's default stream has handle 0, which the C ABI reads as "create your own"; running
+    torch's copies and the stage's kernels on one explicit stream keeps them ordered.
+    """
+
+    def __init__(self, device: int = 0):
+        import torch
+        self.torch = torch
+        self.stream = torch.cuda.Stream(torch.device("cuda", device))
+        self.ctx = torch.cuda.stream(self.stream)
+
+    @property
+    def handle(self):
+        return self.stream.cuda_stream
+
+    def __enter__(self):
+        self.ctx.__enter__()
+        return self
+
+    def __exit__(self, *exc):
+        self.stream.synchronize()
+        return self.ctx.__exit__(*exc)
+
+
+def run_gpu(sc: Scenario, device: int = 0, weights=None) -> RunResult:
+    with compute_stream(device) as cs:
+        return _run_gpu(sc, device, weights, cs.handle)
+
+
+def _run_gpu(sc: Scenario, device: int, weights, cs_handle) -> RunResult:
+    import torch
+    import paper_2512_21835_amd as P
+
+    shape, wl = sc.shape, sc.wl
+    weights = weights or weights_of(shape)
+    dev = torch.device("cuda", device)
+    copy_stream = torch.cuda.Stream(dev)
+    cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=sc.ctx(),
+                       n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
+                       thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
+                       copy_stream=copy_stream.cuda_stream, timing=sc.timing)
+    h = P.stage_init(cfg)
+    res = RunResult()
+    try:
+        for l in range(shape.n_layers):
+            P.stage_load_layer(h, l, weights(l), 1 if l < sc.resident_layers() else 0)
+        prev: Dict[Tuple[int, int], np.ndarray] = {}
+        outs = []
+        for kind, mbs, step in sc.call_plan():
+            x = _inputs(sc, kind, mbs, step, prev)
+            x_in = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
+            x_out = torch.empty_like(x_in)
+            if kind == "prefill":
+                P.stage_prefill(h, mbs, wl.batch, x.shape[2], x_in, x_out)
+            else:
+                P.stage_decode(h, mbs, wl.batch, x_in, x_out)
+            outs.append(x_out)
+            res.inputs.append(x)
+            if wl.feedback:
+                o = x_out.cpu().numpy()
+                for i, m in enumerate(mbs):
+                    for b in range(wl.batch):
+                        prev[(m, b)] = o[i, b, -1]
+        P.stage_sync(h)
+        res.outputs = [o.cpu().numpy() for o in outs]
+        for m in range(wl.n_mb):
+            for b in range(wl.batch):
+                res.block_tables[(m, b)] = P.stage_get_block_table(h, m, b)
+        res.slot_log = P.stage_get_slot_log(h)
+        res.demotion_log = P.stage_get_demotion_log(h)
+        res.residency = P.stage_get_residency(h, shape.n_layers)
+        res.stats = P.stage_get_stats(h)
+        if sc.timing:
+            res.timeline = P.stage_get_timeline(h)
+    finally:
+        P.stage_destroy(h)
+    return res
+
+
+def run_oracle(sc: Scenario, weights=None) -> RunResult:
+    from oracle.policies import BlockAllocator, ResidencySchedule, SlotSchedule
+    from oracle.stage_oracle import OracleStage
+
+    shape, wl = sc.shape, sc.wl
+    weights = weights or weights_of(shape)
+    orc = OracleStage(shape, weights, kv_dtype="f32" if sc.kv_fp32 else "bf16")
+    n_blocks = wl.n_mb * wl.batch * math.ceil(sc.ctx() / 16)
+    alloc = BlockAllocator(n_blocks, 16)
+    slots = SlotSchedule(sc.slots)
+    resid = ResidencySchedule(shape.n_layers, range(sc.resident_layers()), sc.thresholds)
+    res = RunResult()
+    prev: Dict[Tuple[int, int], np.ndarray] = {}
+    for call_no, (kind, mbs, step) in enumerate(sc.call_plan()):
+        x = _inputs(sc, kind, mbs, step, prev)
+        T = x.shape[2]
+        keys = [(m, b) for m in mbs for b in range(wl.batch)]
+        longest = max([alloc.lengths.get(k, 0) for k in alloc.lengths] + [alloc.lengths.get(k, 0) + T for k in keys])
+        resid.before_call(call_no, longest)
+        alloc.call([(k, T) for k in keys])
+        slots.call(call_no, resid.streamed())
+        outs = orc.forward([((m, b), x[i, b]) for i, m in enumerate(mbs) for b in range(wl.batch)])
+        o = np.stack(outs).reshape(x.shape)
+        res.outputs.append(o)
+        res.inputs.append(x)
+        if wl.feedback:
+            for i, m in enumerate(mbs):
+                for b in range(wl.batch):
+                    prev[(m, b)] = o[i, b, -1].astype(np.float32)
+    for m in range(wl.n_mb):
+        for b in range(wl.batch):
+            res.block_tables[(m, b)] = alloc.table((m, b))
+    res.slot_log = list(slots.log)
+    res.demotion_log = list(resid.log)
+    res.residency = [1 if l in resid.resident else 0 for l in range(shape.n_layers)]
+    res._oracle = orc
+    return res
+
+
+def compare(got: np.ndarray, ref: np.ndarray, x_got: np.ndarray, x_ref: np.ndarray) -> dict:
+    """max |d|, cosine of the outputs and cosine of the stage contribution out - in."""
+    g = got.astype(np.float64)
+    r = ref.astype(np.float64)
+    dg = g - x_got.astype(np.float64)
+    dr = r - x_ref.astype(np.float64)
+
+    def cos(a, b):
+        return float((a * b).sum() / math.sqrt((a * a).sum() * (b * b).sum()))
+    return {"max_abs": float(np.abs(g - r).max()), "cos": cos(g, r), "cos_delta": cos(dg, dr),
+            "rms_ref": float(np.sqrt((r * r).mean())), "n": int(g.size)}

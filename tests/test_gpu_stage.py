@@ -1,0 +1,214 @@
+"""GPU parity of the HIP stage (through the C ABI) against the float64 CPU oracle.
+
+Tolerance (stated for the stage output): max |GPU - oracle| <= 2e-2 and cosine >=
+0.9995, on the output and on the stage contribution (output - input).  Integer
+state -- block tables, slot log, demotions -- must match the oracle's independent
+policies exactly.  Offloading must not change a single bit (lossless).
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+from tests.harness import Scenario, compare, compute_stream, run_gpu, run_oracle, weights_of
+
+pytestmark = pytest.mark.gpu
+
+TOL_ABS = 2e-2
+TOL_COS = 0.9995
+
+TINY_RAGGED = synth.Workload("tiny_ragged", 100, synth.TINY, n_mb=3, batch=2, prefill=37, decode_steps=20)
+
+
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def check(name, sc, got, ref, tol_abs=TOL_ABS):
+    m = compare(got.flat_out(), ref.flat_out(), got.flat_in(), ref.flat_in())
+    print(f"\n[{name}] {m}", flush=True)
+    assert m["cos"] >= TOL_COS and m["cos_delta"] >= TOL_COS, m
+    assert m["max_abs"] <= tol_abs, m
+    assert got.block_tables == ref.block_tables
+    assert got.slot_log == ref.slot_log
+    assert got.demotion_log == ref.demotion_log
+    assert got.residency == ref.residency
+    return m
+
+
+@pytest.mark.parametrize("kv_fp32", [False, True])
+def test_tiny_feedback_matches_oracle(kv_fp32):
+    _gpu()
+    sc = Scenario(synth.WORKLOADS["tiny"], prefill=16, decode_steps=16, kv_fp32=kv_fp32)
+    check(f"tiny kv_fp32={kv_fp32}", sc, run_gpu(sc), run_oracle(sc))
+
+
+@pytest.mark.parametrize("calls", ["one", "all"])
+def test_tiny_ragged_multi_sequence(calls):
+    _gpu()
+    sc = Scenario(TINY_RAGGED, prefill=37, decode_steps=20, calls=calls)
+    check(f"tiny ragged calls={calls}", sc, run_gpu(sc), run_oracle(sc))
+
+
+@pytest.mark.parametrize("slots", [1, 2, 3])
+def test_streamed_layers_are_lossless(slots):
+    """Offloaded layers streamed through S slots give the all-resident outputs bit for bit."""
+    _gpu()
+    base = Scenario(TINY_RAGGED, prefill=37, decode_steps=6, calls="all")
+    ref = run_gpu(base)
+    sc = dataclasses.replace(base, n_resident=0, slots=slots)
+    got = run_gpu(sc)
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    orc = run_oracle(sc)
+    assert got.slot_log == orc.slot_log
+    assert got.residency == [0, 0]
+    assert got.stats["layer_loads"] == 2 * len(sc.call_plan())
+
+
+def test_round_robin_equals_all_in_one_call_bitwise():
+    """Per-row arithmetic does not depend on how many micro-batches share a call."""
+    _gpu()
+    a = run_gpu(Scenario(TINY_RAGGED, prefill=37, decode_steps=4, calls="one"))
+    b = run_gpu(Scenario(TINY_RAGGED, prefill=37, decode_steps=4, calls="all"))
+    ga = np.concatenate([o.reshape(-1, 256) for o in a.outputs[:3]])
+    gb = b.outputs[0].reshape(-1, 256)
+    assert np.array_equal(ga, gb)
+    for s in range(4):
+        ga = np.concatenate([o.reshape(-1, 256) for o in a.outputs[3 + 3 * s: 6 + 3 * s]])
+        assert np.array_equal(ga, b.outputs[1 + s].reshape(-1, 256))
+
+
+def test_threshold_demotions_follow_schedule_and_stay_lossless():
+    _gpu()
+    ths = (39, 40, 41)   # prefill 37: decode rounds 2, 3, 4 each demote one layer (2 layers: 2 demotions)
+    sc = Scenario(TINY_RAGGED, prefill=37, decode_steps=6, calls="one", thresholds=ths)
+    got = run_gpu(sc)
+    orc = run_oracle(sc)
+    assert got.demotion_log == orc.demotion_log and len(got.demotion_log) == 2
+    assert got.slot_log == orc.slot_log
+    assert got.residency == [0, 0]
+    ref = run_gpu(dataclasses.replace(sc, thresholds=()))
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+
+
+def test_kv_tail_export_and_append_round_trip():
+    """Alg. 2's tail move: export, drop, re-append -> the next outputs are bit-identical."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape = synth.TINY
+    w = weights_of(shape)
+    wl = TINY_RAGGED
+
+    cs = compute_stream().__enter__()
+
+    def make():
+        cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=2,
+                           compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 1)
+        x = torch.from_numpy(synth.prefill_inputs(wl, 0, 0, 37)).cuda()
+        P.stage_prefill(h, [0], 1, 37, x, torch.empty_like(x))
+        return h
+
+    nxt = torch.from_numpy(synth.decode_input(wl, 0, 0, 0)[None]).cuda()
+    h1 = make()
+    want = torch.empty_like(nxt)
+    P.stage_decode(h1, [0], 1, nxt, want)
+    P.stage_sync(h1)
+    table_before = P.stage_get_block_table(h1, 0, 0)
+    P.stage_destroy(h1)
+
+    h2 = make()
+    try:
+        k = np.zeros((2, 21, 2, 64), np.uint16)
+        v = np.zeros_like(k)
+        P.stage_kv_export_tail(h2, 0, 0, 21, k, v, True)    # 37 -> 16: blocks 1 and 2 freed
+        assert P.stage_get_length(h2, 0, 0) == 16
+        assert P.stage_get_block_table(h2, 0, 0) == table_before[:1]
+        kd = torch.from_numpy(k.view(np.int16)).cuda()
+        vd = torch.from_numpy(v.view(np.int16)).cuda()
+        P.stage_kv_append(h2, 0, 0, 21, kd, vd)              # device source
+        assert P.stage_get_length(h2, 0, 0) == 37
+        got = torch.empty_like(nxt)
+        P.stage_decode(h2, [0], 1, nxt, got)
+        P.stage_sync(h2)
+        assert torch.equal(got, want)
+        # the exported K/V are the values the oracle stores, up to one bf16 rounding flip
+        from oracle.stage_oracle import OracleStage, widen_bf16
+        orc = OracleStage(shape, w, kv_dtype="bf16")
+        orc.forward([("s", synth.prefill_inputs(wl, 0, 0, 37))])
+        ok, ov = orc.export_tail("s", 21, drop=False)
+        gk = widen_bf16(k).numpy()
+        assert np.abs(gk - ok).max() <= 2 ** -7 * np.abs(ok).max()
+        assert np.mean(gk == ok) > 0.99
+    finally:
+        P.stage_destroy(h2)
+        cs.__exit__(None, None, None)
+
+
+def test_error_paths_leave_stage_usable():
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape = synth.TINY
+    w = weights_of(shape)
+    cs = compute_stream().__enter__()
+    cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=20, n_resident_max=1,
+                       kv_pool_blocks=2, compute_stream=cs.handle)
+    h = P.stage_init(cfg)
+    try:
+        x = torch.zeros(1, 1, 16, 256, device="cuda")
+        y = torch.empty_like(x)
+        with pytest.raises(P.StageError) as e:
+            P.stage_prefill(h, [0], 1, 16, x, y)          # layers not loaded
+        assert e.value.code == P.STAGE_EINVAL
+        P.stage_load_layer(h, 0, w(0), 1)
+        with pytest.raises(P.StageError) as e:
+            P.stage_load_layer(h, 1, w(1), 1)             # budget: 1 resident layer
+        assert e.value.code == P.STAGE_ENOMEM
+        P.stage_load_layer(h, 1, w(1), 0)
+        with pytest.raises(P.StageError) as e:
+            P.stage_decode(h, [0], 1, x[:, :, 0], y[:, :, 0])   # empty sequence
+        assert e.value.code == P.STAGE_ESTATE
+        with pytest.raises(P.StageError) as e:
+            P.stage_prefill(h, [0, 0], 1, 16, x, y)       # repeated micro-batch
+        assert e.value.code == P.STAGE_EINVAL
+        xx = torch.zeros(1, 1, 21, 256, device="cuda")
+        with pytest.raises(P.StageError) as e:
+            P.stage_prefill(h, [0], 1, 21, xx, torch.empty_like(xx))   # > max_context
+        assert e.value.code == P.STAGE_ERANGE
+        P.stage_prefill(h, [0], 1, 16, x, y)              # takes 1 of 2 blocks
+        x2 = torch.zeros(1, 1, 17, 256, device="cuda")
+        with pytest.raises(P.StageError) as e:
+            P.stage_prefill(h, [1], 1, 17, x2, torch.empty_like(x2))   # needs 2 blocks, 1 free
+        assert e.value.code == P.STAGE_ENOMEM
+        assert P.stage_get_length(h, 1, 0) == 0 and P.stage_get_stats(h)["kv_blocks_free"] == 1
+        P.stage_decode(h, [0], 1, x[:, :, 0], y[:, :, 0])  # still usable
+        P.stage_sync(h)
+        assert P.stage_get_length(h, 0, 0) == 17
+        assert torch.isfinite(y[:, :, 0]).all()
+    finally:
+        P.stage_destroy(h)
+        cs.__exit__(None, None, None)
+
+
+def test_llama8b_stage_full_length_bf16_kv():
+    """The 8B-shaped stage at its full size: prefill 1024, then 128 decode steps (batch 1)."""
+    _gpu()
+    sc = Scenario(synth.WORKLOADS["llama8b_stage"], prefill=1024, decode_steps=128)
+    got = run_gpu(sc)
+    ref = run_oracle(sc)
+    check("llama8b full bf16-kv", sc, got, ref)
+
+
+def test_llama8b_stage_fp32_kv_short():
+    _gpu()
+    sc = Scenario(synth.WORKLOADS["llama8b_stage"], prefill=64, decode_steps=8, kv_fp32=True)
+    check("llama8b short fp32-kv", sc, run_gpu(sc), run_oracle(sc))
