@@ -1,0 +1,167 @@
+"""Decode throughput of one pipeline stage on one MI355X.
+
+Workload: the LLaMA-3-8B-shaped stage (8 decoder layers, hidden 4096, 32 query /
+8 KV heads, head_dim 128, SwiGLU 14336, bf16 weights resident in HBM, bf16 paged
+KV cache), batch 1, prefill 1024 tokens, then decode steps.  One timed step is
+one decode step of the whole stage (all layers: RMSNorm, QKV, RoPE + KV store,
+GQA attention, O + residual, RMSNorm, gate/up + SwiGLU, down + residual) for one
+new token, with its input already in HBM.  Inputs are seeded synthetic hidden
+states N(0, 1); weights bf16(N(0, 0.02)), gains bf16(1 + N(0, 0.02)).
+
+Prints one JSON line: value = decode tokens/s of the stage, plus the roofline of
+the dominant kernel (the gate/up projection, measured with HIP events on the
+compute stream over the timed region), whole-step HBM bandwidth, prefill
+throughput and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
+
+
+def gateup_bytes(shape, rows: int) -> int:
+    """Algorithmic HBM bytes of one gate/up launch: both weight matrices once, gains, x in, h out."""
+    h, f = shape.hidden, shape.ffn
+    return 2 * f * h * 2 + h * 2 + rows * h * 4 + rows * f * 4
+
+
+def decode_step_bytes(shape, ctx_before: int) -> int:
+    """Algorithmic HBM bytes of one batch-1 decode step at a context of ctx_before tokens.
+
+    Every layer's weights once, the KV cache read (ctx_before + 1 positions, K and V, bf16),
+    the new K/V written, and the hidden state in and out of each projection (fp32).
+    """
+    h, f, qd, kvd = shape.hidden, shape.ffn, shape.q_dim, shape.kv_dim
+    weights = shape.layer_bytes()
+    kv = (ctx_before + 1) * 2 * kvd * 2 + 2 * kvd * 2
+    acts = 4 * (h + (qd + 2 * kvd) + qd + qd + h + h + 2 * h + f + f + 2 * h)
+    return shape.n_layers * (weights + kv + acts)
+
+
+def cpu_baseline(shape, weights, wl, n_tokens: int):
+    """The float64 oracle as it stands, decoding n_tokens fresh tokens after a 16-token prefill."""
+    import torch
+
+    import synth
+    from oracle.stage_oracle import OracleStage
+    orc = OracleStage(shape, weights, kv_dtype="bf16")
+    orc.forward([("s", synth.prefill_inputs(wl, 7, 0, 16))])
+    t0 = time.perf_counter()
+    for i in range(n_tokens):
+        orc.forward([("s", synth.decode_input(wl, 7, 0, i)[None])])
+    dt = time.perf_counter() - t0
+    return {"value": n_tokens / dt, "unit": "decode tokens/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"{n_tokens} decode tokens of the same 8-layer stage after a 16-token prefill "
+                      f"(float64 torch CPU; per-token cost is the weight pass, context adds <1%)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--prefill", type=int, default=1024)
+    ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one stage on one GPU; --gpus {args.gpus} is not supported "
+              "(the stage does not shard across GPUs).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2512_21835_amd as P
+
+    wl = synth.WORKLOADS["llama8b_stage"]
+    shape = wl.shape
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
+    K, W, T = args.steps, args.warmup, args.prefill
+    ctx = T + max(K, W)
+
+    t_gen = time.perf_counter()
+    weights = [synth.layer_weights(shape, l) for l in range(shape.n_layers)]
+    t_gen = time.perf_counter() - t_gen
+    cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=ctx, n_resident_max=shape.n_layers,
+                       compute_stream=stream.cuda_stream)
+    h = P.stage_init(cfg)
+    try:
+        for l, w in enumerate(weights):
+            P.stage_load_layer(h, l, w, 1)
+        H = shape.hidden
+        # prefill both sequences (mb 0: warmup, mb 1: timed); time the second prefill
+        xp = [torch.from_numpy(synth.prefill_inputs(wl, m, 0, T)).to(dev) for m in (0, 1)]
+        yp = [torch.empty_like(x) for x in xp]
+        P.stage_prefill(h, [0], 1, T, xp[0], yp[0])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        P.stage_prefill(h, [1], 1, T, xp[1], yp[1])
+        torch.cuda.synchronize()
+        prefill_s = time.perf_counter() - t0
+
+        xw = torch.from_numpy(np.stack([synth.decode_input(wl, 0, 0, s) for s in range(W)])).to(dev)
+        xd = torch.from_numpy(np.stack([synth.decode_input(wl, 1, 0, s) for s in range(K)])).to(dev)
+        yw, yd = torch.empty_like(xw), torch.empty_like(xd)
+        for s in range(W):
+            P.stage_decode(h, [0], 1, xw[s:s + 1], yw[s:s + 1])
+        torch.cuda.synchronize()
+        P.stage_get_timeline(h)                       # clear
+        P.stage_set_timing(h, P.STAGE_TIME_GATEUP)   # HIP events around every gate/up launch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(K):
+            P.stage_decode(h, [1], 1, xd[s:s + 1], yd[s:s + 1])
+        t_enq = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        P.stage_set_timing(h, 0)
+        tl = P.stage_get_timeline(h)
+        assert bool(torch.isfinite(yd).all()), "non-finite decode output"
+    finally:
+        P.stage_destroy(h)
+
+    gu = [e - s for kind, _, s, e in tl if kind == 2]
+    gu_ms = sum(gu) / len(gu)
+    gu_bytes = gateup_bytes(shape, 1)
+    achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
+    step_bytes = sum(decode_step_bytes(shape, T + s) for s in range(K)) / K
+    ms_step = dt * 1e3 / K
+    out = {
+        "metric": "decode tokens/s per stage", "value": K / dt, "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"llama8b_stage decode: 8 layers, hidden 4096, 32/8 heads x 128, ffn 14336, "
+                               f"bf16 weights resident, bf16 paged KV, batch 1, context {T}->{T + K}",
+                   "global_batch": 1, "seq_len": T + K, "parallelism": "none (one stage, one GPU)",
+                   "weights": "bf16", "kv_cache": "bf16", "accumulate": "f32"},
+        "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (gemv, 1 row)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "bytes_per_launch": gu_bytes, "avg_launch_ms": gu_ms, "launches": len(gu)},
+        "step_hbm": {"bytes_per_step": step_bytes, "achieved_GBs": step_bytes / (ms_step * 1e-3) / 1e9,
+                     "frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "host_enqueue_ms_per_step": t_enq * 1e3 / K,
+        "prefill": {"tokens": T, "tokens_per_s": T / prefill_s, "ms": prefill_s * 1e3},
+        "weight_gen_s": t_gen,
+    }
+    if args.cpu_tokens > 0:
+        out["cpu_baseline"] = cpu_baseline(shape, lambda l: weights[l], wl, args.cpu_tokens)
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -53,6 +53,7 @@ typedef enum {
 
 #define STAGE_MAX_THRESHOLDS 32
 #define STAGE_MAX_SEQS_PER_CALL 64
+#define STAGE_MAX_CONTEXT 16384
 
 /* Timing flags (stage_config.timing). */
 #define STAGE_TIME_CALLS 1   /* events around each prefill/decode call and each slot copy */
@@ -64,7 +65,8 @@ typedef struct {
     int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn;
     float rope_theta; /* RoPE base; angle of pair i at position p is p * theta^(-2i/head_dim) */
     float rms_eps;    /* RMSNorm epsilon, added to mean(x^2) inside the square root */
-    /* Sequence capacity.  max_microbatches * max_batch <= STAGE_MAX_SEQS_PER_CALL. */
+    /* Sequence capacity.  max_microbatches * max_batch <= STAGE_MAX_SEQS_PER_CALL;
+       max_context <= STAGE_MAX_CONTEXT. */
     int32_t max_microbatches, max_batch, max_context;
     int32_t kv_block_tokens; /* tokens per KV block; must be 16 */
     int32_t kv_pool_blocks;  /* blocks in the pool; 0 = every sequence can reach max_context */
@@ -178,6 +180,9 @@ int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
    four floats: kind (0 call, 1 slot copy, 2 gate/up kernel), layer (-1 for a call), start and
    end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
 int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
+
+/* Replaces the STAGE_TIME_* flags of the stage (see stage_config.timing) for later calls. */
+int stage_set_timing(stage *s, int32_t flags);
 
 /* JSON object with counters: calls, tokens, layer loads, bytes streamed, HBM bytes in use. */
 int stage_get_stats(stage *s, char *buf, int32_t cap);

@@ -1,18 +1,23 @@
 // Memory-bound projections for decode: y = W x with bf16 weights W [N, K] (row-major) and fp32
 // activations, fp32 accumulation.  One pass over the weights serves up to 8 activation rows.
 //
-// Work split: a workgroup is 4 wavefronts of 64 lanes.  Each wavefront owns R output rows (or R
-// gate/up row pairs) over the whole K range; lane l reads 16 bytes (8 bf16) of every owned row at
-// k = l*8 + 512*i, so one load instruction covers 1 KiB of contiguous weights per row.  Lane
-// partial sums are combined with a butterfly of cross-lane shuffles.
+// Work split: a workgroup is 4 wavefronts of 64 lanes.  Each wavefront owns R units over the whole
+// K range, a unit being one output row, or a pair of rows that its epilogue needs together:
+// (gate row f, up row f) for SwiGLU, (row i, row i + d/2) of one head for rotate-half RoPE.  Lane
+// l reads 16 bytes (8 bf16) of every owned row at k = l*8 + 512*i, so one load instruction
+// covers 1 KiB of contiguous weights per row.  Lane partial sums are combined with a butterfly of
+// cross-lane shuffles.
 //
-// Fused steps: the RMSNorm in front of the QKV and gate/up projections (the sum of squares of
-// x is accumulated from the same loads, and the 1/rms scale applied to the dot product), the
-// SwiGLU of the gate/up pair, and the residual add after the O and down projections.
+// Fused steps: the RMSNorm in front of the QKV and gate/up projections (the sum of squares of x
+// is accumulated from the same loads and the 1/rms scale applied to the dot product), RoPE and
+// the KV-cache store after the QKV projection, the SwiGLU of the gate/up pair, and the residual
+// add after the O and down projections.
 //
 // Every output element is produced by one fixed sequence of fused multiply-adds and one fixed
-// butterfly, whatever the number of activation rows or the row tiling: results do not depend on
+// butterfly, whatever the number of activation rows or the unit tiling: results do not depend on
 // how many micro-batches share a call.
+#include <hip/hip_ext.h>
+
 #include "stage_kernels.h"
 
 namespace stg {
@@ -45,18 +50,88 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <int MODE> struct Shape {
+    static constexpr bool kNorm = MODE != GEMV_PLAIN_RESIDUAL;
+    static constexpr int NW = (MODE == GEMV_NORM_SWIGLU || MODE == GEMV_NORM_ROPE_KV) ? 2 : 1;
+};
+
+// Weight row w (0 or 1) of unit u; units beyond the last are clamped to it (loads stay in bounds).
+template <int MODE>
+__device__ __forceinline__ const uint16_t *unit_row(const GemvArgs &a, int u, int w) {
+    if (MODE == GEMV_NORM_ROPE_KV) {
+        const int half = a.kv.head_dim / 2;
+        const int h = u / half, i = u % half;
+        return a.w + (size_t)(h * a.kv.head_dim + i + w * half) * a.K;
+    }
+    if (MODE == GEMV_NORM_SWIGLU) return (w ? a.w2 : a.w) + (size_t)u * a.K;
+    return a.w + (size_t)u * a.K;
+}
+
+template <int MODE>
+__device__ __forceinline__ int n_units(const GemvArgs &a) {
+    return MODE == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
+}
+
+__device__ __forceinline__ void store_kv(void *pool, size_t e, float v, int kv_fp32) {
+    if (kv_fp32)
+        static_cast<float *>(pool)[e] = v;
+    else
+        static_cast<uint16_t *>(pool)[e] = to_bf16(v);
+}
+
+// RoPE + KV store of one (row i, row i + d/2) pair of head h for activation row m.
+__device__ __forceinline__ void rope_kv_epilogue(const GemvArgs &a, int u, int m, float x1, float x2) {
+    const int d = a.kv.head_dim, half = d / 2;
+    const int h = u / half, i = u % half;
+    const int row = a.row0 + m;
+    const int sidx = row / a.meta->rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+    const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
+    float r1 = x1, r2 = x2;
+    if (h < hq + hkv) {
+        const float c = a.cos_t[(size_t)pos * half + i], s = a.sin_t[(size_t)pos * half + i];
+        r1 = x1 * c - x2 * s;
+        r2 = x1 * s + x2 * c;
+    }
+    if (h < hq) {
+        float *q = a.out + m * a.out_ld + h * d;
+        q[i] = r1;
+        q[i + half] = r2;
+        return;
+    }
+    const int slot = a.meta->seq_slot[sidx];
+    const int block = a.kv.block_table[(size_t)slot * a.kv.max_blocks + pos / kBlockTokens];
+    const int kv = h < hq + hkv ? 0 : 1;
+    const int g = h - hq - kv * hkv;
+    const size_t e = (((size_t)block * 2 + kv) * hkv + g) * kBlockTokens * d +
+                     (size_t)(pos % kBlockTokens) * d + i;
+    store_kv(a.kv.pool, e, r1, a.kv_fp32);
+    store_kv(a.kv.pool, e + half, r2, a.kv_fp32);
+}
+
 template <int M, int R, int MODE>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
-    constexpr bool kNorm = (MODE == GEMV_NORM_STORE || MODE == GEMV_NORM_SWIGLU);
-    constexpr int NW = (MODE == GEMV_NORM_SWIGLU) ? 2 : 1;
+    constexpr bool kNorm = Shape<MODE>::kNorm;
+    constexpr int NW = Shape<MODE>::NW;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    const int units = n_units<MODE>(a);
     const int unit0 = (blockIdx.x * kWaves + wave) * R;
-    if (unit0 >= a.N) return;
+    if (unit0 >= units) return;
 
-    const uint16_t *wbase[NW];
-    wbase[0] = a.w;
-    if (NW == 2) wbase[NW - 1] = a.w2;
+    const uint16_t *wrow[NW][R];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int r = 0; r < R; ++r) wrow[w][r] = unit_row<MODE>(a, min(unit0 + r, units - 1), w);
 
     float acc[NW][R][M];
     float ss[M];
@@ -74,10 +149,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int row = min(unit0 + r, a.N - 1);
-                wv[w][r] = load_stream16(wbase[w] + (size_t)row * a.K + k);
-            }
+            for (int r = 0; r < R; ++r) wv[w][r] = load_stream16(wrow[w][r] + k);
         float g[8];
         if (kNorm) unpack8(*reinterpret_cast<const uint4 *>(a.gain + k), g);
 #pragma unroll
@@ -114,21 +186,25 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
             for (int r = 0; r < R; ++r) acc[w][r][m] = wave_sum(acc[w][r][m]);
     }
 
-    // Epilogue: lane (r * M + m) writes output row unit0 + r of activation row m.
+    // Epilogue: lane (r * M + m) finishes unit unit0 + r of activation row m.
 #pragma unroll
     for (int r = 0; r < R; ++r) {
 #pragma unroll
         for (int m = 0; m < M; ++m) {
             if (lane != r * M + m) continue;
-            const int row = unit0 + r;
-            if (row >= a.N || m >= a.rows) continue;
+            const int u = unit0 + r;
+            if (u >= units || m >= a.rows) continue;
             float scale = 1.f;
             if (kNorm) scale = 1.f / sqrtf(ss[m] / (float)a.K + a.eps);
-            float *o = a.out + m * a.out_ld + row;
+            if (MODE == GEMV_NORM_ROPE_KV) {
+                rope_kv_epilogue(a, u, m, acc[0][r][m] * scale, acc[NW - 1][r][m] * scale);
+                continue;
+            }
+            float *o = a.out + m * a.out_ld + u;
             if (MODE == GEMV_NORM_STORE) {
                 *o = acc[0][r][m] * scale;
             } else if (MODE == GEMV_PLAIN_RESIDUAL) {
-                *o = a.res[m * a.out_ld + row] + acc[0][r][m];
+                *o = a.res[m * a.out_ld + u] + acc[0][r][m];
             } else {
                 const float gt = acc[0][r][m] * scale;
                 const float up = acc[NW - 1][r][m] * scale;
@@ -138,24 +214,36 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     }
 }
 
+template <int M, int R, int MODE>
+void launch_one(const GemvArgs &c, int grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    if (e0 || e1)
+        hipExtLaunchKernelGGL((gemv_kernel<M, R, MODE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+    else
+        hipLaunchKernelGGL((gemv_kernel<M, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+}
+
 template <int MODE, int R>
-hipError_t launch_mode(GemvArgs a, hipStream_t st) {
-    const int grid = (a.N + kWaves * R - 1) / (kWaves * R);
+hipError_t launch_mode(GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+    const int units = MODE == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
+    const int grid = (units + kWaves * R - 1) / (kWaves * R);
     const int total = a.rows;
     for (int r0 = 0; r0 < total; r0 += kMaxRowsPerLaunch) {
         GemvArgs c = a;
         c.rows = min(kMaxRowsPerLaunch, total - r0);
+        c.row0 = a.row0 + r0;
         c.act = a.act + (size_t)r0 * a.act_ld;
         c.out = a.out + (size_t)r0 * a.out_ld;
         if (a.res) c.res = a.res + (size_t)r0 * a.out_ld;
+        hipEvent_t e0 = r0 == 0 ? ev_start : nullptr;
+        hipEvent_t e1 = r0 + kMaxRowsPerLaunch >= total ? ev_stop : nullptr;
         if (c.rows == 1)
-            hipLaunchKernelGGL((gemv_kernel<1, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+            launch_one<1, R, MODE>(c, grid, st, e0, e1);
         else if (c.rows == 2)
-            hipLaunchKernelGGL((gemv_kernel<2, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+            launch_one<2, R, MODE>(c, grid, st, e0, e1);
         else if (c.rows <= 4)
-            hipLaunchKernelGGL((gemv_kernel<4, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+            launch_one<4, R, MODE>(c, grid, st, e0, e1);
         else
-            hipLaunchKernelGGL((gemv_kernel<8, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+            launch_one<8, R, MODE>(c, grid, st, e0, e1);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -164,12 +252,26 @@ hipError_t launch_mode(GemvArgs a, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st) {
+hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (a.rows <= 0) return hipSuccess;
+    // Two units per wavefront pay off once a matrix is large (measured on the 70B-shaped layer:
+    // one unit per wavefront leaves the long rows of the down projection short of loads in
+    // flight); one unit per wavefront keeps more wavefronts busy on the smaller ones.
+    const long units = mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
+    const bool big = units * (long)a.K >= 200L * 1000 * 1000;
     switch (mode) {
-        case GEMV_NORM_STORE: return launch_mode<GEMV_NORM_STORE, 2>(a, st);
-        case GEMV_PLAIN_RESIDUAL: return launch_mode<GEMV_PLAIN_RESIDUAL, 2>(a, st);
-        case GEMV_NORM_SWIGLU: return launch_mode<GEMV_NORM_SWIGLU, 1>(a, st);
+        case GEMV_NORM_STORE:
+            return big ? launch_mode<GEMV_NORM_STORE, 2>(a, st, ev_start, ev_stop)
+                       : launch_mode<GEMV_NORM_STORE, 1>(a, st, ev_start, ev_stop);
+        case GEMV_PLAIN_RESIDUAL:
+            return big ? launch_mode<GEMV_PLAIN_RESIDUAL, 2>(a, st, ev_start, ev_stop)
+                       : launch_mode<GEMV_PLAIN_RESIDUAL, 1>(a, st, ev_start, ev_stop);
+        case GEMV_NORM_SWIGLU:
+            return big ? launch_mode<GEMV_NORM_SWIGLU, 2>(a, st, ev_start, ev_stop)
+                       : launch_mode<GEMV_NORM_SWIGLU, 1>(a, st, ev_start, ev_stop);
+        case GEMV_NORM_ROPE_KV:
+            return big ? launch_mode<GEMV_NORM_ROPE_KV, 2>(a, st, ev_start, ev_stop)
+                       : launch_mode<GEMV_NORM_ROPE_KV, 1>(a, st, ev_start, ev_stop);
         default: return hipErrorInvalidValue;
     }
 }

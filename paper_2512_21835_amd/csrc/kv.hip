@@ -24,9 +24,9 @@ __device__ __forceinline__ void store_kv(void *pool, size_t e, float v, int kv_f
 // position of the paged cache in the KV element type.
 __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
     const int row = blockIdx.x;
-    const int sidx = row / a.meta.rows_per_seq;
-    const int pos = a.meta.pos0[sidx] + row % a.meta.rows_per_seq;
-    const int slot = a.meta.seq_slot[sidx];
+    const int sidx = row / a.meta->rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+    const int slot = a.meta->seq_slot[sidx];
     const int d = a.kv.head_dim, half = d / 2;
     const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
     const size_t ld = (size_t)(hq + 2 * hkv) * d;
@@ -58,6 +58,12 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
         const size_t e = kbase + (size_t)(hkv + g) * head_stride + c;
         store_kv(a.kv.pool, e, src[(size_t)(hq + hkv) * d + i], a.kv_fp32);
     }
+}
+
+__global__ void meta_write_kernel(CallMeta m, CallMeta *dst) {
+    const int *src = reinterpret_cast<const int *>(&m);
+    int *d = reinterpret_cast<int *>(dst);
+    for (int i = threadIdx.x; i < (int)(sizeof(CallMeta) / sizeof(int)); i += blockDim.x) d[i] = src[i];
 }
 
 constexpr int kTableChunk = 240;
@@ -103,6 +109,11 @@ __global__ __launch_bounds__(256) void kv_copy_kernel(KvCopyArgs a) {
 hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st) {
     if (a.rows <= 0) return hipSuccess;
     hipLaunchKernelGGL(rope_kv_kernel, dim3(a.rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_meta_write(const CallMeta &m, CallMeta *dst, hipStream_t st) {
+    hipLaunchKernelGGL(meta_write_kernel, dim3(1), dim3(256), 0, st, m, dst);
     return hipGetLastError();
 }
 

@@ -32,7 +32,8 @@ struct KvView {
 enum GemvMode {
     GEMV_NORM_STORE = 0,     // out = W (rmsnorm(act) * gain)
     GEMV_PLAIN_RESIDUAL = 1, // out = res + W act
-    GEMV_NORM_SWIGLU = 2     // out = silu(Wg y) * (Wu y), y = rmsnorm(act) * gain
+    GEMV_NORM_SWIGLU = 2,    // out = silu(Wg y) * (Wu y), y = rmsnorm(act) * gain
+    GEMV_NORM_ROPE_KV = 3    // [q | k | v] = Wqkv y; rotate q, k; q -> q_out, k and v -> KV cache
 };
 
 struct GemvArgs {
@@ -41,15 +42,25 @@ struct GemvArgs {
     const float *act;     // [rows, K] with row stride act_ld
     const uint16_t *gain; // [K] bf16 (NORM modes)
     const float *res;     // [rows, N] with row stride out_ld (RESIDUAL)
-    float *out;           // [rows, N] with row stride out_ld
+    float *out;           // [rows, N] with row stride out_ld (ROPE_KV: rotated q, [rows, Hq d])
     long act_ld, out_ld;
     int N, K;
     int rows;  // rows in this launch
+    int row0;  // index of the launch's first row among the call's rows (ROPE_KV: row metadata)
     float eps;
+    // ROPE_KV only
+    const float *cos_t, *sin_t;  // [max_context, d/2]
+    KvView kv;
+    int n_q_heads;
+    int kv_fp32;
+    const CallMeta *meta;  // device copy of the call's row metadata
 };
 
-// y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).
-hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st);
+// y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).  Non-null
+// events are recorded at the start of the first and the end of the last launch (kernel
+// timestamps, no extra stream packets).
+hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start = nullptr,
+                       hipEvent_t ev_stop = nullptr);
 
 struct RopeKvArgs {
     const float *qkv;  // [rows, (Hq + 2 Hkv) d]: q heads, then k heads, then v heads
@@ -59,7 +70,7 @@ struct RopeKvArgs {
     int n_q_heads;
     int kv_fp32;
     int rows;
-    CallMeta meta;
+    const CallMeta *meta; // device copy of the call's row metadata
 };
 hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st);
 
@@ -75,10 +86,15 @@ struct AttnArgs {
     int split_keys;      // keys per split; 0 = one split per row (final output directly)
     int max_splits;      // stride of the partial buffers
     int grid_splits;     // splits launched: ceil(longest context in the call / split_keys)
-    CallMeta meta;
+    int *done;           // [rows, Hkv] split counters, zero between launches (split mode)
+    const CallMeta *meta; // device copy of the call's row metadata
 };
 hipError_t launch_attention(const AttnArgs &a, hipStream_t st);
 bool attention_supported(int group, int head_dim);
+
+// Writes the call's row metadata to device memory (one small launch per call; the hot kernels
+// read it from there instead of carrying it in their arguments).
+hipError_t launch_meta_write(const CallMeta &m, CallMeta *dst, hipStream_t st);
 
 // Writes table[idx[i]] = val[i] for i < n (any n; chunked).
 hipError_t launch_table_write(int *table, const int *idx, const int *val, int n, hipStream_t st);

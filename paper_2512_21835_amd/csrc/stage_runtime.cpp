@@ -38,6 +38,7 @@ using namespace stg;
 namespace {
 
 constexpr int kDecodeSplitKeys = 64;
+constexpr int kMaxContext = 16384;  // decode attention merges at most 256 splits of 64 keys
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -75,6 +76,8 @@ struct stage {
     size_t kv_block_bytes = 0, kv_layer_stride = 0;
     int n_blocks = 0, max_blocks = 0, n_seq_slots = 0;
     int *d_table = nullptr;
+    int *d_done = nullptr;  // [kMaxSeqs, Hkv] split counters of decode attention
+    CallMeta *d_meta = nullptr;  // row metadata of the call in flight
     std::vector<std::vector<int>> tables;
     std::vector<int> lengths;
     std::priority_queue<int, std::vector<int>, std::greater<int>> free_blocks;
@@ -348,7 +351,7 @@ int enqueue_copy(stage *s, int layer, int slot) {
     return STAGE_OK;
 }
 
-int run_layer(stage *s, int layer, const void *blob, int rows, int T, const CallMeta &meta,
+int run_layer(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
               int grid_splits, const float *x_src, float *x_dst) {
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
@@ -358,25 +361,19 @@ int run_layer(stage *s, int layer, const void *blob, int rows, int T, const Call
     q.act = x_src;
     q.act_ld = s->H;
     q.gain = base + s->off_g1 / 2;
-    q.out = s->ws_qkv;
-    q.out_ld = s->qkv_rows;
+    q.out = s->ws_q;
+    q.out_ld = (long)qd;
     q.N = s->qkv_rows;
     q.K = s->H;
     q.rows = rows;
     q.eps = s->cfg.rms_eps;
-    HIP_TRY(launch_gemv(GEMV_NORM_STORE, q, s->cs));
-
-    RopeKvArgs r{};
-    r.qkv = s->ws_qkv;
-    r.q_out = s->ws_q;
-    r.cos_t = s->d_cos;
-    r.sin_t = s->d_sin;
-    r.kv = kv_view(s, layer);
-    r.n_q_heads = s->Hq;
-    r.kv_fp32 = s->cfg.kv_fp32;
-    r.rows = rows;
-    r.meta = meta;
-    HIP_TRY(launch_rope_kv_store(r, s->cs));
+    q.cos_t = s->d_cos;
+    q.sin_t = s->d_sin;
+    q.kv = kv_view(s, layer);
+    q.n_q_heads = s->Hq;
+    q.kv_fp32 = s->cfg.kv_fp32;
+    q.meta = meta;
+    HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
 
     AttnArgs at{};
     at.q = s->ws_q;
@@ -390,6 +387,7 @@ int run_layer(stage *s, int layer, const void *blob, int rows, int T, const Call
     at.split_keys = (T == 1) ? kDecodeSplitKeys : 0;
     at.max_splits = s->max_splits;
     at.grid_splits = grid_splits;
+    at.done = s->d_done;
     at.meta = meta;
     HIP_TRY(launch_attention(at, s->cs));
 
@@ -420,15 +418,12 @@ int run_layer(stage *s, int layer, const void *blob, int rows, int T, const Call
     TimeRec rec{2, layer, nullptr, nullptr};
     const bool t_gu = (s->cfg.timing & STAGE_TIME_GATEUP) != 0;
     if (t_gu) {
-        int rc = record_event(s, s->cs, &rec.a);
-        if (rc) return rc;
+        rec.a = pooled_event(s);
+        rec.b = pooled_event(s);
+        if (!rec.a || !rec.b) return s->fail(STAGE_EHIP, "hipEventCreate failed");
     }
-    HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs));
-    if (t_gu) {
-        int rc = record_event(s, s->cs, &rec.b);
-        if (rc) return rc;
-        s->recs.push_back(rec);
-    }
+    HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
+    if (t_gu) s->recs.push_back(rec);
 
     GemvArgs dn{};
     dn.w = base + s->off_wd / 2;
@@ -510,6 +505,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         max_ctx = std::max(max_ctx, s->lengths[slots[i]]);
     }
     const int grid_splits = (max_ctx + kDecodeSplitKeys - 1) / kDecodeSplitKeys;
+    HIP_TRY(launch_meta_write(meta, s->d_meta, s->cs));
     s->calls++;
     if (decode) s->tok_decode += (long long)rows; else s->tok_prefill += (long long)rows;
 
@@ -543,13 +539,13 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         const float *src = (l == 0) ? x_in : x_out;
         const Layer &ly = s->layers[l];
         if (ly.state == 1) {
-            rc = run_layer(s, l, ly.dev, (int)rows, T, meta, grid_splits, src, x_out);
+            rc = run_layer(s, l, ly.dev, (int)rows, T, s->d_meta, grid_splits, src, x_out);
             if (rc) return rc;
             continue;
         }
         const int sl = slot_of(j);
         HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[sl], 0));
-        rc = run_layer(s, l, s->slots[sl], (int)rows, T, meta, grid_splits, src, x_out);
+        rc = run_layer(s, l, s->slots[sl], (int)rows, T, s->d_meta, grid_splits, src, x_out);
         if (rc) return rc;
         HIP_TRY(hipEventRecord(s->slot_free[sl], s->cs));
         if (j + S < n_str) {
@@ -604,6 +600,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                           c.rope_theta > 0.f && c.rms_eps >= 0.f;
     const bool cap_ok = c.max_microbatches >= 1 && c.max_batch >= 1 &&
                         (long)c.max_microbatches * c.max_batch <= kMaxSeqs && c.max_context >= 1 &&
+                        c.max_context <= kMaxContext &&
                         c.kv_block_tokens == kBlockTokens && c.kv_pool_blocks >= 0 &&
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
@@ -660,11 +657,14 @@ int stage_init(const stage_config *cfg, stage **out) {
     if (hipMalloc(&s->kv_pool, s->kv_layer_stride * s->L) != hipSuccess ||
         hipMalloc(&s->d_table, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
         hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
-        hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess) {
+        hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
+        hipMalloc(&s->d_done, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess ||
+        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);
     }
-    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
+    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
+        hipMemset(s->d_done, 0, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess)
         return cleanup(STAGE_EHIP);
     // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
     const int half = s->D / 2;
@@ -699,7 +699,7 @@ int stage_destroy(stage *s) {
         if (r.b) (void)hipEventDestroy(r.b);
     }
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
-    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_cos, (void *)s->d_sin,
+    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_done, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
         if (p) (void)hipFree(p);
@@ -949,6 +949,12 @@ int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n) {
         s->ev_pool.push_back(r.b);
     }
     s->recs.clear();
+    return STAGE_OK;
+}
+
+int stage_set_timing(stage *s, int32_t flags) {
+    if (!s || (flags & ~(STAGE_TIME_CALLS | STAGE_TIME_GATEUP)) != 0) return STAGE_EINVAL;
+    s->cfg.timing = flags;
     return STAGE_OK;
 }
 

@@ -30,7 +30,7 @@ EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",
     "stage_decode", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
-    "stage_get_demotion_log", "stage_get_timeline", "stage_get_stats", "stage_last_error",
+    "stage_get_demotion_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats", "stage_last_error",
     "stage_strerror",
 )
 
@@ -89,6 +89,7 @@ def lib():
         "stage_get_slot_log": (c_int32, [c_void_p, ip, c_int32, ip]),
         "stage_get_demotion_log": (c_int32, [c_void_p, ip, c_int32, ip]),
         "stage_get_timeline": (c_int32, [c_void_p, POINTER(c_float), c_int32, ip]),
+        "stage_set_timing": (c_int32, [c_void_p, c_int32]),
         "stage_get_stats": (c_int32, [c_void_p, c_char_p, c_int32]),
         "stage_last_error": (c_char_p, [c_void_p]),
         "stage_strerror": (c_char_p, [c_int32]),
@@ -221,6 +222,10 @@ def stage_get_timeline(h) -> List[Tuple[int, int, float, float]]:
     buf = (c_float * (4 * cap))()
     _check(lib().stage_get_timeline(h, buf, cap, ctypes.byref(n)), h)
     return [(int(buf[4 * i]), int(buf[4 * i + 1]), buf[4 * i + 2], buf[4 * i + 3]) for i in range(min(cap, n.value))]
+
+
+def stage_set_timing(h, flags: int) -> None:
+    _check(lib().stage_set_timing(h, flags), h)
 
 
 def stage_get_stats(h) -> dict:
