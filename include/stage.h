@@ -58,6 +58,7 @@ typedef enum {
 /* Timing flags (stage_config.timing). */
 #define STAGE_TIME_CALLS 1   /* events around each prefill/decode call and each slot copy */
 #define STAGE_TIME_GATEUP 2  /* events around each gate/up projection kernel (the largest GEMV) */
+#define STAGE_TIME_LAYERS 4  /* events around each layer's kernels (compute intervals) */
 
 typedef struct {
     /* Layer shape.  hidden, head_dim, ffn and n_q_heads*head_dim must be multiples of 8;
@@ -177,7 +178,8 @@ int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
 /* Timeline recorded under stage_config.timing, then cleared.  Synchronises.  Each record is
-   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel), layer (-1 for a call), start and
+   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel, 3 layer compute), layer (-1 for a
+   call), start and
    end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
 int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
 

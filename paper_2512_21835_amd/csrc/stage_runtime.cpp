@@ -38,7 +38,8 @@ using namespace stg;
 namespace {
 
 constexpr int kDecodeSplitKeys = 64;
-constexpr int kMaxContext = 16384;  // decode attention merges at most 256 splits of 64 keys
+constexpr int kMaxContext = 16384;
+constexpr int kTimeAll = STAGE_TIME_CALLS | STAGE_TIME_GATEUP | STAGE_TIME_LAYERS;  // decode attention merges at most 256 splits of 64 keys
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -351,8 +352,27 @@ int enqueue_copy(stage *s, int layer, int slot) {
     return STAGE_OK;
 }
 
+int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+                      int grid_splits, const float *x_src, float *x_dst);
+
+// One layer's kernels, bracketed by events when STAGE_TIME_LAYERS is set.
 int run_layer(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
               int grid_splits, const float *x_src, float *x_dst) {
+    if (!(s->cfg.timing & STAGE_TIME_LAYERS))
+        return run_layer_kernels(s, layer, blob, rows, T, meta, grid_splits, x_src, x_dst);
+    TimeRec rec{3, layer, nullptr, nullptr};
+    int rc = record_event(s, s->cs, &rec.a);
+    if (rc) return rc;
+    rc = run_layer_kernels(s, layer, blob, rows, T, meta, grid_splits, x_src, x_dst);
+    if (rc) return rc;
+    rc = record_event(s, s->cs, &rec.b);
+    if (rc) return rc;
+    s->recs.push_back(rec);
+    return STAGE_OK;
+}
+
+int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+                      int grid_splits, const float *x_src, float *x_dst) {
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
@@ -605,7 +625,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
-                        (c.timing & ~(STAGE_TIME_CALLS | STAGE_TIME_GATEUP)) == 0;
+                        (c.timing & ~kTimeAll) == 0;
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i)
         if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
@@ -953,7 +973,7 @@ int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n) {
 }
 
 int stage_set_timing(stage *s, int32_t flags) {
-    if (!s || (flags & ~(STAGE_TIME_CALLS | STAGE_TIME_GATEUP)) != 0) return STAGE_EINVAL;
+    if (!s || (flags & ~kTimeAll) != 0) return STAGE_EINVAL;
     s->cfg.timing = flags;
     return STAGE_OK;
 }

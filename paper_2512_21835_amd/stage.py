@@ -25,6 +25,7 @@ STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE = 0
 STAGE_MAX_THRESHOLDS = 32
 STAGE_TIME_CALLS = 1
 STAGE_TIME_GATEUP = 2
+STAGE_TIME_LAYERS = 4
 
 EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",
