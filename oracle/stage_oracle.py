@@ -206,12 +206,26 @@ class OracleStage:
     returns the stage output rows of each, in float64.
     """
 
-    def __init__(self, shape, weights: Callable[[int], Dict[str, np.ndarray]], kv_dtype: str = "bf16"):
+    def __init__(self, shape, weights: Callable[[int], Dict[str, np.ndarray]], kv_dtype: str = "bf16",
+                 kv_jitter: float = 0.0, jitter_seed: int = 0):
         if kv_dtype not in ("bf16", "f32"):
             raise ValueError(kv_dtype)
         self.shape = shape
         self.weights = weights
-        self.kv_round = round_to_bf16 if kv_dtype == "bf16" else round_to_f32
+        base = round_to_bf16 if kv_dtype == "bf16" else round_to_f32
+        if kv_jitter:
+            # Sensitivity of the result to the KV rounding point: every K/V value is scaled by
+            # (1 + kv_jitter * u), u uniform in [-1, 1], before it is rounded to the cache type --
+            # the stage as computed by an arithmetic that is kv_jitter-accurate (relative) up to
+            # the cache store.  Used only to size tolerances; 0 (default) is the plain definition.
+            gen = torch.Generator().manual_seed(jitter_seed)
+
+            def jittered(t: torch.Tensor) -> torch.Tensor:
+                u = torch.rand(t.shape, generator=gen, dtype=F64) * 2.0 - 1.0
+                return base(t * (1.0 + kv_jitter * u))
+            self.kv_round = jittered
+        else:
+            self.kv_round = base
         self.caches: Dict[Hashable, List[LayerCache]] = {}
 
     def cache(self, key: Hashable) -> List[LayerCache]:

@@ -1,0 +1,220 @@
+// Prefill projections on the matrix cores: C[M, N] = A[M, K] . W[N, K]^T with bf16 weights W and
+// an fp32 activation A taken as the exact-sum pair A = hi + lo of two bf16 matrices (hi = bf16(A),
+// lo = bf16(A - hi); the pair keeps ~16 bits of A's mantissa, a single bf16 only 8).  Each 16-wide
+// k step issues v_mfma_f32_32x32x16_bf16 twice per output block, hi then lo, accumulating in fp32.
+//
+// Tiling: a workgroup (4 wavefronts) computes a 128 x 128 tile of C; each wavefront a 64 x 64
+// sub-tile as 2 x 2 blocks of 32 x 32.  K advances 32 at a time through two LDS stages: the next
+// tile's global loads are issued before the current tile's MFMAs and written to the other stage
+// afterwards.  Tiles are stored in LDS in MFMA fragment order (lane l of a fragment at offset
+// 16 l), so every fragment read is one conflict-free ds_read_b128 per lane.  Workgroups that share
+// a weight tile are adjacent in launch order (x over M tiles), so each weight tile is read from HBM
+// once and re-served from L2.
+//
+// The producers of A write the hi/lo pair directly: RMSNorm (before QKV and gate/up), the
+// attention output (before O) and the SwiGLU of the gate/up output (before down).
+#include <hip/hip_runtime.h>
+
+#include "stage_kernels.h"
+
+namespace stg {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int kFrag = (BM / 32) * (BK / 16) * 64;  // 16-byte fragment slots per operand tile (512)
+
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ void split(float v, uint16_t &hi, uint16_t &lo) {
+    hi = to_bf16(v);
+    lo = to_bf16(v - __uint_as_float((uint32_t)hi << 16));
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
+    bf16x8 r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+// LDS slot of 16-byte chunk `ch` (k offset 8 ch) of tile row `row`.
+__device__ __forceinline__ int frag_slot(int row, int ch) {
+    return ((row >> 5) * (BK / 16) + (ch >> 1)) * 64 + (row & 31) + 32 * (ch & 1);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+    __shared__ uint4 lds[2][3][kFrag];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const uint16_t *W = a.w[blockIdx.z];
+    const int M = a.M, N = a.N, K = a.K;
+
+    // global -> register tile load: chunk q = tid + 256 i, row q / 4, 16-byte chunk q % 4
+    uint4 rh[2], rl[2], rw[2];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + 256 * i, row = q >> 2, ch = q & 3, k = k0 + ch * 8;
+            const bool kin = k < K;
+            const int m = m0 + row, n = n0 + row;
+            rh[i] = rl[i] = rw[i] = make_uint4(0, 0, 0, 0);
+            if (kin && m < M) {
+                rh[i] = *reinterpret_cast<const uint4 *>(a.a_hi + (size_t)m * a.lda + k);
+                rl[i] = *reinterpret_cast<const uint4 *>(a.a_lo + (size_t)m * a.lda + k);
+            }
+            if (kin && n < N) rw[i] = *reinterpret_cast<const uint4 *>(W + (size_t)n * K + k);
+        }
+    };
+    auto store = [&](int st) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + 256 * i;
+            const int s = frag_slot(q >> 2, q & 3);
+            lds[st][0][s] = rh[i];
+            lds[st][1][s] = rl[i];
+            lds[st][2][s] = rw[i];
+        }
+    };
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    load(0);
+    store(0);
+    int st = 0;
+    for (int k0 = 0; k0 < K; k0 += BK) {
+        __syncthreads();
+        const bool more = k0 + BK < K;
+        if (more) load(k0 + BK);
+#pragma unroll
+        for (int step = 0; step < BK / 16; ++step) {
+            bf16x8 ah[2], al[2], bw[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int sa = ((wm * 2 + b) * (BK / 16) + step) * 64 + lane;
+                const int sb = ((wn * 2 + b) * (BK / 16) + step) * 64 + lane;
+                ah[b] = as_bf16x8(lds[st][0][sa]);
+                al[b] = as_bf16x8(lds[st][1][sa]);
+                bw[b] = as_bf16x8(lds[st][2][sb]);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bw[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bw[j], acc[i][j], 0, 0, 0);
+                }
+        }
+        if (more) store(st ^ 1);
+        st ^= 1;
+    }
+
+    // result register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the block
+    const int col_off = a.out_col[blockIdx.z];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+            if (n >= N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (m >= M) continue;
+                const size_t o = (size_t)m * a.ldo + col_off + n;
+                if (MODE == GEMM_RESIDUAL)
+                    a.out[o] = a.res[o] + acc[i][j][r];
+                else
+                    a.out[o] = acc[i][j][r];
+            }
+        }
+}
+
+// y = x / sqrt(mean(x^2) + eps) * g, written as a bf16 hi/lo pair.  One workgroup per row.
+__global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, const uint16_t *g, float eps, int H,
+                                                             uint16_t *hi, uint16_t *lo) {
+    const int row = blockIdx.x;
+    const float *xr = x + (size_t)row * H;
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+    __shared__ float red[4];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float tot = ((red[0] + red[1]) + red[2]) + red[3];
+    const float scale = 1.f / sqrtf(tot / (float)H + eps);
+    for (int i = threadIdx.x; i < H; i += 256) {
+        const float y = xr[i] * scale * __uint_as_float((uint32_t)g[i] << 16);
+        split(y, hi[(size_t)row * H + i], lo[(size_t)row * H + i]);
+    }
+}
+
+// hi/lo pair of an fp32 matrix [rows, n] (row stride n).
+__global__ __launch_bounds__(256) void split_kernel(const float *x, size_t count, uint16_t *hi, uint16_t *lo) {
+    for (size_t i = blockIdx.x * 256ull + threadIdx.x; i < count; i += (size_t)gridDim.x * 256)
+        split(x[i], hi[i], lo[i]);
+}
+
+// h = silu(gate) * up from gu [rows, 2F] (gate columns first), written as a hi/lo pair [rows, F].
+__global__ __launch_bounds__(256) void swiglu_split_kernel(const float *gu, int F, size_t rows, uint16_t *hi,
+                                                            uint16_t *lo) {
+    const size_t count = rows * F;
+    for (size_t i = blockIdx.x * 256ull + threadIdx.x; i < count; i += (size_t)gridDim.x * 256) {
+        const size_t r = i / F, f = i % F;
+        const float gt = gu[r * 2 * F + f], up = gu[r * 2 * F + F + f];
+        split(gt / (1.f + expf(-gt)) * up, hi[i], lo[i]);
+    }
+}
+
+int grid_for(size_t count) {
+    const size_t g = (count + 255) / 256;
+    return (int)(g < 8192 ? g : 8192);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) {
+    if (a.M <= 0) return hipSuccess;
+    dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, n_mats);
+    if (mode == GEMM_RESIDUAL)
+        hipLaunchKernelGGL(gemm_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(gemm_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *hi,
+                                uint16_t *lo, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, hi, lo);
+    return hipGetLastError();
+}
+
+hipError_t launch_split(const float *x, size_t count, uint16_t *hi, uint16_t *lo, hipStream_t st) {
+    if (count == 0) return hipSuccess;
+    hipLaunchKernelGGL(split_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, count, hi, lo);
+    return hipGetLastError();
+}
+
+hipError_t launch_swiglu_split(const float *gu, int F, size_t rows, uint16_t *hi, uint16_t *lo, hipStream_t st) {
+    if (rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(swiglu_split_kernel, dim3(grid_for(rows * F)), dim3(256), 0, st, gu, F, rows, hi, lo);
+    return hipGetLastError();
+}
+
+}  // namespace stg

@@ -62,6 +62,28 @@ struct GemvArgs {
 hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start = nullptr,
                        hipEvent_t ev_stop = nullptr);
 
+enum GemmMode { GEMM_STORE = 0, GEMM_RESIDUAL = 1 };
+
+// Prefill projection on the matrix cores: out[m, out_col + n] (+)= sum_k (a_hi + a_lo)[m, k] W[n, k].
+struct GemmArgs {
+    const uint16_t *a_hi, *a_lo;  // [M, K] bf16 pair of the fp32 activation, row stride lda
+    long lda;
+    const uint16_t *w[2];         // [N, K] bf16; grid z selects the matrix
+    float *out;                   // row stride ldo
+    const float *res;             // RESIDUAL: added, same indexing as out
+    long ldo;
+    int out_col[2];               // output column offset of each matrix
+    int M, N, K;
+};
+hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st);
+// y = rmsnorm(x) * g as a bf16 hi/lo pair [rows, H].
+hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *hi,
+                                uint16_t *lo, hipStream_t st);
+// bf16 hi/lo pair of `count` fp32 values.
+hipError_t launch_split(const float *x, size_t count, uint16_t *hi, uint16_t *lo, hipStream_t st);
+// silu(gate) * up of gu [rows, 2F] (gate columns first) as a bf16 hi/lo pair [rows, F].
+hipError_t launch_swiglu_split(const float *gu, int F, size_t rows, uint16_t *hi, uint16_t *lo, hipStream_t st);
+
 struct RopeKvArgs {
     const float *qkv;  // [rows, (Hq + 2 Hkv) d]: q heads, then k heads, then v heads
     float *q_out;      // [rows, Hq d] rotated queries

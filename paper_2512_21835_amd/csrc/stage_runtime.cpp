@@ -87,6 +87,7 @@ struct stage {
 
     size_t ws_rows = 0;
     float *ws_qkv = nullptr, *ws_q = nullptr, *ws_attn = nullptr, *ws_h = nullptr;
+    uint16_t *ws_hi = nullptr, *ws_lo = nullptr;  // bf16 hi/lo pair of a prefill GEMM operand
     size_t part_rows = 0;
     int max_splits = 0;
     float *ws_part_o = nullptr, *ws_part_ml = nullptr;
@@ -236,12 +237,18 @@ int ensure_workspace(stage *s, size_t rows, bool decode) {
     int rc = sync_all(s);
     if (rc) return rc;
     if (rows > s->ws_rows) {
-        for (float *p : {s->ws_qkv, s->ws_q, s->ws_attn, s->ws_h})
+        for (void *p : {(void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
+                        (void *)s->ws_hi, (void *)s->ws_lo})
             if (p) (void)hipFree(p);
         s->ws_qkv = s->ws_q = s->ws_attn = s->ws_h = nullptr;
+        s->ws_hi = s->ws_lo = nullptr;
         s->ws_rows = 0;
         const size_t qd = (size_t)s->Hq * s->D;
-        if (hipMalloc(&s->ws_qkv, rows * s->qkv_rows * sizeof(float)) != hipSuccess ||
+        const size_t wide = std::max<size_t>(s->qkv_rows, 2 * (size_t)s->F);
+        const size_t pair = std::max<size_t>(std::max<size_t>(s->H, qd), s->F);
+        if (hipMalloc(&s->ws_qkv, rows * wide * sizeof(float)) != hipSuccess ||
+            hipMalloc(&s->ws_hi, rows * pair * sizeof(uint16_t)) != hipSuccess ||
+            hipMalloc(&s->ws_lo, rows * pair * sizeof(uint16_t)) != hipSuccess ||
             hipMalloc(&s->ws_q, rows * qd * sizeof(float)) != hipSuccess ||
             hipMalloc(&s->ws_attn, rows * qd * sizeof(float)) != hipSuccess ||
             hipMalloc(&s->ws_h, rows * (size_t)s->F * sizeof(float)) != hipSuccess) {
@@ -371,8 +378,75 @@ int run_layer(stage *s, int layer, const void *blob, int rows, int T, const Call
     return STAGE_OK;
 }
 
+// Prefill (T >= 2): projections on the matrix cores with bf16 hi/lo operand pairs.
+int run_layer_prefill(stage *s, int layer, const void *blob, int rows, const CallMeta *meta, const float *x_src,
+                      float *x_dst) {
+    const uint16_t *base = static_cast<const uint16_t *>(blob);
+    const int H = s->H, F = s->F, qd = s->Hq * s->D;
+    const float eps = s->cfg.rms_eps;
+
+    HIP_TRY(launch_rmsnorm_split(x_src, base + s->off_g1 / 2, eps, rows, H, s->ws_hi, s->ws_lo, s->cs));
+    GemmArgs q{};
+    q.a_hi = s->ws_hi; q.a_lo = s->ws_lo; q.lda = H;
+    q.w[0] = base + s->off_wqkv / 2;
+    q.out = s->ws_qkv; q.ldo = s->qkv_rows;
+    q.M = rows; q.N = s->qkv_rows; q.K = H;
+    HIP_TRY(launch_gemm(GEMM_STORE, q, 1, s->cs));
+
+    RopeKvArgs r{};
+    r.qkv = s->ws_qkv;
+    r.q_out = s->ws_q;
+    r.cos_t = s->d_cos;
+    r.sin_t = s->d_sin;
+    r.kv = kv_view(s, layer);
+    r.n_q_heads = s->Hq;
+    r.kv_fp32 = s->cfg.kv_fp32;
+    r.rows = rows;
+    r.meta = meta;
+    HIP_TRY(launch_rope_kv_store(r, s->cs));
+
+    AttnArgs at{};
+    at.q = s->ws_q;
+    at.out = s->ws_attn;
+    at.kv = kv_view(s, layer);
+    at.n_q_heads = s->Hq;
+    at.kv_fp32 = s->cfg.kv_fp32;
+    at.rows = rows;
+    at.split_keys = 0;
+    at.meta = meta;
+    HIP_TRY(launch_attention(at, s->cs));
+    HIP_TRY(launch_split(s->ws_attn, (size_t)rows * qd, s->ws_hi, s->ws_lo, s->cs));
+
+    GemmArgs o{};
+    o.a_hi = s->ws_hi; o.a_lo = s->ws_lo; o.lda = qd;
+    o.w[0] = base + s->off_wo / 2;
+    o.out = x_dst; o.res = x_src; o.ldo = H;
+    o.M = rows; o.N = H; o.K = qd;
+    HIP_TRY(launch_gemm(GEMM_RESIDUAL, o, 1, s->cs));
+
+    HIP_TRY(launch_rmsnorm_split(x_dst, base + s->off_g2 / 2, eps, rows, H, s->ws_hi, s->ws_lo, s->cs));
+    GemmArgs gu{};
+    gu.a_hi = s->ws_hi; gu.a_lo = s->ws_lo; gu.lda = H;
+    gu.w[0] = base + s->off_wg / 2;
+    gu.w[1] = base + s->off_wu / 2;
+    gu.out = s->ws_qkv; gu.ldo = 2 * (long)F;
+    gu.out_col[0] = 0; gu.out_col[1] = F;
+    gu.M = rows; gu.N = F; gu.K = H;
+    HIP_TRY(launch_gemm(GEMM_STORE, gu, 2, s->cs));
+    HIP_TRY(launch_swiglu_split(s->ws_qkv, F, rows, s->ws_hi, s->ws_lo, s->cs));
+
+    GemmArgs dn{};
+    dn.a_hi = s->ws_hi; dn.a_lo = s->ws_lo; dn.lda = F;
+    dn.w[0] = base + s->off_wd / 2;
+    dn.out = x_dst; dn.res = x_dst; dn.ldo = H;
+    dn.M = rows; dn.N = H; dn.K = F;
+    HIP_TRY(launch_gemm(GEMM_RESIDUAL, dn, 1, s->cs));
+    return STAGE_OK;
+}
+
 int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
                       int grid_splits, const float *x_src, float *x_dst) {
+    if (T >= 2) return run_layer_prefill(s, layer, blob, rows, meta, x_src, x_dst);
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
@@ -721,6 +795,7 @@ int stage_destroy(stage *s) {
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
     for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_done, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
+                    (void *)s->ws_hi, (void *)s->ws_lo,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
         if (p) (void)hipFree(p);
     if (s->own_cs && s->cs) (void)hipStreamDestroy(s->cs);

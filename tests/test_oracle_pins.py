@@ -306,3 +306,13 @@ def test_kv_tail_export_and_reappend_round_trip():
     assert st.length("s") == 5 and k.shape == (2, 4, 1, 4)
     st.append_kv("s", k, v)
     assert np.array_equal(st.forward([("s", nxt)])[0], want)
+
+
+def test_kv_jitter_zero_is_the_plain_definition_and_small_jitter_stays_close():
+    bits = {l: tiny_bits(60 + l) for l in range(2)}
+    x = rand(9, 8, seed=61).numpy()
+    plain = O.OracleStage(TINY3, lambda l: bits[l]).forward([("s", x)])[0]
+    zero = O.OracleStage(TINY3, lambda l: bits[l], kv_jitter=0.0).forward([("s", x)])[0]
+    assert np.array_equal(plain, zero)
+    jit = O.OracleStage(TINY3, lambda l: bits[l], kv_jitter=2.0 ** -16, jitter_seed=3).forward([("s", x)])[0]
+    assert np.abs(jit - plain).max() < 0.05 * np.abs(plain).max()
