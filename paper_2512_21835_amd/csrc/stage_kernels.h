@@ -114,6 +114,23 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs &a, hipStream_t st);
 bool attention_supported(int group, int head_dim);
 
+// One decode layer as one persistent kernel (decode_layer.hip): the four projections and the
+// attention of the per-kernel path, ordered by device-scope phase counters.
+struct DecodeLayerArgs {
+    GemvArgs qkv, o, gu, dn;
+    AttnArgs at;
+    int *phase;          // [6] counters, zero between launches (the kernel resets them)
+    int *abort;          // set when a wait exceeded spin_limit; the host reports and clears it
+    int phase_tasks[5];  // filled by fill_decode_layer_tasks
+    long spin_limit;
+};
+void fill_decode_layer_tasks(DecodeLayerArgs &L);
+bool decode_layer_supported(int rows, int group, int head_dim);
+// Workgroups that can be resident at once (the launch grid).
+hipError_t decode_layer_grid(int rows, int group, int head_dim, bool kv_fp32, int *grid);
+hipError_t launch_decode_layer(const DecodeLayerArgs &L, int grid, hipStream_t st, hipEvent_t e0 = nullptr,
+                               hipEvent_t e1 = nullptr);
+
 // Writes the call's row metadata to device memory (one small launch per call; the hot kernels
 // read it from there instead of carrying it in their arguments).
 hipError_t launch_meta_write(const CallMeta &m, CallMeta *dst, hipStream_t st);

@@ -39,6 +39,8 @@ namespace {
 
 constexpr int kDecodeSplitKeys = 64;
 constexpr int kMaxContext = 16384;
+// Bound of every wait in the per-layer decode kernel (polls of ~1 us; a phase takes < 1 ms).
+constexpr long kSpinLimit = 500000;
 constexpr int kTimeAll = STAGE_TIME_CALLS | STAGE_TIME_GATEUP | STAGE_TIME_LAYERS;  // decode attention merges at most 256 splits of 64 keys
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -79,6 +81,9 @@ struct stage {
     int *d_table = nullptr;
     int *d_done = nullptr;  // [kMaxSeqs, Hkv] split counters of decode attention
     CallMeta *d_meta = nullptr;  // row metadata of the call in flight
+    int *d_phase = nullptr;      // [6] phase counters of the per-layer decode kernel
+    int *d_abort = nullptr;      // its bounded-wait abort flag
+    int dl_grid[3][2] = {};      // its launch grid per (rows, kv_fp32), 0 = not yet computed
     std::vector<std::vector<int>> tables;
     std::vector<int> lengths;
     std::priority_queue<int, std::vector<int>, std::greater<int>> free_blocks;
@@ -450,7 +455,8 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
-    GemvArgs q{};
+    DecodeLayerArgs L{};
+    GemvArgs &q = L.qkv;
     q.w = base + s->off_wqkv / 2;
     q.act = x_src;
     q.act_ld = s->H;
@@ -467,9 +473,8 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     q.n_q_heads = s->Hq;
     q.kv_fp32 = s->cfg.kv_fp32;
     q.meta = meta;
-    HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
 
-    AttnArgs at{};
+    AttnArgs &at = L.at;
     at.q = s->ws_q;
     at.out = s->ws_attn;
     at.part_o = s->ws_part_o;
@@ -478,14 +483,13 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     at.n_q_heads = s->Hq;
     at.kv_fp32 = s->cfg.kv_fp32;
     at.rows = rows;
-    at.split_keys = (T == 1) ? kDecodeSplitKeys : 0;
+    at.split_keys = kDecodeSplitKeys;
     at.max_splits = s->max_splits;
     at.grid_splits = grid_splits;
-    at.done = s->d_done;
+    at.done = nullptr;     // per-kernel path: splits merged by their own launch
     at.meta = meta;
-    HIP_TRY(launch_attention(at, s->cs));
 
-    GemvArgs o{};
+    GemvArgs &o = L.o;
     o.w = base + s->off_wo / 2;
     o.act = s->ws_attn;
     o.act_ld = (long)qd;
@@ -495,9 +499,8 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     o.N = s->H;
     o.K = (int)qd;
     o.rows = rows;
-    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
 
-    GemvArgs gu{};
+    GemvArgs &gu = L.gu;
     gu.w = base + s->off_wg / 2;
     gu.w2 = base + s->off_wu / 2;
     gu.act = x_dst;
@@ -509,17 +512,8 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     gu.K = s->H;
     gu.rows = rows;
     gu.eps = s->cfg.rms_eps;
-    TimeRec rec{2, layer, nullptr, nullptr};
-    const bool t_gu = (s->cfg.timing & STAGE_TIME_GATEUP) != 0;
-    if (t_gu) {
-        rec.a = pooled_event(s);
-        rec.b = pooled_event(s);
-        if (!rec.a || !rec.b) return s->fail(STAGE_EHIP, "hipEventCreate failed");
-    }
-    HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
-    if (t_gu) s->recs.push_back(rec);
 
-    GemvArgs dn{};
+    GemvArgs &dn = L.dn;
     dn.w = base + s->off_wd / 2;
     dn.act = s->ws_h;
     dn.act_ld = s->F;
@@ -529,7 +523,32 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     dn.N = s->H;
     dn.K = s->F;
     dn.rows = rows;
-    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
+
+    // Timed kernel: the whole layer when it runs as one kernel, else the gate/up projection.
+    const bool fused = s->cfg.decode_fusion && decode_layer_supported(rows, s->Hq / s->Hkv, s->D);
+    TimeRec rec{fused ? 4 : 2, layer, nullptr, nullptr};
+    if (s->cfg.timing & STAGE_TIME_GATEUP) {
+        rec.a = pooled_event(s);
+        rec.b = pooled_event(s);
+        if (!rec.a || !rec.b) return s->fail(STAGE_EHIP, "hipEventCreate failed");
+    }
+    if (fused) {
+        at.done = s->d_done;   // the persistent kernel merges splits in the last workgroup
+        int &grid = s->dl_grid[rows][s->cfg.kv_fp32];
+        if (grid == 0) HIP_TRY(decode_layer_grid(rows, s->Hq / s->Hkv, s->D, s->cfg.kv_fp32 != 0, &grid));
+        L.phase = s->d_phase;
+        L.abort = s->d_abort;
+        L.spin_limit = kSpinLimit;
+        fill_decode_layer_tasks(L);
+        HIP_TRY(launch_decode_layer(L, grid, s->cs, rec.a, rec.b));
+    } else {
+        HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
+        HIP_TRY(launch_attention(at, s->cs));
+        HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
+        HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
+        HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
+    }
+    if (rec.a) s->recs.push_back(rec);
     return STAGE_OK;
 }
 
@@ -667,6 +686,7 @@ void stage_config_default(stage_config *cfg) {
     cfg->rms_eps = 1e-5f;
     cfg->kv_block_tokens = kBlockTokens;
     cfg->n_stream_slots = 2;
+    cfg->decode_fusion = 0;
 }
 
 const char *stage_strerror(int32_t status) {
@@ -699,7 +719,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
-                        (c.timing & ~kTimeAll) == 0;
+                        (c.timing & ~kTimeAll) == 0 && (c.decode_fusion == 0 || c.decode_fusion == 1);
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i)
         if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
@@ -753,12 +773,15 @@ int stage_init(const stage_config *cfg, stage **out) {
         hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
         hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
         hipMalloc(&s->d_done, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess ||
-        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess) {
+        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess ||
+        hipMalloc(&s->d_phase, sizeof(int) * 8) != hipSuccess) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);
     }
+    s->d_abort = s->d_phase + 7;
     if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
-        hipMemset(s->d_done, 0, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess)
+        hipMemset(s->d_done, 0, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess ||
+        hipMemset(s->d_phase, 0, sizeof(int) * 8) != hipSuccess)
         return cleanup(STAGE_EHIP);
     // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
     const int half = s->D / 2;
@@ -793,7 +816,7 @@ int stage_destroy(stage *s) {
         if (r.b) (void)hipEventDestroy(r.b);
     }
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
-    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_done, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
+    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_done, (void *)s->d_meta, (void *)s->d_phase, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_hi, (void *)s->ws_lo,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
@@ -974,6 +997,14 @@ int stage_sync(stage *s) {
     int rc = sync_all(s);
     if (rc) return rc;
     HIP_TRY(hipGetLastError());
+    int aborted = 0;
+    HIP_TRY(hipMemcpy(&aborted, s->d_abort, sizeof(int), hipMemcpyDeviceToHost));
+    if (aborted) {
+        HIP_TRY(hipMemset(s->d_abort, 0, sizeof(int)));
+        HIP_TRY(hipMemset(s->d_phase, 0, sizeof(int) * 6));
+        return s->fail(STAGE_EHIP, "a per-layer decode kernel exceeded its wait bound; outputs since the "
+                                   "previous sync are invalid");
+    }
     return STAGE_OK;
 }
 

@@ -82,6 +82,17 @@ def test_round_robin_equals_all_in_one_call_bitwise():
         assert np.array_equal(ga, b.outputs[1 + s].reshape(-1, 256))
 
 
+@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 6), (synth.WORKLOADS["llama8b_stage"], 64, 6)])
+def test_one_kernel_decode_layer_equals_per_projection_kernels(wl, prefill, steps):
+    """The persistent per-layer decode kernel and the per-projection kernels give the same bits."""
+    _gpu()
+    sc = Scenario(wl, prefill=prefill, decode_steps=steps, calls="one")
+    a = run_gpu(dataclasses.replace(sc, decode_fusion=True))
+    b = run_gpu(dataclasses.replace(sc, decode_fusion=False))
+    for x, y in zip(a.outputs, b.outputs):
+        assert np.array_equal(x, y)
+
+
 def test_threshold_demotions_follow_schedule_and_stay_lossless():
     _gpu()
     ths = (39, 40, 41)   # prefill 37: decode rounds 2, 3, 4 each demote one layer (2 layers: 2 demotions)
