@@ -188,6 +188,8 @@ def main() -> int:
     ap.add_argument("--prefill", type=int, default=1024)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one plain 1 GiB device copy first (reference for hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one stage on one GPU; --gpus {args.gpus} is not supported "
@@ -208,6 +210,12 @@ def main() -> int:
     K, W, T = args.steps, args.warmup, args.prefill
     ctx = T + max(K, W)
 
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     t_gen = time.perf_counter()
     weights = [synth.layer_weights(shape, l) for l in range(shape.n_layers)]
     t_gen = time.perf_counter() - t_gen
@@ -250,15 +258,9 @@ def main() -> int:
         P.stage_destroy(h)
 
     step_bytes = sum(decode_step_bytes(shape, T + s) for s in range(K)) / K
-    layer_k = [e - s for kind, _, s, e in tl if kind == 4]
-    if layer_k:   # each decode layer ran as one kernel: that kernel is the timed one
-        kname = "one-kernel decode layer (QKV+RoPE+KV store, attention, O, gate/up+SwiGLU, down)"
-        gu = layer_k
-        gu_bytes = step_bytes / shape.n_layers
-    else:
-        kname = "gate/up projection + SwiGLU (gemv, 1 row)"
-        gu = [e - s for kind, _, s, e in tl if kind == 2]
-        gu_bytes = gateup_bytes(shape, 1)
+    kname = "gate/up projection + SwiGLU (gemv, 1 row)"
+    gu = [e - s for kind, _, s, e in tl if kind == 2]
+    gu_bytes = gateup_bytes(shape, 1)
     gu_ms = sum(gu) / len(gu)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
     ms_step = dt * 1e3 / K

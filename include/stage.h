@@ -57,8 +57,8 @@ typedef enum {
 
 /* Timing flags (stage_config.timing). */
 #define STAGE_TIME_CALLS 1   /* events around each prefill/decode call and each slot copy */
-#define STAGE_TIME_GATEUP 2  /* events around the largest decode kernel of each layer: the whole
-                                layer's kernel when decode_fusion applies, else gate/up */
+#define STAGE_TIME_GATEUP 2  /* events around the gate/up projection kernel of one decode layer
+                                per call (layer = call number mod n_layers) */
 #define STAGE_TIME_LAYERS 4  /* events around each layer's kernels (compute intervals) */
 
 typedef struct {
@@ -87,12 +87,6 @@ typedef struct {
     void *compute_stream; /* hipStream_t for kernels; NULL = the library creates one */
     void *copy_stream;    /* hipStream_t for slot copies; NULL = the library creates one */
     int32_t timing;       /* STAGE_TIME_* flags; 0 = no events */
-    /* 0 (default): one kernel per projection (plus attention and its split merge).  1: a decode
-       layer of up to 2 rows runs as one persistent kernel whose phases (QKV+RoPE, attention, O,
-       gate/up, down) are ordered by device-scope counters.  Both give bit-identical results; on
-       MI355X the per-projection kernels are faster (each phase boundary inside one kernel costs
-       an L2 write-back and invalidate per workgroup, since the XCDs' L2s are not coherent). */
-    int32_t decode_fusion;
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
@@ -185,9 +179,8 @@ int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
 /* Timeline recorded under stage_config.timing, then cleared.  Synchronises.  Each record is
-   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel, 3 layer compute, 4 one-kernel decode
-   layer), layer (-1 for a call), start and
-   end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
+   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel, 3 layer compute), layer (-1 for a
+   call), start and end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
 int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
 
 /* Replaces the STAGE_TIME_* flags of the stage (see stage_config.timing) for later calls. */

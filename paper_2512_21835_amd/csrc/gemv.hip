@@ -1,50 +1,288 @@
-// Per-projection decode kernels (one launch per projection); the device code is in gemv_device.h.
+// Decode projections: y = W x with bf16 weights W [N, K] (row-major), fp32 activations and fp32
+// accumulation, for up to 8 activation rows per launch.
+//
+// Work split.  A workgroup of four wavefronts owns R units over the whole K range.  A unit is one
+// output row, or a pair of rows that the epilogue needs together: (gate row f, up row f) for
+// SwiGLU, (row i, row i + d/2) of one head for rotate-half RoPE.  K is cut into steps of 512
+// (1 KiB of bf16 per row); wavefront w takes steps w, w + 4, w + 8, ... of every owned row, lane l
+// reading 16 bytes at k = 512 s + 8 l of step s.  Splitting K across the wavefronts (instead of
+// giving each wavefront whole rows) lets one activation load serve all R units and leaves each
+// wavefront a quarter of the dependent load round trips; U steps are loaded before they are used.
+// Each wavefront reduces its lane partial sums with a butterfly of shuffles, the four wavefront
+// partials meet in LDS, and wavefront 0 runs the epilogue.
+//
+// Fused: the RMSNorm in front of the QKV and gate/up projections (the sum of squares of x comes
+// from the same activation loads; the 1/rms scale is applied to the finished dot product), RoPE and
+// the KV-cache store after the QKV projection, SwiGLU of the gate/up pair, and the residual add
+// after the O and down projections.
+//
+// Arithmetic of one output element (and of one row's sum of squares): per wavefront, per lane, a
+// chain of fused multiply-adds over the wavefront's steps in ascending k; one fixed butterfly; then
+// the partials of wavefronts 0, 1, 2, 3 added in that order.  R, U and M only decide which
+// workgroup computes what and how loads are batched, so results do not depend on how many
+// micro-batches share a call.
 #include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
 
-#include "gemv_device.h"
+#include "stage_kernels.h"
 
 namespace stg {
 namespace {
 
-using namespace gemv_dev;
+constexpr int kWaves = 4;
+constexpr int kStep = 512;  // k per wavefront step (64 lanes x 8 bf16)
 constexpr int kMaxRowsPerLaunch = 8;
 
-template <int M, int R, int MODE>
-__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
-    const Prefetch<MODE, R, 1> none{};
-    gemv_wave<M, R, MODE, 1>(a, (blockIdx.x * kWaves + (threadIdx.x >> 6)) * R, false, none);
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte weight load marked non-temporal: weights are streamed once per call.
+__device__ __forceinline__ uint4 load_stream16(const uint16_t *p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-template <int M, int R, int MODE>
-void launch_one(const GemvArgs &c, int grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    if (e0 || e1)
-        hipExtLaunchKernelGGL((gemv_kernel<M, R, MODE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+__device__ __forceinline__ float bf16lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+__device__ __forceinline__ void unpack8(const uint4 &v, float f[8]) {
+    f[0] = bf16lo(v.x); f[1] = bf16hi(v.x);
+    f[2] = bf16lo(v.y); f[3] = bf16hi(v.y);
+    f[4] = bf16lo(v.z); f[5] = bf16hi(v.z);
+    f[6] = bf16lo(v.w); f[7] = bf16hi(v.w);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <int MODE> struct Shape {
+    static constexpr bool kNorm = MODE != GEMV_PLAIN_RESIDUAL;
+    static constexpr int NW = MODE == GEMV_PLAIN_RESIDUAL ? 1 : 2;  // weight rows per unit
+};
+
+template <int MODE>
+__device__ __forceinline__ int n_units(const GemvArgs &a) {
+    return MODE == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
+}
+
+// Weight row w (0 or 1) of unit u.
+template <int MODE>
+__device__ __forceinline__ const uint16_t *unit_row(const GemvArgs &a, int u, int w) {
+    if (MODE == GEMV_NORM_ROPE_KV) {
+        const int half = a.kv.head_dim / 2;
+        const int h = u / half, i = u % half;
+        return a.w + (size_t)(h * a.kv.head_dim + i + w * half) * a.K;
+    }
+    if (MODE == GEMV_NORM_SWIGLU) return (w ? a.w2 : a.w) + (size_t)u * a.K;
+    return a.w + (size_t)u * a.K;
+}
+
+__device__ __forceinline__ void store_kv(void *pool, size_t e, float v, int kv_fp32) {
+    if (kv_fp32)
+        static_cast<float *>(pool)[e] = v;
     else
-        hipLaunchKernelGGL((gemv_kernel<M, R, MODE>), dim3(grid), dim3(256), 0, st, c);
+        static_cast<uint16_t *>(pool)[e] = to_bf16(v);
 }
 
-template <int MODE, int R>
-hipError_t launch_mode(GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
-    const int units = MODE == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
-    const int grid = (units + kWaves * R - 1) / (kWaves * R);
-    const int total = a.rows;
-    for (int r0 = 0; r0 < total; r0 += kMaxRowsPerLaunch) {
+// RoPE + KV store of one (row i, row i + d/2) pair of head h for activation row m.  Heads below Hq
+// are queries (rotated, to out), the next Hkv keys (rotated, to the cache), the last Hkv values.
+__device__ __forceinline__ void rope_kv_epilogue(const GemvArgs &a, int u, int m, float x1, float x2) {
+    const int d = a.kv.head_dim, half = d / 2;
+    const int h = u / half, i = u % half;
+    const int row = a.row0 + m;
+    const int sidx = row / a.meta->rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+    const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
+    float r1 = x1, r2 = x2;
+    if (h < hq + hkv) {
+        const float c = a.cos_t[(size_t)pos * half + i], s = a.sin_t[(size_t)pos * half + i];
+        r1 = x1 * c - x2 * s;
+        r2 = x1 * s + x2 * c;
+    }
+    if (h < hq) {
+        float *q = a.out + m * a.out_ld + h * d;
+        q[i] = r1;
+        q[i + half] = r2;
+        return;
+    }
+    const int slot = a.meta->seq_slot[sidx];
+    const int block = a.kv.block_table[(size_t)slot * a.kv.max_blocks + pos / kBlockTokens];
+    const int kv = h < hq + hkv ? 0 : 1;
+    const int g = h - hq - kv * hkv;
+    const size_t e = (((size_t)block * 2 + kv) * hkv + g) * kBlockTokens * d +
+                     (size_t)(pos % kBlockTokens) * d + i;
+    store_kv(a.kv.pool, e, r1, a.kv_fp32);
+    store_kv(a.kv.pool, e + half, r2, a.kv_fp32);
+}
+
+// One workgroup: units blockIdx.x * R .. + R - 1 for the launch's a.rows (<= M) activation rows.
+template <int M, int R, int U, int MODE>
+__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+    constexpr bool kNorm = Shape<MODE>::kNorm;
+    constexpr int NW = Shape<MODE>::NW;
+    constexpr int NP = NW * R * M + (kNorm ? M : 0);  // partials per wavefront
+    __shared__ float part[kWaves][NP];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int units = n_units<MODE>(a);
+    const int unit0 = blockIdx.x * R;
+    const int K = a.K, steps = (K + kStep - 1) / kStep, rows = a.rows;
+
+    // rows of units past the last are clamped to it: their loads stay in bounds, results are dropped
+    const uint16_t *wrow[NW][R];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int r = 0; r < R; ++r) wrow[w][r] = unit_row<MODE>(a, min(unit0 + r, units - 1), w);
+
+    float acc[NW][R][M];
+    float ss[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+        ss[m] = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[w][r][m] = 0.f;
+    }
+
+    for (int s0 = wave; s0 < steps; s0 += kWaves * U) {
+        uint4 wv[U][NW][R];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = s0 + kWaves * u, k = s * kStep + lane * 8;
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    wv[u][w][r] = (s < steps && k < K) ? load_stream16(wrow[w][r] + k) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = s0 + kWaves * u, k = s * kStep + lane * 8;
+            if (s >= steps || k >= K) break;
+            float g[8];
+            if (kNorm) unpack8(*reinterpret_cast<const uint4 *>(a.gain + k), g);
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                if (m >= rows) break;
+                const float4 *xp = reinterpret_cast<const float4 *>(a.act + m * a.act_ld + k);
+                const float4 x0 = xp[0], x1 = xp[1];
+                float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+                if (kNorm) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        ss[m] = fmaf(x[j], x[j], ss[m]);
+                        x[j] = x[j] * g[j];
+                    }
+                }
+#pragma unroll
+                for (int w = 0; w < NW; ++w)
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        float f[8];
+                        unpack8(wv[u][w][r], f);
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) acc[w][r][m] = fmaf(f[j], x[j], acc[w][r][m]);
+                    }
+            }
+        }
+    }
+
+    // wavefront partials -> LDS, laid out [w][r][m] then the sums of squares [m]
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                const float v = wave_sum(acc[w][r][m]);
+                if (lane == 0) part[wave][(w * R + r) * M + m] = v;
+            }
+    if (kNorm) {
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+            const float v = wave_sum(ss[m]);
+            if (lane == 0) part[wave][NW * R * M + m] = v;
+        }
+    }
+    __syncthreads();
+
+    // epilogue: lane r * M + m of wavefront 0 finishes unit unit0 + r of activation row m
+    if (wave != 0 || lane >= R * M) return;
+    const int r = lane / M, m = lane % M, u = unit0 + r;
+    if (u >= units || m >= rows) return;
+    auto total = [&](int i) { return ((part[0][i] + part[1][i]) + part[2][i]) + part[3][i]; };
+    float scale = 1.f;
+    if (kNorm) scale = 1.f / sqrtf(total(NW * R * M + m) / (float)K + a.eps);
+    const float y0 = total(r * M + m) * scale;
+    if (MODE == GEMV_NORM_ROPE_KV) {
+        rope_kv_epilogue(a, u, m, y0, total((R + r) * M + m) * scale);
+    } else if (MODE == GEMV_PLAIN_RESIDUAL) {
+        a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
+    } else {
+        const float up = total((R + r) * M + m) * scale;
+        a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
+    }
+}
+
+int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
+
+template <int M, int R, int U, int MODE>
+void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    const int grid = (host_units(MODE, c) + R - 1) / R;
+    if (e0 || e1)
+        hipExtLaunchKernelGGL((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+    else
+        hipLaunchKernelGGL((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, c);
+}
+
+// Units per workgroup and steps in flight, by mode and rows (measured on the 8B- and 70B-shaped
+// layers): four units and two steps where registers allow, fewer as the rows multiply them.
+template <int M, int MODE>
+void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    if (MODE == GEMV_PLAIN_RESIDUAL) {
+        if (M <= 2) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
+        else launch_one<M, 4, 1, MODE>(c, st, e0, e1);
+    } else if (MODE == GEMV_NORM_SWIGLU) {
+        if (M <= 2) launch_one<M, 4, 1, MODE>(c, st, e0, e1);
+        else launch_one<M, 2, 1, MODE>(c, st, e0, e1);
+    } else {
+        const bool big = (long)host_units(MODE, c) * c.K >= 40L * 1000 * 1000;
+        if (M <= 2 && big) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
+        else launch_one<M, 2, 1, MODE>(c, st, e0, e1);
+    }
+}
+
+template <int MODE>
+hipError_t launch_mode(const GemvArgs &a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
+    for (int r0 = 0; r0 < a.rows; r0 += kMaxRowsPerLaunch) {
         GemvArgs c = a;
-        c.rows = min(kMaxRowsPerLaunch, total - r0);
+        c.rows = min(kMaxRowsPerLaunch, a.rows - r0);
         c.row0 = a.row0 + r0;
         c.act = a.act + (size_t)r0 * a.act_ld;
         c.out = a.out + (size_t)r0 * a.out_ld;
         if (a.res) c.res = a.res + (size_t)r0 * a.out_ld;
         hipEvent_t e0 = r0 == 0 ? ev_start : nullptr;
-        hipEvent_t e1 = r0 + kMaxRowsPerLaunch >= total ? ev_stop : nullptr;
+        hipEvent_t e1 = r0 + kMaxRowsPerLaunch >= a.rows ? ev_stop : nullptr;
         if (c.rows == 1)
-            launch_one<1, R, MODE>(c, grid, st, e0, e1);
+            launch_rows<1, MODE>(c, st, e0, e1);
         else if (c.rows == 2)
-            launch_one<2, R, MODE>(c, grid, st, e0, e1);
+            launch_rows<2, MODE>(c, st, e0, e1);
         else if (c.rows <= 4)
-            launch_one<4, R, MODE>(c, grid, st, e0, e1);
+            launch_rows<4, MODE>(c, st, e0, e1);
         else
-            launch_one<8, R, MODE>(c, grid, st, e0, e1);
+            launch_rows<8, MODE>(c, st, e0, e1);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -55,24 +293,11 @@ hipError_t launch_mode(GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent
 
 hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (a.rows <= 0) return hipSuccess;
-    // Two units per wavefront pay off once a matrix is large (measured on the 70B-shaped layer:
-    // one unit per wavefront leaves the long rows of the down projection short of loads in
-    // flight); one unit per wavefront keeps more wavefronts busy on the smaller ones.
-    const long units = mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N;
-    const bool big = units * (long)a.K >= 200L * 1000 * 1000;
+    if (a.K <= 0 || a.K % 8 != 0 || a.N <= 0) return hipErrorInvalidValue;
     switch (mode) {
-        case GEMV_NORM_STORE:
-            return big ? launch_mode<GEMV_NORM_STORE, 2>(a, st, ev_start, ev_stop)
-                       : launch_mode<GEMV_NORM_STORE, 1>(a, st, ev_start, ev_stop);
-        case GEMV_PLAIN_RESIDUAL:
-            return big ? launch_mode<GEMV_PLAIN_RESIDUAL, 2>(a, st, ev_start, ev_stop)
-                       : launch_mode<GEMV_PLAIN_RESIDUAL, 1>(a, st, ev_start, ev_stop);
-        case GEMV_NORM_SWIGLU:
-            return big ? launch_mode<GEMV_NORM_SWIGLU, 2>(a, st, ev_start, ev_stop)
-                       : launch_mode<GEMV_NORM_SWIGLU, 1>(a, st, ev_start, ev_stop);
-        case GEMV_NORM_ROPE_KV:
-            return big ? launch_mode<GEMV_NORM_ROPE_KV, 2>(a, st, ev_start, ev_stop)
-                       : launch_mode<GEMV_NORM_ROPE_KV, 1>(a, st, ev_start, ev_stop);
+        case GEMV_PLAIN_RESIDUAL: return launch_mode<GEMV_PLAIN_RESIDUAL>(a, st, ev_start, ev_stop);
+        case GEMV_NORM_SWIGLU: return launch_mode<GEMV_NORM_SWIGLU>(a, st, ev_start, ev_stop);
+        case GEMV_NORM_ROPE_KV: return launch_mode<GEMV_NORM_ROPE_KV>(a, st, ev_start, ev_stop);
         default: return hipErrorInvalidValue;
     }
 }

@@ -30,7 +30,6 @@ struct KvView {
 };
 
 enum GemvMode {
-    GEMV_NORM_STORE = 0,     // out = W (rmsnorm(act) * gain)
     GEMV_PLAIN_RESIDUAL = 1, // out = res + W act
     GEMV_NORM_SWIGLU = 2,    // out = silu(Wg y) * (Wu y), y = rmsnorm(act) * gain
     GEMV_NORM_ROPE_KV = 3    // [q | k | v] = Wqkv y; rotate q, k; q -> q_out, k and v -> KV cache
@@ -56,9 +55,9 @@ struct GemvArgs {
     const CallMeta *meta;  // device copy of the call's row metadata
 };
 
-// y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).  Non-null
-// events are recorded at the start of the first and the end of the last launch (kernel
-// timestamps, no extra stream packets).
+// y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).  K must be a
+// multiple of 8.  Non-null events are recorded at the start of the first and the end of the last
+// launch (kernel timestamps, no extra stream packets).
 hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start = nullptr,
                        hipEvent_t ev_stop = nullptr);
 
@@ -108,28 +107,10 @@ struct AttnArgs {
     int split_keys;      // keys per split; 0 = one split per row (final output directly)
     int max_splits;      // stride of the partial buffers
     int grid_splits;     // splits launched: ceil(longest context in the call / split_keys)
-    int *done;           // [rows, Hkv] split counters, zero between launches (split mode)
     const CallMeta *meta; // device copy of the call's row metadata
 };
 hipError_t launch_attention(const AttnArgs &a, hipStream_t st);
 bool attention_supported(int group, int head_dim);
-
-// One decode layer as one persistent kernel (decode_layer.hip): the four projections and the
-// attention of the per-kernel path, ordered by device-scope phase counters.
-struct DecodeLayerArgs {
-    GemvArgs qkv, o, gu, dn;
-    AttnArgs at;
-    int *phase;          // [6] counters, zero between launches (the kernel resets them)
-    int *abort;          // set when a wait exceeded spin_limit; the host reports and clears it
-    int phase_tasks[5];  // filled by fill_decode_layer_tasks
-    long spin_limit;
-};
-void fill_decode_layer_tasks(DecodeLayerArgs &L);
-bool decode_layer_supported(int rows, int group, int head_dim);
-// Workgroups that can be resident at once (the launch grid).
-hipError_t decode_layer_grid(int rows, int group, int head_dim, bool kv_fp32, int *grid);
-hipError_t launch_decode_layer(const DecodeLayerArgs &L, int grid, hipStream_t st, hipEvent_t e0 = nullptr,
-                               hipEvent_t e1 = nullptr);
 
 // Writes the call's row metadata to device memory (one small launch per call; the hot kernels
 // read it from there instead of carrying it in their arguments).

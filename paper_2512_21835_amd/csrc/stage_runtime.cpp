@@ -38,10 +38,8 @@ using namespace stg;
 namespace {
 
 constexpr int kDecodeSplitKeys = 64;
-constexpr int kMaxContext = 16384;
-// Bound of every wait in the per-layer decode kernel (polls of ~1 us; a phase takes < 1 ms).
-constexpr long kSpinLimit = 500000;
-constexpr int kTimeAll = STAGE_TIME_CALLS | STAGE_TIME_GATEUP | STAGE_TIME_LAYERS;  // decode attention merges at most 256 splits of 64 keys
+constexpr int kMaxContext = 16384;  // decode attention merges at most 256 splits of 64 keys
+constexpr int kTimeAll = STAGE_TIME_CALLS | STAGE_TIME_GATEUP | STAGE_TIME_LAYERS;
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -79,11 +77,7 @@ struct stage {
     size_t kv_block_bytes = 0, kv_layer_stride = 0;
     int n_blocks = 0, max_blocks = 0, n_seq_slots = 0;
     int *d_table = nullptr;
-    int *d_done = nullptr;  // [kMaxSeqs, Hkv] split counters of decode attention
     CallMeta *d_meta = nullptr;  // row metadata of the call in flight
-    int *d_phase = nullptr;      // [6] phase counters of the per-layer decode kernel
-    int *d_abort = nullptr;      // its bounded-wait abort flag
-    int dl_grid[3][2] = {};      // its launch grid per (rows, kv_fp32), 0 = not yet computed
     std::vector<std::vector<int>> tables;
     std::vector<int> lengths;
     std::priority_queue<int, std::vector<int>, std::greater<int>> free_blocks;
@@ -455,8 +449,7 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
-    DecodeLayerArgs L{};
-    GemvArgs &q = L.qkv;
+    GemvArgs q{};
     q.w = base + s->off_wqkv / 2;
     q.act = x_src;
     q.act_ld = s->H;
@@ -474,7 +467,7 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     q.kv_fp32 = s->cfg.kv_fp32;
     q.meta = meta;
 
-    AttnArgs &at = L.at;
+    AttnArgs at{};
     at.q = s->ws_q;
     at.out = s->ws_attn;
     at.part_o = s->ws_part_o;
@@ -486,10 +479,9 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     at.split_keys = kDecodeSplitKeys;
     at.max_splits = s->max_splits;
     at.grid_splits = grid_splits;
-    at.done = nullptr;     // per-kernel path: splits merged by their own launch
     at.meta = meta;
 
-    GemvArgs &o = L.o;
+    GemvArgs o{};
     o.w = base + s->off_wo / 2;
     o.act = s->ws_attn;
     o.act_ld = (long)qd;
@@ -500,7 +492,7 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     o.K = (int)qd;
     o.rows = rows;
 
-    GemvArgs &gu = L.gu;
+    GemvArgs gu{};
     gu.w = base + s->off_wg / 2;
     gu.w2 = base + s->off_wu / 2;
     gu.act = x_dst;
@@ -513,7 +505,7 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     gu.rows = rows;
     gu.eps = s->cfg.rms_eps;
 
-    GemvArgs &dn = L.dn;
+    GemvArgs dn{};
     dn.w = base + s->off_wd / 2;
     dn.act = s->ws_h;
     dn.act_ld = s->F;
@@ -524,30 +516,19 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     dn.K = s->F;
     dn.rows = rows;
 
-    // Timed kernel: the whole layer when it runs as one kernel, else the gate/up projection.
-    const bool fused = s->cfg.decode_fusion && decode_layer_supported(rows, s->Hq / s->Hkv, s->D);
-    TimeRec rec{fused ? 4 : 2, layer, nullptr, nullptr};
-    if (s->cfg.timing & STAGE_TIME_GATEUP) {
+    // Timed kernel: the gate/up projection of one layer per call (rotating), so that the events
+    // barely perturb the step.
+    TimeRec rec{2, layer, nullptr, nullptr};
+    if ((s->cfg.timing & STAGE_TIME_GATEUP) && layer == (int)((s->calls - 1) % s->L)) {
         rec.a = pooled_event(s);
         rec.b = pooled_event(s);
         if (!rec.a || !rec.b) return s->fail(STAGE_EHIP, "hipEventCreate failed");
     }
-    if (fused) {
-        at.done = s->d_done;   // the persistent kernel merges splits in the last workgroup
-        int &grid = s->dl_grid[rows][s->cfg.kv_fp32];
-        if (grid == 0) HIP_TRY(decode_layer_grid(rows, s->Hq / s->Hkv, s->D, s->cfg.kv_fp32 != 0, &grid));
-        L.phase = s->d_phase;
-        L.abort = s->d_abort;
-        L.spin_limit = kSpinLimit;
-        fill_decode_layer_tasks(L);
-        HIP_TRY(launch_decode_layer(L, grid, s->cs, rec.a, rec.b));
-    } else {
-        HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
-        HIP_TRY(launch_attention(at, s->cs));
-        HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
-        HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
-        HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
-    }
+    HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
+    HIP_TRY(launch_attention(at, s->cs));
+    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
+    HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
+    HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
     if (rec.a) s->recs.push_back(rec);
     return STAGE_OK;
 }
@@ -686,7 +667,6 @@ void stage_config_default(stage_config *cfg) {
     cfg->rms_eps = 1e-5f;
     cfg->kv_block_tokens = kBlockTokens;
     cfg->n_stream_slots = 2;
-    cfg->decode_fusion = 0;
 }
 
 const char *stage_strerror(int32_t status) {
@@ -719,7 +699,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
-                        (c.timing & ~kTimeAll) == 0 && (c.decode_fusion == 0 || c.decode_fusion == 1);
+                        (c.timing & ~kTimeAll) == 0;
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i)
         if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
@@ -772,16 +752,11 @@ int stage_init(const stage_config *cfg, stage **out) {
         hipMalloc(&s->d_table, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
         hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
         hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
-        hipMalloc(&s->d_done, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess ||
-        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess ||
-        hipMalloc(&s->d_phase, sizeof(int) * 8) != hipSuccess) {
+        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);
     }
-    s->d_abort = s->d_phase + 7;
-    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
-        hipMemset(s->d_done, 0, sizeof(int) * (size_t)kMaxSeqs * s->Hkv) != hipSuccess ||
-        hipMemset(s->d_phase, 0, sizeof(int) * 8) != hipSuccess)
+    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
         return cleanup(STAGE_EHIP);
     // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
     const int half = s->D / 2;
@@ -816,7 +791,7 @@ int stage_destroy(stage *s) {
         if (r.b) (void)hipEventDestroy(r.b);
     }
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
-    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_done, (void *)s->d_meta, (void *)s->d_phase, (void *)s->d_cos, (void *)s->d_sin,
+    for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_hi, (void *)s->ws_lo,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
@@ -997,14 +972,6 @@ int stage_sync(stage *s) {
     int rc = sync_all(s);
     if (rc) return rc;
     HIP_TRY(hipGetLastError());
-    int aborted = 0;
-    HIP_TRY(hipMemcpy(&aborted, s->d_abort, sizeof(int), hipMemcpyDeviceToHost));
-    if (aborted) {
-        HIP_TRY(hipMemset(s->d_abort, 0, sizeof(int)));
-        HIP_TRY(hipMemset(s->d_phase, 0, sizeof(int) * 6));
-        return s->fail(STAGE_EHIP, "a per-layer decode kernel exceeded its wait bound; outputs since the "
-                                   "previous sync are invalid");
-    }
     return STAGE_OK;
 }
 

@@ -61,7 +61,6 @@ class Scenario:
     thresholds: Tuple[int, ...] = ()
     max_context: Optional[int] = None
     timing: int = 0
-    decode_fusion: bool = False
 
     @property
     def shape(self):
@@ -152,7 +151,7 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle) -> RunResult:
     cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=sc.ctx(),
                        n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
                        thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
-                       copy_stream=copy_stream.cuda_stream, timing=sc.timing, decode_fusion=sc.decode_fusion)
+                       copy_stream=copy_stream.cuda_stream, timing=sc.timing)
     h = P.stage_init(cfg)
     res = RunResult()
     try:

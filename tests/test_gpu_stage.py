@@ -19,6 +19,9 @@ TOL_ABS = 2e-2
 TOL_COS = 0.9995
 
 TINY_RAGGED = synth.Workload("tiny_ragged", 100, synth.TINY, n_mb=3, batch=2, prefill=37, decode_steps=20)
+# 8B-shaped layers, 3 micro-batches of batch 3: 9 rows per call when all share it, 3 otherwise
+LLAMA8B_MULTI = synth.Workload("llama8b_multi", 101, synth.LLAMA8B_STAGE, n_mb=3, batch=3, prefill=24,
+                               decode_steps=3)
 
 
 def _gpu():
@@ -69,28 +72,20 @@ def test_streamed_layers_are_lossless(slots):
     assert got.stats["layer_loads"] == 2 * len(sc.call_plan())
 
 
-def test_round_robin_equals_all_in_one_call_bitwise():
-    """Per-row arithmetic does not depend on how many micro-batches share a call."""
+@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 4), (LLAMA8B_MULTI, 24, 3)])
+def test_round_robin_equals_all_in_one_call_bitwise(wl, prefill, steps):
+    """Per-row arithmetic does not depend on how many micro-batches share a call (the decode
+    projections take other launch shapes for 1-2, 3-4 and 5-8 rows and split calls of more
+    than 8 rows into several launches)."""
     _gpu()
-    a = run_gpu(Scenario(TINY_RAGGED, prefill=37, decode_steps=4, calls="one"))
-    b = run_gpu(Scenario(TINY_RAGGED, prefill=37, decode_steps=4, calls="all"))
-    ga = np.concatenate([o.reshape(-1, 256) for o in a.outputs[:3]])
-    gb = b.outputs[0].reshape(-1, 256)
-    assert np.array_equal(ga, gb)
-    for s in range(4):
-        ga = np.concatenate([o.reshape(-1, 256) for o in a.outputs[3 + 3 * s: 6 + 3 * s]])
-        assert np.array_equal(ga, b.outputs[1 + s].reshape(-1, 256))
-
-
-@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 6), (synth.WORKLOADS["llama8b_stage"], 64, 6)])
-def test_one_kernel_decode_layer_equals_per_projection_kernels(wl, prefill, steps):
-    """The persistent per-layer decode kernel and the per-projection kernels give the same bits."""
-    _gpu()
-    sc = Scenario(wl, prefill=prefill, decode_steps=steps, calls="one")
-    a = run_gpu(dataclasses.replace(sc, decode_fusion=True))
-    b = run_gpu(dataclasses.replace(sc, decode_fusion=False))
-    for x, y in zip(a.outputs, b.outputs):
-        assert np.array_equal(x, y)
+    a = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="one"))
+    b = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="all"))
+    H, n = wl.shape.hidden, wl.n_mb
+    ga = np.concatenate([o.reshape(-1, H) for o in a.outputs[:n]])
+    assert np.array_equal(ga, b.outputs[0].reshape(-1, H))
+    for s in range(steps):
+        ga = np.concatenate([o.reshape(-1, H) for o in a.outputs[n + n * s: 2 * n + n * s]])
+        assert np.array_equal(ga, b.outputs[1 + s].reshape(-1, H))
 
 
 def test_threshold_demotions_follow_schedule_and_stay_lossless():
