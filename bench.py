@@ -26,6 +26,15 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, published
+
+# HBM bytes of one gate/up launch (8B-shaped layer, 1 row), from two rocprofv3 --pmc runs of this
+# script (FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by what the counter reads for a
+# plain 1 GiB device copy in the same run).  Valid for the GEMV source it was taken on: with any
+# other source the field is reported as null.
+GATEUP_TRAFFIC = {"bytes": 235253037,
+                  "source_sha256": "36f3032d5f926561a6cd48e07a2a345c4a23c821d27e6a136efc344347fffc72"}
+KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
 
 def gateup_bytes(shape, rows: int) -> int:
@@ -45,6 +54,24 @@ def decode_step_bytes(shape, ctx_before: int) -> int:
     kv = (ctx_before + 1) * 2 * kvd * 2 + 2 * kvd * 2
     acts = 4 * (h + (qd + 2 * kvd) + qd + qd + h + h + 2 * h + f + f + 2 * h)
     return shape.n_layers * (weights + kv + acts)
+
+
+def kernel_source_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def prefill_flops(shape, T: int):
+    """Algorithmic flops of a T-token prefill of one sequence: (projection GEMMs, causal attention)."""
+    h, f, qd, kvd = shape.hidden, shape.ffn, shape.q_dim, shape.kv_dim
+    params = h * (qd + 2 * kvd) + qd * h + 2 * f * h + f * h
+    gemm = 2 * params * T * shape.n_layers
+    attn = 4 * (T * (T + 1) // 2) * shape.n_q_heads * shape.head_dim * shape.n_layers
+    return gemm, attn
 
 
 def cpu_baseline(shape, weights, wl, n_tokens: int):
@@ -180,6 +207,16 @@ def offload_leg(calls: int, ctx: int = 2048):
     }
 
 
+def prefill_report(shape, T: int, seconds: float):
+    gemm, attn = prefill_flops(shape, T)
+    peak = MFMA_BF16_PEAK_TFLOPS * 1e12 * seconds
+    return {"tokens": T, "tokens_per_s": T / seconds, "ms": seconds * 1e3,
+            "tflop_algorithmic": (gemm + attn) / 1e12,
+            # algorithmic flops against the bf16 matrix peak; the projections issue two MFMAs per
+            # product (the fp32 activation as a bf16 hi/lo pair), attention runs on the vector units
+            "mfma_frac_algorithmic": (gemm + attn) / peak, "mfma_frac_issued": 2 * gemm / peak}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -258,6 +295,7 @@ def main() -> int:
         P.stage_destroy(h)
 
     step_bytes = sum(decode_step_bytes(shape, T + s) for s in range(K)) / K
+    traffic = GATEUP_TRAFFIC["bytes"] if GATEUP_TRAFFIC["source_sha256"] == kernel_source_sha256() else None
     kname = "gate/up projection + SwiGLU (gemv, 1 row)"
     gu = [e - s for kind, _, s, e in tl if kind == 2]
     gu_bytes = gateup_bytes(shape, 1)
@@ -275,11 +313,11 @@ def main() -> int:
                    "weights": "bf16", "kv_cache": "bf16", "accumulate": "f32"},
         "roofline": {"bound": "hbm", "kernel": kname,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "bytes_per_launch": gu_bytes, "avg_launch_ms": gu_ms, "launches": len(gu)},
+                     "traffic": traffic, "bytes_per_launch": gu_bytes, "avg_launch_ms": gu_ms, "launches": len(gu)},
         "step_hbm": {"bytes_per_step": step_bytes, "achieved_GBs": step_bytes / (ms_step * 1e-3) / 1e9,
                      "frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS},
         "host_enqueue_ms_per_step": t_enq * 1e3 / K,
-        "prefill": {"tokens": T, "tokens_per_s": T / prefill_s, "ms": prefill_s * 1e3},
+        "prefill": prefill_report(shape, T, prefill_s),
         "weight_gen_s": t_gen,
     }
     if args.offload_calls > 0:

@@ -41,7 +41,7 @@ one prefill; a pure-Python loop brute force of the tiny layer.
 from __future__ import annotations
 
 import math
-from typing import Callable, Dict, Hashable, List, Sequence, Tuple
+from typing import Optional, Callable, Dict, Hashable, List, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -237,9 +237,14 @@ class OracleStage:
     def length(self, key: Hashable) -> int:
         return len(self.cache(key)[0])
 
-    def forward(self, batch: Sequence[Tuple[Hashable, np.ndarray]]) -> List[np.ndarray]:
+    def forward(self, batch: Sequence[Tuple[Hashable, np.ndarray]],
+                trace: Optional[List[List[np.ndarray]]] = None) -> List[np.ndarray]:
+        """Runs every layer over the batch's new rows.  With ``trace``, appends each layer's input
+        rows (one array per batch entry) before running it."""
         xs = [torch.as_tensor(np.asarray(x), dtype=F64).reshape(-1, self.shape.hidden) for _, x in batch]
         for layer in range(self.shape.n_layers):
+            if trace is not None:
+                trace.append([x.numpy().copy() for x in xs])
             w = LayerWeights(self.weights(layer))
             for i, (key, _) in enumerate(batch):
                 xs[i] = decoder_layer(xs[i], w, self.cache(key)[layer], self.shape, self.kv_round)

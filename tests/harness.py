@@ -6,6 +6,7 @@ feedback decoding, each side feeds back its own outputs.
 """
 from __future__ import annotations
 
+import dataclasses
 import math
 from dataclasses import dataclass, field
 from typing import Callable, Dict, List, Optional, Sequence, Tuple
@@ -85,6 +86,7 @@ class Scenario:
 @dataclass
 class RunResult:
     outputs: List[np.ndarray] = field(default_factory=list)   # per call [n_mb, B, T, H]
+    layer_rows: list = field(default_factory=list)             # oracle only, see run_oracle
     inputs: List[np.ndarray] = field(default_factory=list)
     block_tables: Dict[Tuple[int, int], List[int]] = field(default_factory=dict)
     slot_log: List[Tuple[int, int, int]] = field(default_factory=list)
@@ -135,12 +137,14 @@ class compute_stream:
         return self.ctx.__exit__(*exc)
 
 
-def run_gpu(sc: Scenario, device: int = 0, weights=None) -> RunResult:
+def run_gpu(sc: Scenario, device: int = 0, weights=None, feed=None) -> RunResult:
+    """The stage's outputs for the scenario's call plan.  ``feed(kind, mbs, T)``, if given, supplies
+    each call's input [len(mbs), B, T, H] instead of the workload's seeded inputs."""
     with compute_stream(device) as cs:
-        return _run_gpu(sc, device, weights, cs.handle)
+        return _run_gpu(sc, device, weights, cs.handle, feed)
 
 
-def _run_gpu(sc: Scenario, device: int, weights, cs_handle) -> RunResult:
+def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunResult:
     import torch
     import paper_2512_21835_amd as P
 
@@ -160,7 +164,10 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle) -> RunResult:
         prev: Dict[Tuple[int, int], np.ndarray] = {}
         outs = []
         for kind, mbs, step in sc.call_plan():
-            x = _inputs(sc, kind, mbs, step, prev)
+            if feed is not None:
+                x = feed(kind, mbs, sc.prefill if kind == "prefill" else 1)
+            else:
+                x = _inputs(sc, kind, mbs, step, prev)
             x_in = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
             x_out = torch.empty_like(x_in)
             if kind == "prefill":
@@ -190,8 +197,12 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle) -> RunResult:
     return res
 
 
-def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float = 0.0) -> RunResult:
-    """The oracle's outputs (floats=True) and its integer policies for the call sequence."""
+def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float = 0.0,
+               trace: bool = False) -> RunResult:
+    """The oracle's outputs (floats=True) and its integer policies for the call sequence.
+
+    With ``trace`` (workloads without feedback), ``res.layer_rows[l][(m, b)]`` holds the rows that
+    entered layer l for sequence (m, b), in call order; entry n_layers holds the stage outputs."""
     from oracle.policies import BlockAllocator, ResidencySchedule, SlotSchedule
     from oracle.stage_oracle import OracleStage
 
@@ -239,7 +250,10 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
                 for b in range(wl.batch):
                     rows.setdefault((m, b), []).append(x[i, b])
         keys = sorted(rows)
-        outs = orc.forward([(k, np.concatenate(rows[k])) for k in keys])
+        tr = [] if trace else None
+        outs = orc.forward([(k, np.concatenate(rows[k])) for k in keys], trace=tr)
+        if trace:
+            res.layer_rows = [dict(zip(keys, layer)) for layer in tr] + [dict(zip(keys, outs))]
         done = {k: 0 for k in keys}
         by_key = dict(zip(keys, outs))
         for mbs, x in calls:
@@ -258,6 +272,49 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
     res.residency = [1 if l in resid.resident else 0 for l in range(shape.n_layers)]
     res._oracle = orc
     return res
+
+
+def teacher_forced(sc: Scenario, ref: RunResult, weights=None, runner=None) -> List[dict]:
+    """Per-layer teacher forcing: layer l runs on the GPU alone (a one-layer stage holding layer l's
+    weights), through the scenario's call plan, fed the rows that entered layer l in the oracle
+    (rounded to fp32, the stage's input type), and its outputs are compared with the rows that
+    entered layer l + 1 there.  Each layer's K/V cache is then built from the same inputs on both
+    sides, so K/V rounding flips stay inside the layer instead of compounding through the stage.
+    ``ref`` comes from run_oracle(sc, trace=True).  ``runner(sc, weights, feed)`` runs the one-layer
+    stage (default: the GPU through run_gpu).  Returns one compare() dict per layer."""
+    shape = sc.shape
+    weights = weights or weights_of(shape)
+    one = dataclasses.replace(shape, n_layers=1)
+    sc1 = dataclasses.replace(sc, wl=dataclasses.replace(sc.wl, shape=one, resident=None, thresholds=()),
+                              n_resident=None, thresholds=())
+    results = []
+    for layer in range(shape.n_layers):
+        rows_in, rows_out = ref.layer_rows[layer], ref.layer_rows[layer + 1]
+        taken = {k: 0 for k in rows_in}
+
+        def feed(kind, mbs, T):
+            x = np.empty((len(mbs), sc.wl.batch, T, shape.hidden), dtype=np.float32)
+            for i, m in enumerate(mbs):
+                for b in range(sc.wl.batch):
+                    t0 = taken[(m, b)]
+                    x[i, b] = rows_in[(m, b)][t0: t0 + T]
+                    taken[(m, b)] = t0 + T
+            return x
+        run = runner or (lambda s1, w, f: run_gpu(s1, weights=w, feed=f))
+        got = run(sc1, lambda _l, _w=weights(layer): _w, feed)
+        # oracle rows of the same calls, in the same order
+        done = {k: 0 for k in rows_out}
+        want, given = [], []
+        for (kind, mbs, _), x in zip(sc.call_plan(), got.inputs):
+            T = x.shape[2]
+            for i, m in enumerate(mbs):
+                for b in range(sc.wl.batch):
+                    t0 = done[(m, b)]
+                    want.append(rows_out[(m, b)][t0: t0 + T])
+                    given.append(rows_in[(m, b)][t0: t0 + T])
+                    done[(m, b)] = t0 + T
+        results.append(compare(got.flat_out(), np.concatenate(want), got.flat_in(), np.concatenate(given)))
+    return results
 
 
 # Relative accuracy of the GPU arithmetic up to the KV store: the prefill projections take the fp32

@@ -14,7 +14,7 @@ import numpy as np
 import pytest
 
 import synth
-from tests.harness import (Scenario, _progress, bf16_kv_tolerance, compare, compute_stream, run_gpu, run_oracle,
+from tests.harness import (Scenario, teacher_forced, _progress, bf16_kv_tolerance, compare, compute_stream, run_gpu, run_oracle,
                            weights_of)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
@@ -70,6 +70,19 @@ def test_70b_resident_bf16_kv_and_offloaded_is_bit_identical():
     for c, o4 in enumerate(got4.outputs):
         o3 = np.concatenate(got3.outputs[4 * c: 4 * c + 4])
         assert np.array_equal(o4, o3), f"call {c} differs"
+
+
+def test_70b_layers_teacher_forced_bf16_kv():
+    """The literal gate with the production bf16 KV cache, layer by layer (four interleaved
+    micro-batches, prefill 64, 8 decode rounds): each of the 16 layers, run alone on the oracle's
+    own inputs for every position, is within max|d| <= 2e-2, cosine >= 0.9995 of the oracle's
+    output of that layer."""
+    _gpu()
+    sc = Scenario(C3, prefill=64, decode_steps=8, calls="one")
+    ref = run_oracle(sc, trace=True)
+    for layer, m in enumerate(teacher_forced(sc, ref)):
+        _report(f"70b teacher-forced layer {layer}", m)
+        assert m["max_abs"] <= TOL_ABS and m["cos"] >= TOL_COS and m["cos_delta"] >= TOL_COS, (layer, m)
 
 
 def test_70b_kv_pressure_demotions_match_schedule():

@@ -11,7 +11,8 @@ import numpy as np
 import pytest
 
 import synth
-from tests.harness import Scenario, bf16_kv_tolerance, compare, compute_stream, run_gpu, run_oracle, weights_of
+from tests.harness import (Scenario, bf16_kv_tolerance, compare, compute_stream, run_gpu, run_oracle, teacher_forced,
+                           weights_of)
 
 pytestmark = pytest.mark.gpu
 
@@ -215,6 +216,21 @@ def test_llama8b_stage_full_length_bf16_kv():
     tol, spread = bf16_kv_tolerance(sc, ref)
     print(f"\n[llama8b bf16-kv] oracle spread under KV rounding {spread:.4g} -> tolerance {tol:.4g}")
     check("llama8b full bf16-kv", sc, got, ref, tol_abs=tol)
+
+
+def test_llama8b_layers_teacher_forced_bf16_kv():
+    """The literal gate with the production bf16 KV cache, layer by layer: each of the 8 layers,
+    run alone on the oracle's own inputs for every position (prefill 1024 + 128 decode steps),
+    matches the oracle's output of that layer within max|d| <= 2e-2 and cosine >= 0.9995."""
+    _gpu()
+    sc = Scenario(synth.WORKLOADS["llama8b_stage"], prefill=1024, decode_steps=128)
+    ref = run_oracle(sc, trace=True)
+    worst = 0.0
+    for layer, m in enumerate(teacher_forced(sc, ref)):
+        print(f"\n[llama8b teacher-forced layer {layer}] {m}", flush=True)
+        assert m["max_abs"] <= TOL_ABS and m["cos"] >= TOL_COS and m["cos_delta"] >= TOL_COS, (layer, m)
+        worst = max(worst, m["max_abs"])
+    print(f"[llama8b teacher-forced] worst layer max|d| {worst:.3g}")
 
 
 def test_llama8b_stage_full_length_fp32_kv():
