@@ -119,21 +119,22 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
     const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
     const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
 
-    // keys of this lane: kk = st * KPS + wave * KPW + kl
+    // keys of this lane: kk = st * KPS + wave * KPW + kl.  Slots past the split's last key load that
+    // key again (in bounds; their scores are masked below), so that the loads carry no branches and
+    // all block-table loads, then all K/V loads, are in flight together: two round trips in all.
+    int blk[STEPS];
+#pragma unroll
+    for (int st = 0; st < STEPS; ++st) {
+        const int key = kbeg + min(st * KPS + wave * KPW + kl, n - 1);
+        blk[st] = table[key / kBlockTokens];
+    }
     float kf[STEPS][8], vf[STEPS][8];
 #pragma unroll
     for (int st = 0; st < STEPS; ++st) {
-        const int kk = st * KPS + wave * KPW + kl;
-        if (kk < n) {
-            const int key = kbeg + kk;
-            const size_t e = (size_t)table[key / kBlockTokens] * blk_stride +
-                             ((size_t)g * kBlockTokens + key % kBlockTokens) * D + c0;
-            load8<F32KV>(a.kv.pool, e, kf[st]);
-            load8<F32KV>(a.kv.pool, e + (size_t)hkv * kBlockTokens * D, vf[st]);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) kf[st][j] = vf[st][j] = 0.f;
-        }
+        const int key = kbeg + min(st * KPS + wave * KPW + kl, n - 1);
+        const size_t e = (size_t)blk[st] * blk_stride + ((size_t)g * kBlockTokens + key % kBlockTokens) * D + c0;
+        load8<F32KV>(a.kv.pool, e, kf[st]);
+        load8<F32KV>(a.kv.pool, e + (size_t)hkv * kBlockTokens * D, vf[st]);
     }
     const float scale = 1.f / sqrtf((float)D);
     float q[G][8];

@@ -247,8 +247,9 @@ void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
         hipLaunchKernelGGL((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, c);
 }
 
-// Units per workgroup and steps in flight, by mode and rows (measured on the 8B- and 70B-shaped
-// layers): four units and two steps where registers allow, fewer as the rows multiply them.
+// Units per workgroup and steps in flight, by mode and rows (swept on the 8B- and 70B-shaped
+// layers, one row): gate/up 4 units x 1 step, O and down 4 x 2, QKV 2 x 1 (2 x 2 on the larger
+// shape); fewer as the rows multiply the registers.
 template <int M, int MODE>
 void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     if (MODE == GEMV_PLAIN_RESIDUAL) {
@@ -259,7 +260,7 @@ void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
         else launch_one<M, 2, 1, MODE>(c, st, e0, e1);
     } else {
         const bool big = (long)host_units(MODE, c) * c.K >= 40L * 1000 * 1000;
-        if (M <= 2 && big) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
+        if (M <= 2 && big) launch_one<M, 2, 2, MODE>(c, st, e0, e1);
         else launch_one<M, 2, 1, MODE>(c, st, e0, e1);
     }
 }
