@@ -217,6 +217,64 @@ def prefill_report(shape, T: int, seconds: float):
             "mfma_frac_algorithmic": (gemm + attn) / peak, "mfma_frac_issued": 2 * gemm / peak}
 
 
+def resident70b_leg(rounds: int, ctx: int = 2048):
+    """The 70B-shaped stage with all 16 layers resident, 4 micro-batches of batch 1 at context `ctx`
+    (filled through stage_kv_append with random K/V): decode rounds either round-robin, one
+    micro-batch per call (every call streams all weights for one token), or with all four
+    micro-batches in one call (the weights are read once for four tokens).  Weights are random bf16
+    generated on the device (timing only; parity of this configuration is covered by the tests)."""
+    import torch
+
+    import synth
+    import paper_2512_21835_amd as P
+
+    shape = synth.LLAMA70B_STAGE
+    dev = torch.device("cuda", 0)
+    cstream = torch.cuda.current_stream(dev)
+    n_mb, L = 4, shape.n_layers
+    cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + 4 * rounds + 8,
+                       n_resident_max=L, compute_stream=cstream.cuda_stream)
+    h = P.stage_init(cfg)
+    gen = torch.Generator(device=dev).manual_seed(2513)
+    res = {}
+    try:
+        for l in range(L):
+            w = {}
+            for name, shp in synth.layer_weight_shapes(shape).items():
+                t = torch.randn(shp, generator=gen, device=dev) * 0.02 + (1.0 if name in ("g1", "g2") else 0.0)
+                w[name] = t.to(torch.bfloat16).view(torch.int16).contiguous()
+            P.stage_load_layer(h, l, w, 1)
+            del w
+        for m in range(n_mb):
+            kv = [torch.randn(L, ctx, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
+                  .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)]
+            P.stage_kv_append(h, m, 0, ctx, kv[0], kv[1])
+        x = torch.randn(n_mb, 1, shape.hidden, generator=gen, device=dev)
+        y = torch.empty_like(x)
+        layer = shape.layer_bytes()
+        for mode in ("round_robin", "all_in_one_call"):
+            groups = [[m] for m in range(n_mb)] if mode == "round_robin" else [list(range(n_mb))]
+            for g in groups:   # warm-up round
+                P.stage_decode(h, g, 1, x[g[0]: g[0] + len(g)], y[g[0]: g[0] + len(g)])
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(rounds):
+                for g in groups:
+                    P.stage_decode(h, g, 1, x[g[0]: g[0] + len(g)], y[g[0]: g[0] + len(g)])
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            calls = rounds * len(groups)
+            kv_read = n_mb * rounds * L * (ctx + 2 * rounds) * 2 * shape.kv_dim * 2
+            hbm = calls * L * layer + kv_read
+            res[mode] = {"tokens_per_s": n_mb * rounds / dt, "ms_per_call": dt * 1e3 / calls,
+                         "hbm_GBs": hbm / dt / 1e9, "hbm_frac": hbm / dt / 1e9 / HBM_PEAK_GBS}
+    finally:
+        P.stage_destroy(h)
+    res["workload"] = (f"llama70b_resident decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672) resident, "
+                       f"4 micro-batches of batch 1, context {ctx}")
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -225,6 +283,8 @@ def main() -> int:
     ap.add_argument("--prefill", type=int, default=1024)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
+    ap.add_argument("--resident70b-rounds", type=int, default=8,
+                    help="timed decode rounds of the resident 70B leg (0 = skip)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for hardware traffic counters)")
     args = ap.parse_args()
@@ -320,6 +380,8 @@ def main() -> int:
         "prefill": prefill_report(shape, T, prefill_s),
         "weight_gen_s": t_gen,
     }
+    if args.resident70b_rounds > 0:
+        out["resident70b"] = resident70b_leg(args.resident70b_rounds)
     if args.offload_calls > 0:
         out["offload"] = offload_leg(args.offload_calls)
     if args.cpu_tokens > 0:

@@ -7,8 +7,9 @@
 // wavefront per head takes the chunk maximum and exponentials (online softmax across chunks), and
 // the same lanes then accumulate P.V from V rows fetched the same way.
 //
-// Prefill (split_keys == 0, attn_kernel): one workgroup per (row, KV head) walks all of the row's
-// keys.  Decode (split_keys > 0, attn_decode_kernel): the context is cut into splits of
+// Prefill (split_keys == 0): with a bf16 cache, attn_prefill_mfma runs the products on the matrix
+// cores (flash-attention tiling, below); with an fp32 cache (the parity mode), attn_kernel: one
+// workgroup per (row, KV head) walks all of the row's keys.  Decode (split_keys > 0, attn_decode_kernel): the context is cut into splits of
 // split_keys keys so that one token's attention still fills the GPU, and a second launch
 // (attn_merge_kernel) merges each row's splits in ascending order.
 #include <hip/hip_runtime.h>
@@ -379,15 +380,203 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     attn_merge_group<G, D>(a, g, row, (ctx + a.split_keys - 1) / a.split_keys, sm);
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ bf16x8_t as_bf(uint4 v) {
+    bf16x8_t r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+// x as an exact-sum pair of bf16 vectors: hi = bf16(x), lo = bf16(x - hi), both nearest even.
+__device__ __forceinline__ void split8(const float *x, bf16x8_t &hi, bf16x8_t &lo) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        hi[j] = (__bf16)x[j];                   // v_cvt_pk_bf16_f32: nearest even
+        lo[j] = (__bf16)(x[j] - (float)hi[j]);
+    }
+}
+
+constexpr int KT = 32;                 // keys per tile of the prefill kernel
+constexpr int VROW = KT + 8;           // transposed V tile row stride in bf16 (padding)
+
+// One workgroup: 128 query rows = G heads x (128 / G) consecutive positions of one sequence, one
+// KV head.  Wave w owns rows 32 w .. 32 w + 31 (row r: head r / BQ, position offset r % BQ).
+// Per 32-key tile: S^T = K Q^T (lane = one query column, 16 keys), online softmax in-lane,
+// O^T += V^T P^T with V transposed in LDS.  q and p enter the MFMAs as bf16 hi + lo pairs.
+template <int G, int D>
+__global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
+    constexpr int KROW = D + 8;         // K tile row stride in bf16 (padding)
+    constexpr int BQ = 128 / G;
+    constexpr int KK = D / 16;          // k16 steps over d
+    constexpr int NB = D / 32;          // 32-row blocks of d in O^T
+    __shared__ uint16_t sk[KT * KROW];
+    __shared__ uint16_t sv[D * VROW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, col = lane & 31;
+    const int qb = gridDim.x - 1 - blockIdx.x, g = blockIdx.y, sidx = blockIdx.z;  // longest first
+    const int T = a.meta->rows_per_seq;
+    const int pos0 = a.meta->pos0[sidx], slot = a.meta->seq_slot[sidx];
+    const int hkv = a.kv.n_kv_heads, hq_total = a.n_q_heads;
+    const size_t q_ld = (size_t)hq_total * D;
+    const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
+    const uint16_t *pool = static_cast<const uint16_t *>(a.kv.pool);
+    const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
+
+    // this lane's query (column) and its position
+    const int r = wave * 32 + col, hh = r / BQ, t = qb * BQ + r % BQ;
+    const bool qvalid = t < T;
+    const int qpos = pos0 + (qvalid ? t : T - 1);
+    const size_t qrow = (size_t)(sidx * T + (qvalid ? t : T - 1));
+    // Q^T fragments: B[k = d 16 kk + 8 half + j][query col]
+    bf16x8_t qh[KK], ql[KK];
+    {
+        const float scale = 1.4426950408889634f / sqrtf((float)D);   // log2(e) / sqrt(d): scores in base 2
+        const float *qp = a.q + qrow * q_ld + (size_t)(g * G + hh) * D + 8 * half;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            float x[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = qp[16 * kk + j] * scale;
+            split8(x, qh[kk], ql[kk]);
+        }
+    }
+    f32x16_t o[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[b][i] = 0.f;
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const int last_t = min(T, (qb + 1) * BQ) - 1;
+    const int n_keys = pos0 + last_t + 1;
+    const int n_tiles = (n_keys + KT - 1) / KT;
+    // wave's largest query position (tiles past it are fully masked for the wave)
+    int wave_max = 0;
+    {
+        const int r_lo = wave * 32, r_hi = wave * 32 + 31;
+        for (int rr = r_lo; rr <= r_hi; rr += 1) {
+            const int tt = qb * BQ + rr % BQ;
+            if (tt < T) wave_max = max(wave_max, pos0 + tt);
+        }
+    }
+
+    // tile loads: thread tid handles key (tid >> 3) ... 32 keys x (D / 8) chunks = 512 (D = 128)
+    constexpr int CHUNKS = KT * D / 8;          // 16-byte chunks per K (or V) tile
+    constexpr int PER_T = CHUNKS / 256;         // per thread (2 for D = 128, 1 for D = 64)
+    // chunk c = tid + 256 i (i < PER_T): key c / (D / 8), d chunk c % (D / 8)
+    uint4 kr0, kr1, vr0, vr1;
+#define STG_GLOAD(TILE, I, KR, VR)                                                                        \
+    do {                                                                                                  \
+        const int c_ = tid + 256 * (I);                                                                   \
+        const int kp_ = min((TILE) * KT + c_ / (D / 8), n_keys - 1);                                      \
+        const size_t b_ = (size_t)table[kp_ / kBlockTokens] * blk_stride +                                \
+                          (size_t)(kp_ % kBlockTokens) * D + (c_ % (D / 8)) * 8;                          \
+        KR = *reinterpret_cast<const uint4 *>(pool + b_ + (size_t)g * kBlockTokens * D);                 \
+        VR = *reinterpret_cast<const uint4 *>(pool + b_ + (size_t)(hkv + g) * kBlockTokens * D);         \
+    } while (0)
+#define STG_LSTORE(I, KR, VR)                                                                             \
+    do {                                                                                                  \
+        const int c_ = tid + 256 * (I);                                                                   \
+        const int key_ = c_ / (D / 8), d_ = (c_ % (D / 8)) * 8;                                           \
+        *reinterpret_cast<uint4 *>(sk + key_ * KROW + d_) = KR;                                           \
+        const uint32_t w_[4] = {VR.x, VR.y, VR.z, VR.w};                                                  \
+        _Pragma("unroll") for (int j_ = 0; j_ < 4; ++j_) {                                                \
+            sv[(d_ + 2 * j_) * VROW + key_] = (uint16_t)(w_[j_] & 0xFFFFu);                               \
+            sv[(d_ + 2 * j_ + 1) * VROW + key_] = (uint16_t)(w_[j_] >> 16);                               \
+        }                                                                                                 \
+    } while (0)
+    auto gload = [&](int tile) {
+        STG_GLOAD(tile, 0, kr0, vr0);
+        if (PER_T > 1) STG_GLOAD(tile, 1, kr1, vr1);
+    };
+    auto lstore = [&]() {
+        STG_LSTORE(0, kr0, vr0);
+        if (PER_T > 1) STG_LSTORE(1, kr1, vr1);
+    };
+
+    gload(0);
+    for (int tile = 0; tile < n_tiles; ++tile) {
+        __syncthreads();            // previous tile's LDS reads done
+        lstore();
+        __syncthreads();
+        if (tile + 1 < n_tiles) gload(tile + 1);
+        const int k0 = tile * KT;
+        if (k0 <= wave_max) {           // wave-uniform: past it every key of the tile is masked
+        // S^T[key][query] = sum_d K[key][d] Q[query][d]: A = K (lane: key col, d 16kk + 8 half)
+        f32x16_t s;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[i] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8_t kf = as_bf(*reinterpret_cast<const uint4 *>(sk + col * KROW + 16 * kk + 8 * half));
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qh[kk], s, 0, 0, 0);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, ql[kk], s, 0, 0, 0);
+        }
+        // lane holds keys k0 + 8 (i / 4) + 4 half + i % 4 for query column col
+        float mt = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int kp = k0 + 8 * (i / 4) + 4 * half + (i % 4);
+            if (kp > qpos) s[i] = -INFINITY;
+            mt = fmaxf(mt, s[i]);
+        }
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        const float m_new = fmaxf(m_run, mt);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        float p[16], ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            p[i] = s[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i] - m_new);
+            ps += p[i];
+        }
+        ps += __shfl_xor(ps, 32, 64);
+        l_run = l_run * alpha + ps;
+        m_run = m_new;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {   // some lane's maximum moved
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) o[b][i] *= alpha;
+        }
+        // O^T[d][query] += sum_key V[key][d] P[query][key]; k index (8 half + j) of MFMA m is the
+        // lane's key 16 m + 8 (j / 4) + 4 half + j % 4 = its p[8 m + j]
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            bf16x8_t ph, pl;
+            split8(p + 8 * m, ph, pl);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const uint16_t *vr = sv + (32 * b + col) * VROW + 16 * m + 4 * half;
+                const uint2 v0 = *reinterpret_cast<const uint2 *>(vr), v1 = *reinterpret_cast<const uint2 *>(vr + 8);
+                const bf16x8_t vf = as_bf(make_uint4(v0.x, v0.y, v1.x, v1.y));
+                o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, ph, o[b], 0, 0, 0);
+                o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pl, o[b], 0, 0, 0);
+            }
+        }
+        }
+    }
+    if (!qvalid) return;
+    // O^T[d = 32 b + 8 (i / 4) + 4 half + i % 4][query col]
+    float *orow = a.out + qrow * q_ld + (size_t)(g * G + hh) * D;
+    const float inv = 1.f / l_run;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) orow[32 * b + 8 * (i / 4) + 4 * half + (i % 4)] = o[b][i] * inv;
+}
+
 template <int G, int D>
 hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
     const int hkv = a.kv.n_kv_heads;
     if (a.split_keys == 0) {
-        dim3 grid(1, hkv, a.rows);
-        if (a.kv_fp32)
-            hipLaunchKernelGGL((attn_kernel<G, D, true>), grid, dim3(256), 0, st, a);
-        else
-            hipLaunchKernelGGL((attn_kernel<G, D, false>), grid, dim3(256), 0, st, a);
+        if (a.kv_fp32) {
+            hipLaunchKernelGGL((attn_kernel<G, D, true>), dim3(1, hkv, a.rows), dim3(256), 0, st, a);
+        } else {
+            if (a.n_seqs * a.rows_per_seq != a.rows) return hipErrorInvalidValue;
+            constexpr int BQ = 128 / G;
+            dim3 grid((a.rows_per_seq + BQ - 1) / BQ, hkv, a.n_seqs);
+            hipLaunchKernelGGL((attn_prefill_mfma<G, D>), grid, dim3(256), 0, st, a);
+        }
         return hipGetLastError();
     }
     if (a.split_keys > kChunk || a.max_splits > kMaxDecodeSplits) return hipErrorInvalidValue;

@@ -256,7 +256,7 @@ void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
         if (M <= 2) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
         else launch_one<M, 4, 1, MODE>(c, st, e0, e1);
     } else if (MODE == GEMV_NORM_SWIGLU) {
-        if (M <= 2) launch_one<M, 4, 1, MODE>(c, st, e0, e1);
+        if (M <= 4) launch_one<M, 4, 1, MODE>(c, st, e0, e1);
         else launch_one<M, 2, 1, MODE>(c, st, e0, e1);
     } else {
         const bool big = (long)host_units(MODE, c) * c.K >= 40L * 1000 * 1000;

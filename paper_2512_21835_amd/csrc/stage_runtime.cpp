@@ -378,8 +378,8 @@ int run_layer(stage *s, int layer, const void *blob, int rows, int T, const Call
 }
 
 // Prefill (T >= 2): projections on the matrix cores with bf16 hi/lo operand pairs.
-int run_layer_prefill(stage *s, int layer, const void *blob, int rows, const CallMeta *meta, const float *x_src,
-                      float *x_dst) {
+int run_layer_prefill(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+                      const float *x_src, float *x_dst) {
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const int H = s->H, F = s->F, qd = s->Hq * s->D;
     const float eps = s->cfg.rms_eps;
@@ -412,6 +412,8 @@ int run_layer_prefill(stage *s, int layer, const void *blob, int rows, const Cal
     at.kv_fp32 = s->cfg.kv_fp32;
     at.rows = rows;
     at.split_keys = 0;
+    at.n_seqs = rows / T;
+    at.rows_per_seq = T;
     at.meta = meta;
     HIP_TRY(launch_attention(at, s->cs));
     HIP_TRY(launch_split(s->ws_attn, (size_t)rows * qd, s->ws_hi, s->ws_lo, s->cs));
@@ -445,7 +447,7 @@ int run_layer_prefill(stage *s, int layer, const void *blob, int rows, const Cal
 
 int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
                       int grid_splits, const float *x_src, float *x_dst) {
-    if (T >= 2) return run_layer_prefill(s, layer, blob, rows, meta, x_src, x_dst);
+    if (T >= 2) return run_layer_prefill(s, layer, blob, rows, T, meta, x_src, x_dst);
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
