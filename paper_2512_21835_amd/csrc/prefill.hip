@@ -4,9 +4,9 @@
 // k step issues v_mfma_f32_32x32x16_bf16 twice per output block, hi then lo, accumulating in fp32.
 //
 // Tiling: a workgroup (4 wavefronts) computes a 128 x 128 tile of C; each wavefront a 64 x 64
-// sub-tile as 2 x 2 blocks of 32 x 32.  K advances 32 at a time through two LDS stages: the next
-// tile's global loads are issued before the current tile's MFMAs and written to the other stage
-// afterwards.  Tiles are stored in LDS in MFMA fragment order (lane l of a fragment at offset
+// sub-tile as 2 x 2 blocks of 32 x 32.  K advances 32 at a time.  gemm_dma_kernel (K a multiple
+// of 32) copies tiles global -> LDS directly into a ring of three stages, two tiles ahead;
+// gemm_kernel (any K) stages them through registers into two LDS stages, one tile ahead.  Tiles are stored in LDS in MFMA fragment order (lane l of a fragment at offset
 // 16 l), so every fragment read is one conflict-free ds_read_b128 per lane.  Workgroups that share
 // a weight tile are adjacent in launch order (x over M tiles), so each weight tile is read from HBM
 // once and re-served from L2.
@@ -144,6 +144,118 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         }
 }
 
+// Copies 16 bytes per lane from global memory straight into LDS (global_load_lds_dwordx4): lane l
+// of the wavefront writes LDS bytes [lds_addr + 16 l, lds_addr + 16 l + 16).  Issued as inline
+// assembly so that the compiler does not wait for every such load before each LDS read (it cannot
+// tell which LDS bytes a DMA load writes); the kernel waits for them itself (wait_vm).  m0 holds
+// the wavefront-uniform LDS address; nothing else in the kernel uses m0.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory");
+}
+
+// s_waitcnt vmcnt(N), other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    __builtin_amdgcn_s_waitcnt(0x3F70 | (N & 0xF) | ((N >> 4) << 14));
+}
+
+// The same product as gemm_kernel (same MFMAs in the same order: bit-identical results) for K a
+// multiple of 32, with the operand tiles copied into a ring of three LDS stages by
+// global_load_lds: tile t + 2 is in flight while tile t is multiplied, and no registers stage it.
+// Wavefront w fills fragments 2w and 2w + 1 of each operand tile, one load instruction each:
+// lane l of fragment f = (32-row block f / 2, k16 half f % 2) loads row 32 (f / 2) + (l & 31),
+// k offset 16 (f % 2) + 8 (l >> 5) -- exactly the fragment-order slot f * 64 + l.
+template <int MODE>
+__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
+    constexpr int S = 3;
+    constexpr int PER_TILE = 6;  // load instructions per wavefront per k tile
+    __shared__ uint4 lds[S][3][kFrag];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4 *)&lds[0][0][0];
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const uint16_t *W = a.w[blockIdx.z];
+    const int M = a.M, N = a.N, K = a.K, nk = K / BK;
+
+    // rows past M or N are clamped (in bounds); their results are never stored
+    const uint16_t *src_hi[2], *src_lo[2], *src_w[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int f = wave * 2 + i, r = (f >> 1) * 32 + (lane & 31), kof = (f & 1) * 16 + (lane >> 5) * 8;
+        const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
+        src_hi[i] = a.a_hi + (size_t)m * a.lda + kof;
+        src_lo[i] = a.a_lo + (size_t)m * a.lda + kof;
+        src_w[i] = W + (size_t)n * K + kof;
+    }
+    auto issue = [&](int t) {
+        const int st = t % S, k0 = t * BK;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int f = wave * 2 + i;
+            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * kFrag + f * 64) * 16);
+            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * kFrag + f * 64) * 16);
+            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * kFrag + f * 64) * 16);
+        }
+    };
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    issue(0);
+    if (nk > 1) issue(1);
+    for (int t = 0; t < nk; ++t) {
+        // tile t has landed when at most the next tile's loads are still in flight
+        if (t + 1 < nk) wait_vm<PER_TILE>();
+        else wait_vm<0>();
+        __syncthreads();  // every wavefront's part of tile t is in LDS; stage (t - 1) % S is free
+        if (t + 2 < nk) issue(t + 2);
+        const uint4 *L = &lds[t % S][0][0];
+#pragma unroll
+        for (int step = 0; step < BK / 16; ++step) {
+            bf16x8 ah[2], al[2], bw[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int sa = ((wm * 2 + b) * (BK / 16) + step) * 64 + lane;
+                const int sb = ((wn * 2 + b) * (BK / 16) + step) * 64 + lane;
+                ah[b] = as_bf16x8(L[sa]);
+                al[b] = as_bf16x8(L[kFrag + sa]);
+                bw[b] = as_bf16x8(L[2 * kFrag + sb]);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bw[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bw[j], acc[i][j], 0, 0, 0);
+                }
+        }
+    }
+
+    const int col_off = a.out_col[blockIdx.z];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+            if (n >= N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (m >= M) continue;
+                const size_t o = (size_t)m * a.ldo + col_off + n;
+                if (MODE == GEMM_RESIDUAL)
+                    a.out[o] = a.res[o] + acc[i][j][r];
+                else
+                    a.out[o] = acc[i][j][r];
+            }
+        }
+}
+
 // y = x / sqrt(mean(x^2) + eps) * g, written as a bf16 hi/lo pair.  One workgroup per row.
 __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, const uint16_t *g, float eps, int H,
                                                              uint16_t *hi, uint16_t *lo) {
@@ -191,10 +303,14 @@ int grid_for(size_t count) {
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) {
     if (a.M <= 0) return hipSuccess;
     dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, n_mats);
-    if (mode == GEMM_RESIDUAL)
-        hipLaunchKernelGGL(gemm_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
-    else
-        hipLaunchKernelGGL(gemm_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
+    const bool dma = a.K % BK == 0;   // whole k tiles: the LDS-DMA ring (bit-identical results)
+    if (mode == GEMM_RESIDUAL) {
+        if (dma) hipLaunchKernelGGL(gemm_dma_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
+        else hipLaunchKernelGGL(gemm_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
+    } else {
+        if (dma) hipLaunchKernelGGL(gemm_dma_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
+        else hipLaunchKernelGGL(gemm_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
+    }
     return hipGetLastError();
 }
 
