@@ -32,8 +32,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, published
 # script (FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by what the counter reads for a
 # plain 1 GiB device copy in the same run).  Valid for the GEMV source it was taken on: with any
 # other source the field is reported as null.
-GATEUP_TRAFFIC = {"bytes": 235253037,
-                  "source_sha256": "36f3032d5f926561a6cd48e07a2a345c4a23c821d27e6a136efc344347fffc72"}
+GATEUP_TRAFFIC = {"bytes": 235239486,
+                  "source_sha256": "7d179ec10219b7ea7c5a5c817605bd40e0bf9751ce8817c1ca2bfec42988eae0"}
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
 
