@@ -230,8 +230,8 @@ int set_residency(stage *s, int layer, int resident) {
     return STAGE_OK;
 }
 
-int ensure_workspace(stage *s, size_t rows, bool decode) {
-    const size_t need_part = decode ? rows : 0;
+int ensure_workspace(stage *s, size_t rows, bool split_attention) {
+    const size_t need_part = split_attention ? rows : 0;
     if (rows <= s->ws_rows && need_part <= s->part_rows) return STAGE_OK;
     int rc = sync_all(s);
     if (rc) return rc;
@@ -448,6 +448,8 @@ int run_layer_prefill(stage *s, int layer, const void *blob, int rows, int T, co
 int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
                       int grid_splits, const float *x_src, float *x_dst) {
     if (T >= 2) return run_layer_prefill(s, layer, blob, rows, T, meta, x_src, x_dst);
+    if ((size_t)rows > s->part_rows || !s->ws_part_o || !s->ws_part_ml)
+        return s->fail(STAGE_ESTATE, "attention partials sized for %zu rows, call has %d", s->part_rows, rows);
     const uint16_t *base = static_cast<const uint16_t *>(blob);
     const size_t qd = (size_t)s->Hq * s->D;
 
@@ -571,7 +573,9 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
                        (int)s->free_blocks.size());
     const size_t rows = (size_t)slots.size() * T;
     DeviceGuard dg(c.device);
-    int rc = ensure_workspace(s, rows, decode);
+    // one row per sequence (a decode, or a one-token prefill) runs the decode kernels, whose
+    // attention needs the split partials
+    int rc = ensure_workspace(s, rows, T == 1);
     if (rc) return rc;
 
     const long long call_no = s->calls;

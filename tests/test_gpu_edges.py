@@ -1,0 +1,100 @@
+"""GPU parity at the edges of the call sequence: a one-token prefill, prefills that continue a
+sequence (chunked prefill, prefill after K/V appended through stage_kv_append), and decode at the
+largest context the library supports (16384 positions, 256 attention splits)."""
+import numpy as np
+import pytest
+
+import synth
+from tests.harness import compare, compute_stream, weights_of
+
+pytestmark = pytest.mark.gpu
+
+TOL_ABS = 2e-2
+TOL_COS = 0.9995
+
+
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(shape, plan, kv_fp32, seed_tag, max_context):
+    """Runs `plan` ([("append", n) | ("prefill", T) | ("decode", 1)]) for one sequence on the GPU
+    and on the oracle; returns [(name, compare dict)] for every prefill and decode call."""
+    import torch
+    import paper_2512_21835_amd as P
+    from oracle.stage_oracle import OracleStage
+
+    w = weights_of(shape)
+    L, hkv, d, H = shape.n_layers, shape.n_kv_heads, shape.head_dim, shape.hidden
+    orc = OracleStage(shape, w, kv_dtype="f32" if kv_fp32 else "bf16")
+    results = []
+    with compute_stream() as cs:
+        cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=max_context,
+                           n_resident_max=L, kv_fp32=kv_fp32, compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        try:
+            for l in range(L):
+                P.stage_load_layer(h, l, w(l), 1)
+            for i, (kind, n) in enumerate(plan):
+                if kind == "append":
+                    seed = synth.seed_of(0xE1, seed_tag, i)
+                    k = synth.normal_bf16(seed, (L, n, hkv, d))
+                    v = synth.normal_bf16(seed + 1, (L, n, hkv, d))
+                    if kv_fp32:
+                        kd = torch.from_numpy(synth.bf16_to_f32(k)).cuda()
+                        vd = torch.from_numpy(synth.bf16_to_f32(v)).cuda()
+                    else:
+                        kd = torch.from_numpy(k.view(np.int16)).cuda()
+                        vd = torch.from_numpy(v.view(np.int16)).cuda()
+                    P.stage_kv_append(h, 0, 0, n, kd, vd)
+                    orc.append_kv("s", synth.bf16_to_f32(k).astype(np.float64), synth.bf16_to_f32(v).astype(np.float64))
+                    continue
+                x = synth.normal_f32(synth.seed_of(0xE2, seed_tag, i), (n, H))
+                xd = torch.from_numpy(x).cuda().reshape(1, 1, n, H)
+                yd = torch.empty_like(xd)
+                if kind == "prefill":
+                    P.stage_prefill(h, [0], 1, n, xd, yd)
+                else:
+                    P.stage_decode(h, [0], 1, xd[:, :, 0], yd[:, :, 0])
+                P.stage_sync(h)
+                got = yd.cpu().numpy().reshape(n, H)
+                want = orc.forward([("s", x)])[0]
+                results.append((f"{kind} {n} (call {i})", compare(got, want, x, x)))
+            assert P.stage_get_length(h, 0, 0) == orc.length("s")
+        finally:
+            P.stage_destroy(h)
+    return results
+
+
+def _check(tag, results):
+    for name, m in results:
+        print(f"\n[{tag} {name}] {m}", flush=True)
+        assert m["max_abs"] <= TOL_ABS and m["cos"] >= TOL_COS and m["cos_delta"] >= TOL_COS, (name, m)
+
+
+@pytest.mark.parametrize("kv_fp32", [False, True])
+def test_one_token_prefill_then_chunked_prefill_then_decode(kv_fp32):
+    """Tiny stage: prefill of 1 token, then 5, then 40 (crossing 16-token blocks, 32-key tiles and a
+    128-row query block), then decode."""
+    _gpu()
+    plan = [("prefill", 1), ("prefill", 5), ("prefill", 40), ("decode", 1), ("decode", 1)]
+    _check(f"tiny chunked kv_fp32={kv_fp32}", _run(synth.TINY, plan, kv_fp32, 1, 64))
+
+
+def test_llama8b_prefill_continuing_a_long_appended_context():
+    """8B-shaped stage: 3000 positions of K/V appended, then a 200-token prefill on top of them
+    (matrix-core attention over a long history, ragged last query block), then decode."""
+    _gpu()
+    plan = [("append", 3000), ("prefill", 200), ("decode", 1)]
+    _check("llama8b append+prefill", _run(synth.LLAMA8B_STAGE, plan, False, 2, 3300))
+
+
+@pytest.mark.parametrize("kv_fp32", [False, True])
+def test_decode_at_the_largest_context(kv_fp32):
+    """Tiny stage: 16383 positions appended, one decode step brings the context to 16384, the
+    largest supported (256 attention splits of 64 keys)."""
+    _gpu()
+    plan = [("append", 16383), ("decode", 1)]
+    _check(f"tiny max-context kv_fp32={kv_fp32}", _run(synth.TINY, plan, kv_fp32, 3, 16384))
