@@ -218,11 +218,12 @@ def prefill_report(shape, T: int, seconds: float):
 
 
 def resident70b_leg(rounds: int, ctx: int = 2048):
-    """The 70B-shaped stage with all 16 layers resident, 4 micro-batches of batch 1 at context `ctx`
-    (filled through stage_kv_append with random K/V): decode rounds either round-robin, one
-    micro-batch per call (every call streams all weights for one token), or with all four
-    micro-batches in one call (the weights are read once for four tokens).  Weights are random bf16
-    generated on the device (timing only; parity of this configuration is covered by the tests)."""
+    """The 70B-shaped stage with all 16 layers resident and sequences at context `ctx` (filled
+    through stage_kv_append with random K/V), decoded three ways: 4 micro-batches of batch 1
+    round-robin, one micro-batch per call (every call streams all weights for one token); the same
+    4 in one call (weights read once for 4 tokens, vector kernels); 8 micro-batches of batch 2 in
+    one call (16 rows, matrix cores).  Weights are random bf16 generated on the device (timing only;
+    parity of these configurations is covered by the tests)."""
     import torch
 
     import synth
@@ -231,8 +232,8 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
     shape = synth.LLAMA70B_STAGE
     dev = torch.device("cuda", 0)
     cstream = torch.cuda.current_stream(dev)
-    n_mb, L = 4, shape.n_layers
-    cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + 4 * rounds + 8,
+    L = shape.n_layers
+    cfg = P.config_for(shape, max_microbatches=8, max_batch=2, max_context=ctx + 3 * (rounds + 1) + 8,
                        n_resident_max=L, compute_stream=cstream.cuda_stream)
     h = P.stage_init(cfg)
     gen = torch.Generator(device=dev).manual_seed(2513)
@@ -245,33 +246,38 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
                 w[name] = t.to(torch.bfloat16).view(torch.int16).contiguous()
             P.stage_load_layer(h, l, w, 1)
             del w
-        for m in range(n_mb):
-            kv = [torch.randn(L, ctx, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
-                  .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)]
-            P.stage_kv_append(h, m, 0, ctx, kv[0], kv[1])
-        x = torch.randn(n_mb, 1, shape.hidden, generator=gen, device=dev)
+        for m in range(8):
+            for b in range(2):
+                kv = [torch.randn(L, ctx, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
+                      .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)]
+                P.stage_kv_append(h, m, b, ctx, kv[0], kv[1])
+        x = torch.randn(8, 2, shape.hidden, generator=gen, device=dev)
         y = torch.empty_like(x)
         layer = shape.layer_bytes()
-        for mode in ("round_robin", "all_in_one_call"):
-            groups = [[m] for m in range(n_mb)] if mode == "round_robin" else [list(range(n_mb))]
-            for g in groups:   # warm-up round
-                P.stage_decode(h, g, 1, x[g[0]: g[0] + len(g)], y[g[0]: g[0] + len(g)])
+        modes = {"round_robin": ([[m] for m in range(4)], 1), "4_in_one_call": ([list(range(4))], 1),
+                 "16_rows_in_one_call": ([list(range(8))], 2)}
+        for mode, (groups, B) in modes.items():
+            xs = [x[g[0]: g[0] + len(g), :B].contiguous() for g in groups]
+            ys = [torch.empty_like(xi) for xi in xs]
+            for g, xi, yi in zip(groups, xs, ys):   # warm-up round
+                P.stage_decode(h, g, B, xi, yi)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             for _ in range(rounds):
-                for g in groups:
-                    P.stage_decode(h, g, 1, x[g[0]: g[0] + len(g)], y[g[0]: g[0] + len(g)])
+                for g, xi, yi in zip(groups, xs, ys):
+                    P.stage_decode(h, g, B, xi, yi)
             torch.cuda.synchronize()
             dt = time.perf_counter() - t0
             calls = rounds * len(groups)
-            kv_read = n_mb * rounds * L * (ctx + 2 * rounds) * 2 * shape.kv_dim * 2
-            hbm = calls * L * layer + kv_read
-            res[mode] = {"tokens_per_s": n_mb * rounds / dt, "ms_per_call": dt * 1e3 / calls,
+            tokens = rounds * sum(len(g) for g in groups) * B
+            hbm = calls * L * layer + tokens * L * (ctx + 3 * rounds) * 2 * shape.kv_dim * 2
+            res[mode] = {"tokens_per_s": tokens / dt, "ms_per_call": dt * 1e3 / calls,
                          "hbm_GBs": hbm / dt / 1e9, "hbm_frac": hbm / dt / 1e9 / HBM_PEAK_GBS}
     finally:
         P.stage_destroy(h)
     res["workload"] = (f"llama70b_resident decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672) resident, "
-                       f"4 micro-batches of batch 1, context {ctx}")
+                       f"context {ctx}; 4 micro-batches of batch 1 (round robin or one call), or 8 of batch 2 "
+                       f"in one call")
     return res
 
 

@@ -21,6 +21,15 @@
 // the partials of wavefronts 0, 1, 2, 3 added in that order.  R, U and M only decide which
 // workgroup computes what and how loads are batched, so results do not depend on how many
 // micro-batches share a call.
+//
+// Matrix-core engine (gemv_mfma_kernel), for launches of 5 to 16 activation rows, where the
+// vector kernel becomes bound by its multiply-adds (one per row per weight element): the rows
+// are the A operand of v_mfma_f32_16x16x32_bf16 (padded to 16, the fp32 activation as a bf16
+// hi + lo pair, two MFMAs), 16 weight rows of a block the B operand, read straight from memory
+// (lane l: row l % 16, 16 bytes at k = 32 s + 8 (l / 16)).  The same K split across the four
+// wavefronts (128-wide k chunks, chunk c to wavefront c % 4), the same wavefront-order sum in
+// LDS and the same epilogues.  Its results are independent of the row count too, but differ in
+// rounding from the vector kernel's (by ~1e-5 relative).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -236,7 +245,126 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     }
 }
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int kMfmaRows = 16;     // activation rows per matrix-core launch
+constexpr int kMfmaMinRows = 5;   // fewer rows: the vector kernel is faster
+constexpr int kChunkK = 128;      // k per wavefront chunk (4 MFMA k steps of 32)
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
+    bf16x8 r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+// One workgroup: RB blocks of 16 units (units blockIdx.x * 16 RB ..) for up to 16 activation rows.
+template <int MODE, int RB>
+__global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
+    constexpr bool kNorm = Shape<MODE>::kNorm;
+    constexpr int NW = Shape<MODE>::NW;
+    __shared__ float part[kWaves][NW * RB][16][17];   // wavefront partial D[m][n] per weight block
+    __shared__ float ssp[kWaves][16];                  // wavefront partial sums of squares per row
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int units = n_units<MODE>(a);
+    const int unit0 = blockIdx.x * 16 * RB;
+    const int K = a.K, chunks = K / kChunkK, rows = a.rows;
+    const int nl = lane & 15, kq = lane >> 4;
+    const bool mvalid = nl < rows;   // this lane's A row (activation row nl)
+
+    const uint16_t *wrow[NW][RB];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int b = 0; b < RB; ++b)
+            wrow[w][b] = unit_row<MODE>(a, min(unit0 + 16 * b + nl, units - 1), w) + 8 * kq;
+    const float *xr = a.act + (size_t)(mvalid ? nl : 0) * a.act_ld + 8 * kq;
+
+    f32x4 d[NW][RB];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int b = 0; b < RB; ++b) d[w][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float ss = 0.f;
+    for (int c = wave; c < chunks; c += kWaves) {
+        uint4 wv[4][NW][RB];
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+#pragma unroll
+                for (int b = 0; b < RB; ++b) wv[s4][w][b] = load_stream16(wrow[w][b] + kChunkK * c + 32 * s4);
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const int k = kChunkK * c + 32 * s4;
+            const float4 x0 = *reinterpret_cast<const float4 *>(xr + k);
+            const float4 x1 = *reinterpret_cast<const float4 *>(xr + k + 4);
+            float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            float g[8];
+            if (kNorm) unpack8(*reinterpret_cast<const uint4 *>(a.gain + k + 8 * kq), g);
+            bf16x8 xh, xl;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                float v = mvalid ? x[j] : 0.f;
+                if (kNorm) {
+                    ss = fmaf(v, v, ss);
+                    v = v * g[j];
+                }
+                xh[j] = (__bf16)v;                       // nearest even
+                xl[j] = (__bf16)(v - (float)xh[j]);
+            }
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+#pragma unroll
+                for (int b = 0; b < RB; ++b) {
+                    d[w][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, as_bf16x8(wv[s4][w][b]), d[w][b], 0, 0, 0);
+                    d[w][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl, as_bf16x8(wv[s4][w][b]), d[w][b], 0, 0, 0);
+                }
+        }
+    }
+    // result register i of lane l: D[m = 4 (l / 16) + i][n = l % 16]
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int b = 0; b < RB; ++b)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) part[wave][w * RB + b][4 * kq + i][nl] = d[w][b][i];
+    if (kNorm) {
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        if (lane < 16) ssp[wave][lane] = ss;
+    }
+    __syncthreads();
+
+    for (int e = threadIdx.x; e < 16 * RB * kMfmaRows; e += 256) {
+        const int m = e % kMfmaRows, ub = e / kMfmaRows, b = ub / 16, n = ub % 16;
+        const int u = unit0 + ub;
+        if (m >= rows || u >= units) continue;
+        auto total = [&](int wb) { return ((part[0][wb][m][n] + part[1][wb][m][n]) + part[2][wb][m][n]) + part[3][wb][m][n]; };
+        float scale = 1.f;
+        if (kNorm) scale = 1.f / sqrtf((((ssp[0][m] + ssp[1][m]) + ssp[2][m]) + ssp[3][m]) / (float)K + a.eps);
+        const float y0 = total(b) * scale;
+        if (MODE == GEMV_NORM_ROPE_KV) {
+            rope_kv_epilogue(a, u, m, y0, total(RB + b) * scale);
+        } else if (MODE == GEMV_PLAIN_RESIDUAL) {
+            a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
+        } else {
+            const float up = total(RB + b) * scale;
+            a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
+        }
+    }
+}
+
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
+
+template <int MODE>
+void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    constexpr int RB = 2;
+    const int grid = (host_units(MODE, c) + 16 * RB - 1) / (16 * RB);
+    if (e0 || e1)
+        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+    else
+        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, c);
+}
 
 template <int M, int R, int U, int MODE>
 void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
@@ -267,16 +395,23 @@ void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
 
 template <int MODE>
 hipError_t launch_mode(const GemvArgs &a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
-    for (int r0 = 0; r0 < a.rows; r0 += kMaxRowsPerLaunch) {
+    // 16-unit blocks must not straddle the two halves of a RoPE head
+    const bool mfma_ok = a.K % kChunkK == 0 && (MODE != GEMV_NORM_ROPE_KV || (a.kv.head_dim / 2) % 16 == 0);
+    for (int r0 = 0, n = 0; r0 < a.rows; r0 += n) {
+        const int left = a.rows - r0;
+        const bool mfma = mfma_ok && left >= kMfmaMinRows;
+        n = min(left, mfma ? kMfmaRows : kMaxRowsPerLaunch);
         GemvArgs c = a;
-        c.rows = min(kMaxRowsPerLaunch, a.rows - r0);
+        c.rows = n;
         c.row0 = a.row0 + r0;
         c.act = a.act + (size_t)r0 * a.act_ld;
         c.out = a.out + (size_t)r0 * a.out_ld;
         if (a.res) c.res = a.res + (size_t)r0 * a.out_ld;
         hipEvent_t e0 = r0 == 0 ? ev_start : nullptr;
-        hipEvent_t e1 = r0 + kMaxRowsPerLaunch >= a.rows ? ev_stop : nullptr;
-        if (c.rows == 1)
+        hipEvent_t e1 = r0 + n >= a.rows ? ev_stop : nullptr;
+        if (mfma)
+            launch_mfma<MODE>(c, st, e0, e1);
+        else if (c.rows == 1)
             launch_rows<1, MODE>(c, st, e0, e1);
         else if (c.rows == 2)
             launch_rows<2, MODE>(c, st, e0, e1);
