@@ -32,8 +32,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, published
 # script (FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by what the counter reads for a
 # plain 1 GiB device copy in the same run).  Valid for the GEMV source it was taken on: with any
 # other source the field is reported as null.
-GATEUP_TRAFFIC = {"bytes": 235239486,
-                  "source_sha256": "7d179ec10219b7ea7c5a5c817605bd40e0bf9751ce8817c1ca2bfec42988eae0"}
+GATEUP_TRAFFIC = {"bytes": 235248073,
+                  "source_sha256": "2466b8caf4e484e9f91697444bb5528b1958c46ff0737afc7bf9a62e7efe29e4"}
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
 

@@ -356,14 +356,22 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
 
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
 
-template <int MODE>
-void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    constexpr int RB = 2;
+template <int MODE, int RB>
+void launch_mfma_rb(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int grid = (host_units(MODE, c) + 16 * RB - 1) / (16 * RB);
     if (e0 || e1)
         hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
     else
         hipLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, c);
+}
+
+// Two 16-unit blocks per workgroup where that still gives at least 256 workgroups (swept on the
+// 8B- and 70B-shaped layers: fewer workgroups than compute units cost more than the block pair
+// saves), one otherwise.
+template <int MODE>
+void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    if (host_units(MODE, c) >= 32 * 256) launch_mfma_rb<MODE, 2>(c, st, e0, e1);
+    else launch_mfma_rb<MODE, 1>(c, st, e0, e1);
 }
 
 template <int M, int R, int U, int MODE>
