@@ -119,14 +119,16 @@ def _intersect(a, b):
     return tot
 
 
-def offload_leg(calls: int, ctx: int = 2048):
+def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False):
     """The 70B-shaped stage with 4 resident layers and 12 streamed through 2 HBM slots.
 
     Four micro-batches at context `ctx` (filled through stage_kv_append with random K/V), each
     decode call carrying all four (streamed layers loaded once per call).  Reports the call time
     and the copy/compute overlap measured from events: slot copies on the copy stream, layer
-    compute intervals on the compute stream.  Weights are random bf16 generated on the device
-    (timing only; parity of this configuration is covered by the tests).
+    compute intervals on the compute stream.  With `zero_copy` the decode kernels of the 12
+    offloaded layers read their pinned host blobs directly instead (no slot copies); the report
+    then gives the call time and the host-link rate those reads reach.  Weights are random bf16
+    generated on the device (timing only; parity of this configuration is covered by the tests).
     """
     import torch
 
@@ -139,7 +141,8 @@ def offload_leg(calls: int, ctx: int = 2048):
     xstream = torch.cuda.Stream(dev)
     n_mb, L = 4, shape.n_layers
     cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + calls + 2, n_resident_max=4,
-                       n_stream_slots=2, compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream)
+                       n_stream_slots=2, compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream,
+                       zero_copy=zero_copy)
     h = P.stage_init(cfg)
     gen = torch.Generator(device=dev).manual_seed(2512)
     try:
@@ -187,12 +190,25 @@ def offload_leg(calls: int, ctx: int = 2048):
     ends = [i for i, r in enumerate(tl) if r[0] == 0]
     seg = tl[ends[-2] + 1: ends[-1] + 1] if len(ends) > 1 else tl[: ends[-1] + 1]
     last = [(s, e) for k, _, s, e in seg if k == 0][0]
+    streamed = 12 * blob
+    if zero_copy:
+        t_call = last[1] - last[0]
+        direct = [(l, e - s) for k, l, s, e in seg if k == 3 and l >= 4]
+        t_direct = sum(d for _, d in direct)
+        return {
+            "workload": f"llama70b_offload decode, zero-copy: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 4 "
+                        f"resident + 12 read by the decode kernels from pinned host memory, 4 micro-batches of "
+                        f"batch 1 per call, context {ctx}",
+            "tokens_per_s": n_mb * calls / wall, "ms_per_call": t_call, "host_read_GB_per_call": streamed / 1e9,
+            "offloaded_layers_ms": t_direct, "host_read_GBs": streamed / (t_direct * 1e-3) / 1e9,
+            "h2d_peak_GBs": h2d_gbs, "link_util": streamed / (t_direct * 1e-3) / 1e9 / h2d_gbs,
+            "layer_loads": stats["layer_loads"], "bytes_direct": stats["bytes_direct"],
+        }
     copies = _union([(s, e) for k, _, s, e in seg if k == 1])
     comp = _union([(s, e) for k, _, s, e in seg if k == 3])
     t_copy, t_comp = _length(copies), _length(comp)
     t_call = max(last[1], copies[-1][1]) - min(last[0], copies[0][0])
     both = _intersect(copies, comp)
-    streamed = 12 * blob
     return {
         "workload": f"llama70b_offload decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 4 resident + 12 "
                     f"streamed through 2 HBM slots from pinned host memory, 4 micro-batches of batch 1 per call, "
@@ -390,6 +406,7 @@ def main() -> int:
         out["resident70b"] = resident70b_leg(args.resident70b_rounds)
     if args.offload_calls > 0:
         out["offload"] = offload_leg(args.offload_calls)
+        out["offload_zero_copy"] = offload_leg(args.offload_calls, zero_copy=True)
     if args.cpu_tokens > 0:
         out["cpu_baseline"] = cpu_baseline(shape, lambda l: weights[l], wl, args.cpu_tokens)
     print(json.dumps(out))

@@ -74,7 +74,10 @@ typedef struct {
     int32_t kv_pool_blocks;  /* blocks in the pool; 0 = every sequence can reach max_context */
     int32_t kv_fp32;         /* KV element type: 0 = bf16 (rounded to nearest even), 1 = fp32 */
     /* Weight memory: at most n_resident_max layers resident in HBM (the HBM weight budget, in
-       layers); every other layer streams through n_stream_slots reusable HBM slots. */
+       layers); every other layer streams through n_stream_slots reusable HBM slots.  Without
+       zero_copy the slots are allocated when the first layer is offloaded; with zero_copy, by the
+       first call that stages a layer (n_stream_slots may then be 0 for a stage that only runs
+       one-token calls; a call that would stage fails with EINVAL). */
     int32_t n_resident_max;
     int32_t n_stream_slots;
     /* Residency schedule (Section III-E, online memory-aware planner): before a prefill or
@@ -87,6 +90,13 @@ typedef struct {
     void *compute_stream; /* hipStream_t for kernels; NULL = the library creates one */
     void *copy_stream;    /* hipStream_t for slot copies; NULL = the library creates one */
     int32_t timing;       /* STAGE_TIME_* flags; 0 = no events */
+    /* 0 (default): offloaded layers are copied into a stream slot before their kernels run.
+       1: calls with one token per sequence (every decode call, and a prefill with T = 1) run the
+       kernels of offloaded layers on the pinned host blob directly, read over the host link (the
+       zero-copy access of Section III-C): no slot copy and no slot-log entry for them.  Longer
+       prefills still stage through the slots, since their GEMMs re-read every weight tile.
+       Outputs are identical in both modes. */
+    int32_t zero_copy;
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during

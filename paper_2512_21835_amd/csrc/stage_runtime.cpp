@@ -47,6 +47,7 @@ struct Layer {
     int state = -1;       // -1 not loaded, 0 offloaded (pinned host blob), 1 resident (HBM blob)
     void *dev = nullptr;  // HBM blob when resident
     void *host = nullptr; // pinned host blob when offloaded
+    void *host_dev = nullptr;  // the same blob as kernels address it (zero-copy decode)
 };
 
 struct TimeRec {
@@ -97,6 +98,7 @@ struct stage {
     std::vector<hipEvent_t> ev_pool;
 
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
+    long long bytes_direct = 0;   // offloaded-layer bytes read by zero-copy decode kernels
     std::string err;
 
     int fail(int code, const char *fmt, ...) {
@@ -209,15 +211,23 @@ int set_residency(stage *s, int layer, int resident) {
         HIP_TRY(hipMemcpy(dev, ly.host, s->blob_bytes, hipMemcpyHostToDevice));
         HIP_TRY(hipHostFree(ly.host));
         ly.host = nullptr;
+        ly.host_dev = nullptr;
         ly.dev = dev;
         ly.state = 1;
     } else {
-        int rc = ensure_slots(s);
+        int rc = s->cfg.zero_copy ? STAGE_OK : ensure_slots(s);
         if (rc) return rc;
-        void *host = nullptr;
+        void *host = nullptr, *host_dev = nullptr;
         if (hipHostMalloc(&host, s->blob_bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
             return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+        }
+        if (s->cfg.zero_copy) {
+            hipError_t e = hipHostGetDevicePointer(&host_dev, host, 0);
+            if (e != hipSuccess) {
+                (void)hipHostFree(host);
+                return s->fail_hip(e, "hipHostGetDevicePointer");
+            }
         }
         rc = sync_all(s);
         if (rc) { (void)hipHostFree(host); return rc; }
@@ -225,6 +235,7 @@ int set_residency(stage *s, int layer, int resident) {
         HIP_TRY(hipFree(ly.dev));
         ly.dev = nullptr;
         ly.host = host;
+        ly.host_dev = host_dev;
         ly.state = 0;
     }
     return STAGE_OK;
@@ -577,6 +588,17 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     // attention needs the split partials
     int rc = ensure_workspace(s, rows, T == 1);
     if (rc) return rc;
+    // A zero-copy call with one token per sequence runs offloaded layers on their host blobs and
+    // stages nothing; in zero-copy mode the slots are allocated by the first call that stages.
+    const bool direct = c.zero_copy && T == 1;
+    if (!direct && s->slots.empty()) {
+        bool may_stream = s->thresholds_applied < c.n_thresholds;
+        for (const Layer &ly : s->layers) may_stream = may_stream || ly.state == 0;
+        if (may_stream) {
+            rc = ensure_slots(s);
+            if (rc) return rc;
+        }
+    }
 
     const long long call_no = s->calls;
     // residency schedule: thresholds reached by this call demote resident layers, highest first
@@ -618,7 +640,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     // streamed layers of this call, ascending; load j -> slot (loads + j) mod S
     std::vector<int> streamed;
     for (int l = 0; l < s->L; ++l)
-        if (s->layers[l].state == 0) streamed.push_back(l);
+        if (s->layers[l].state == 0 && !direct) streamed.push_back(l);
     const int S = c.n_stream_slots;
     const long long load0 = s->loads;
     auto slot_of = [&](int j) { return (int)((load0 + j) % S); };
@@ -638,8 +660,9 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     for (int l = 0; l < s->L; ++l) {
         const float *src = (l == 0) ? x_in : x_out;
         const Layer &ly = s->layers[l];
-        if (ly.state == 1) {
-            rc = run_layer(s, l, ly.dev, (int)rows, T, s->d_meta, grid_splits, src, x_out);
+        if (ly.state == 1 || direct) {
+            if (ly.state == 0) s->bytes_direct += (long long)s->blob_bytes;
+            rc = run_layer(s, l, ly.state == 1 ? ly.dev : ly.host_dev, (int)rows, T, s->d_meta, grid_splits, src, x_out);
             if (rc) return rc;
             continue;
         }
@@ -705,7 +728,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
-                        (c.timing & ~kTimeAll) == 0;
+                        (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1);
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i)
         if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
@@ -824,7 +847,7 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
         if (!p) return s->fail(STAGE_EINVAL, "null weight pointer");
     if (resident && ly.state != 1 && n_resident(s) + 1 > s->cfg.n_resident_max)
         return s->fail(STAGE_ENOMEM, "HBM weight budget of %d resident layers reached", s->cfg.n_resident_max);
-    if (!resident) {
+    if (!resident && !s->cfg.zero_copy) {
         int rc = ensure_slots(s);
         if (rc) return rc;
     }
@@ -838,8 +861,19 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
         (void)hipGetLastError();
         return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
     }
+    void *dst_dev = nullptr;
+    if (!resident && s->cfg.zero_copy) {
+        hipError_t e = hipHostGetDevicePointer(&dst_dev, dst, 0);
+        if (e != hipSuccess) {
+            (void)hipHostFree(dst);
+            return s->fail_hip(e, "hipHostGetDevicePointer");
+        }
+    }
     int rc = sync_all(s);
-    if (rc) return rc;
+    if (rc) {
+        if (resident) (void)hipFree(dst); else (void)hipHostFree(dst);
+        return rc;
+    }
     const size_t H = s->H, F = s->F, qd = (size_t)s->Hq * s->D, kvd = (size_t)s->Hkv * s->D;
     const size_t offs[9] = {s->off_wqkv, s->off_wqkv + qd * H * 2, s->off_wqkv + (qd + kvd) * H * 2,
                             s->off_wo, s->off_wg, s->off_wu, s->off_wd, s->off_g1, s->off_g2};
@@ -856,6 +890,7 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
     if (ly.host) (void)hipHostFree(ly.host);
     ly.dev = resident ? dst : nullptr;
     ly.host = resident ? nullptr : dst;
+    ly.host_dev = dst_dev;
     ly.state = resident;
     return STAGE_OK;
 }
@@ -1066,10 +1101,10 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
     const int written = snprintf(
         buf, cap,
         "{\"calls\": %lld, \"prefill_tokens\": %lld, \"decode_tokens\": %lld, \"layer_loads\": %lld, "
-        "\"bytes_streamed\": %lld, \"layer_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
+        "\"bytes_streamed\": %lld, \"bytes_direct\": %lld, \"layer_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
         "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, \"kv_blocks\": %d, "
         "\"kv_blocks_free\": %d}",
-        s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->blob_bytes, res, streamed,
+        s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes, res, streamed,
         s->slots.size(), hbm_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }

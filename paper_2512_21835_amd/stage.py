@@ -46,7 +46,7 @@ class StageConfig(ctypes.Structure):
         ("n_resident_max", c_int32), ("n_stream_slots", c_int32),
         ("n_thresholds", c_int32), ("thresholds", c_int32 * STAGE_MAX_THRESHOLDS),
         ("device", c_int32), ("compute_stream", c_void_p), ("copy_stream", c_void_p),
-        ("timing", c_int32),
+        ("timing", c_int32), ("zero_copy", c_int32),
     ]
 
 
@@ -243,7 +243,7 @@ def stage_strerror(code: int) -> str:
 def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int, n_resident_max: int,
                n_stream_slots: int = 2, kv_fp32: bool = False, thresholds: Sequence[int] = (),
                kv_pool_blocks: int = 0, device: int = 0, compute_stream=None, copy_stream=None,
-               timing: int = 0) -> StageConfig:
+               timing: int = 0, zero_copy: bool = False) -> StageConfig:
     """A StageConfig for a stage shape (any object with the StageShape fields)."""
     cfg = stage_config_default()
     cfg.n_layers, cfg.hidden = shape.n_layers, shape.hidden
@@ -263,4 +263,5 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
     cfg.compute_stream = compute_stream
     cfg.copy_stream = copy_stream
     cfg.timing = timing
+    cfg.zero_copy = int(bool(zero_copy))
     return cfg

@@ -62,6 +62,7 @@ class Scenario:
     thresholds: Tuple[int, ...] = ()
     max_context: Optional[int] = None
     timing: int = 0
+    zero_copy: bool = False
 
     @property
     def shape(self):
@@ -155,7 +156,7 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
     cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=sc.ctx(),
                        n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
                        thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
-                       copy_stream=copy_stream.cuda_stream, timing=sc.timing)
+                       copy_stream=copy_stream.cuda_stream, timing=sc.timing, zero_copy=sc.zero_copy)
     h = P.stage_init(cfg)
     res = RunResult()
     try:
@@ -229,7 +230,9 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
         longest = max([alloc.lengths.get(k, 0) for k in alloc.lengths] + [alloc.lengths.get(k, 0) + T for k in keys])
         resid.before_call(call_no, longest)
         alloc.call([(k, T) for k in keys])
-        slots.call(call_no, resid.streamed())
+        # zero-copy access (Section III-C): a call with one token per sequence reads offloaded
+        # layers where they are, in host memory, so it stages nothing through the slots
+        slots.call(call_no, [] if (sc.zero_copy and T == 1) else resid.streamed())
         if not floats:
             continue
         res.inputs.append(x)

@@ -77,6 +77,27 @@ def test_streamed_layers_are_lossless(slots):
     assert got.stats["layer_loads"] == 2 * len(sc.call_plan())
 
 
+@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 6), (LLAMA8B_MULTI, 24, 3)])
+def test_zero_copy_decode_equals_slot_staging(wl, prefill, steps):
+    """Decode kernels reading the offloaded layers from pinned host memory give the slot-staged
+    outputs bit for bit; only prefill calls load slots, and every decode call reads each offloaded
+    layer once over the host link."""
+    _gpu()
+    staged = Scenario(wl, prefill=prefill, decode_steps=steps, calls="all", n_resident=1)
+    direct = dataclasses.replace(staged, zero_copy=True)
+    ref = run_gpu(staged)
+    got = run_gpu(direct)
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    orc = run_oracle(direct, floats=False)
+    assert got.slot_log == orc.slot_log
+    assert all(call == 0 for call, _, _ in got.slot_log)
+    n_off = wl.shape.n_layers - 1
+    assert got.stats["layer_loads"] == n_off
+    assert got.stats["bytes_direct"] == steps * n_off * got.stats["layer_bytes"]
+    assert ref.stats["bytes_direct"] == 0
+
+
 def _one_vs_all(wl, prefill, steps):
     a = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="one"))
     b = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="all"))
@@ -182,6 +203,59 @@ def test_kv_tail_export_and_append_round_trip():
         assert np.mean(gk == ok) > 0.99
     finally:
         P.stage_destroy(h2)
+        cs.__exit__(None, None, None)
+
+
+def test_zero_copy_decode_only_stage_needs_no_slots():
+    """A decode-only zero-copy stage (context received as a KV tail, Alg. 2) holds no HBM slot and
+    no weights in HBM, and decodes bit-identically to an all-resident stage; a multi-token prefill
+    then needs a slot and is refused without changing the stage."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape = synth.TINY
+    w = weights_of(shape)
+    wl = TINY_RAGGED
+    cs = compute_stream().__enter__()
+    nxt = torch.from_numpy(synth.decode_input(wl, 0, 0, 0)[None]).cuda()
+    k = np.zeros((2, 37, 2, 64), np.uint16)
+    v = np.zeros_like(k)
+    cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=2,
+                       compute_stream=cs.handle)
+    h = P.stage_init(cfg)
+    try:
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 1)
+        x = torch.from_numpy(synth.prefill_inputs(wl, 0, 0, 37)).cuda()
+        P.stage_prefill(h, [0], 1, 37, x, torch.empty_like(x))
+        P.stage_kv_export_tail(h, 0, 0, 37, k, v, False)
+        want = torch.empty_like(nxt)
+        P.stage_decode(h, [0], 1, nxt, want)
+        P.stage_sync(h)
+    finally:
+        P.stage_destroy(h)
+
+    cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=0,
+                       n_stream_slots=0, compute_stream=cs.handle, zero_copy=True)
+    h = P.stage_init(cfg)
+    try:
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 0)
+        P.stage_kv_append(h, 0, 0, 37, k, v)
+        got = torch.empty_like(nxt)
+        P.stage_decode(h, [0], 1, nxt, got)
+        P.stage_sync(h)
+        assert torch.equal(got, want)
+        st = P.stage_get_stats(h)
+        assert st["hbm_weight_bytes"] == 0 and st["stream_slots"] == 0 and st["layer_loads"] == 0
+        assert st["bytes_direct"] == 2 * st["layer_bytes"]
+        x4 = torch.zeros(1, 1, 4, 256, device="cuda")
+        with pytest.raises(P.StageError) as e:
+            P.stage_prefill(h, [0], 1, 4, x4, torch.empty_like(x4))    # would stage: no slots
+        assert e.value.code == P.STAGE_EINVAL
+        assert P.stage_get_length(h, 0, 0) == 38 and P.stage_get_slot_log(h) == []
+    finally:
+        P.stage_destroy(h)
         cs.__exit__(None, None, None)
 
 
