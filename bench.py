@@ -193,7 +193,7 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False):
     streamed = 12 * blob
     if zero_copy:
         t_call = last[1] - last[0]
-        direct = [(l, e - s) for k, l, s, e in seg if k == 3 and l >= 4]
+        direct = [(l, e - s) for k, l, s, e in seg if k in (3, 5) and l >= 4]
         t_direct = sum(d for _, d in direct)
         return {
             "workload": f"llama70b_offload decode, zero-copy: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 4 "
@@ -204,8 +204,8 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False):
             "h2d_peak_GBs": h2d_gbs, "link_util": streamed / (t_direct * 1e-3) / 1e9 / h2d_gbs,
             "layer_loads": stats["layer_loads"], "bytes_direct": stats["bytes_direct"],
         }
-    copies = _union([(s, e) for k, _, s, e in seg if k == 1])
-    comp = _union([(s, e) for k, _, s, e in seg if k == 3])
+    copies = _union([(s, e) for k, _, s, e in seg if k in (1, 4)])
+    comp = _union([(s, e) for k, _, s, e in seg if k in (3, 5)])
     t_copy, t_comp = _length(copies), _length(comp)
     t_call = max(last[1], copies[-1][1]) - min(last[0], copies[0][0])
     both = _intersect(copies, comp)

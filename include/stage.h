@@ -10,6 +10,9 @@
  * offloaded layers per stage; Section III-B: weight memory is the retained
  * layers plus one stage's worth of offloaded layers; Section III-C: a reusable
  * loading buffer refilled once the GPU signals it has finished with it).
+ * Residency is per block: a layer's MHA block (Wq, Wk, Wv, Wo, g1) and its MLP
+ * block (Wg, Wu, Wd, g2) can be resident or offloaded independently (Section
+ * III-D, block-level offloading).
  * Streaming changes where the weights are, never the arithmetic: outputs are
  * bit-identical whichever layers are resident (lossless inference, abstract and
  * Section IV-A).
@@ -55,11 +58,18 @@ typedef enum {
 #define STAGE_MAX_SEQS_PER_CALL 64
 #define STAGE_MAX_CONTEXT 16384
 
+/* Residency of a layer (stage_load_layer, stage_get_residency).  "MHA-only offloading" in the
+   sense of Section III-D: the MHA block streams, the MLP block stays resident. */
+#define STAGE_RES_OFFLOADED 0      /* both blocks in pinned host memory */
+#define STAGE_RES_RESIDENT 1       /* both blocks in HBM */
+#define STAGE_RES_MHA_OFFLOADED 2  /* MHA block offloaded, MLP block resident */
+#define STAGE_RES_MLP_OFFLOADED 3  /* MLP block offloaded, MHA block resident */
+
 /* Timing flags (stage_config.timing). */
 #define STAGE_TIME_CALLS 1   /* events around each prefill/decode call and each slot copy */
 #define STAGE_TIME_GATEUP 2  /* events around the gate/up projection kernel of one decode layer
                                 per call (layer = call number mod n_layers) */
-#define STAGE_TIME_LAYERS 4  /* events around each layer's kernels (compute intervals) */
+#define STAGE_TIME_LAYERS 4  /* events around each layer's MHA-block and MLP-block kernels */
 
 typedef struct {
     /* Layer shape.  hidden, head_dim, ffn and n_q_heads*head_dim must be multiples of 8;
@@ -73,8 +83,9 @@ typedef struct {
     int32_t kv_block_tokens; /* tokens per KV block; must be 16 */
     int32_t kv_pool_blocks;  /* blocks in the pool; 0 = every sequence can reach max_context */
     int32_t kv_fp32;         /* KV element type: 0 = bf16 (rounded to nearest even), 1 = fp32 */
-    /* Weight memory: at most n_resident_max layers resident in HBM (the HBM weight budget, in
-       layers); every other layer streams through n_stream_slots reusable HBM slots.  Without
+    /* Weight memory: resident blocks may hold at most n_resident_max whole layers' bytes of HBM
+       (the HBM weight budget, in layers; a block counts its own bytes); every layer with an
+       offloaded block streams through n_stream_slots reusable HBM slots of one layer each.  Without
        zero_copy the slots are allocated when the first layer is offloaded; with zero_copy, by the
        first call that stages a layer (n_stream_slots may then be 0 for a stage that only runs
        one-token calls; a call that would stage fails with EINVAL). */
@@ -118,14 +129,14 @@ int stage_init(const stage_config *cfg, stage **out);
 /* Frees everything the stage owns after waiting for its streams.  NULL is a no-op. */
 int stage_destroy(stage *s);
 
-/* Loads layer `layer` (0 <= layer < n_layers) and sets its residency (Section III-A:
-   retained vs offloaded layers).  w != NULL: copy the weights into library storage -- an HBM
-   blob if resident, a pinned host blob (hipHostMalloc) if not; the caller may free w on return
-   (the call synchronises its copies).  w == NULL: change the residency of an already loaded
-   layer (demotion copies the HBM blob to pinned host memory; promotion copies it back), which
-   is the planner's offload action (Section III-E).
-   EINVAL: bad layer; ENOMEM: more than n_resident_max resident layers, or allocation failed;
-   ESTATE: w == NULL for a layer never loaded. */
+/* Loads layer `layer` (0 <= layer < n_layers) and sets its residency `resident`, a STAGE_RES_*
+   code (Section III-A: retained vs offloaded layers; Section III-D: MHA or MLP block only).
+   w != NULL: copy the weights into library storage -- HBM for a resident block, pinned host
+   memory (hipHostMalloc) for an offloaded one; the caller may free w on return (the call
+   synchronises its copies).  w == NULL: change the residency of an already loaded layer (each
+   block that changes side is copied across), which is the planner's offload action (Section
+   III-E).  EINVAL: bad layer or code; ENOMEM: the resident blocks would exceed the weight budget,
+   or allocation failed (the layer is unchanged); ESTATE: w == NULL for a layer never loaded. */
 int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int32_t resident);
 
 /* Prefill: runs T new tokens of each of B rows of each listed micro-batch through all layers.
@@ -177,26 +188,30 @@ int stage_get_block_table(stage *s, int32_t mb, int32_t b, int32_t *blocks, int3
 /* Current length (tokens stored) of sequence (mb, b). */
 int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length);
 
-/* Residency of every layer: 1 resident, 0 streamed, -1 not loaded; out has n_layers entries. */
+/* Residency of every layer: a STAGE_RES_* code, -1 if not loaded; out has n_layers entries. */
 int stage_get_residency(stage *s, int32_t *out);
 
-/* Slot log: one (call number, layer, slot) triple per streamed-layer load since init, in
-   load order; call numbers count prefill and decode calls from 0.  Writes min(cap, count)
-   triples (3*cap ints), *n = count. */
+/* Slot log: one (call number, layer, slot) triple per streamed-layer load (a layer with any
+   offloaded block) since init, in load order; call numbers count prefill and decode calls from 0.
+   Writes min(cap, count) triples (3*cap ints), *n = count. */
 int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
-/* Demotions made by the residency schedule: (call number, layer) pairs, like the slot log. */
+/* Demotions made by the residency schedule: (call number, layer) pairs, like the slot log.  A
+   demotion offloads both blocks of the highest-id layer that still has a resident block. */
 int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
 /* Timeline recorded under stage_config.timing, then cleared.  Synchronises.  Each record is
-   four floats: kind (0 call, 1 slot copy, 2 gate/up kernel, 3 layer compute), layer (-1 for a
-   call), start and end in milliseconds from the first record.  Writes min(cap, count) records, *n = count. */
+   four floats: kind (0 call, 1 slot copy of an MHA block, 2 gate/up kernel, 3 a layer's
+   MHA-block kernels, 4 slot copy of an MLP block, 5 a layer's MLP-block kernels), layer (-1 for
+   a call), start and end in milliseconds from the first record.  Kinds 3 and 5 exclude the wait
+   for an MLP block still being copied.  Writes min(cap, count) records, *n = count. */
 int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
 
 /* Replaces the STAGE_TIME_* flags of the stage (see stage_config.timing) for later calls. */
 int stage_set_timing(stage *s, int32_t flags);
 
-/* JSON object with counters: calls, tokens, layer loads, bytes streamed, HBM bytes in use. */
+/* JSON object with counters: calls, tokens, layer loads, bytes streamed through slots and read in
+   place (zero copy), block sizes, residency counts, HBM bytes in use. */
 int stage_get_stats(stage *s, char *buf, int32_t cap);
 
 /* Message of the last error on this handle ("" if none); valid until the next call. */

@@ -11,21 +11,29 @@ open; the readings are:
   a call, sequences allocate in call order (micro-batch ids in the order given,
   then batch rows ascending), each taking all blocks its new tokens need before
   the next.  A call that would exhaust the pool changes nothing.
+* Residency is per block (Section III-D: a layer splits into its MHA block and
+  its MLP block, each offloadable alone), given per layer as a code: 1 both
+  resident, 0 both offloaded, 2 MHA block offloaded ("MHA-only offloading"),
+  3 MLP block offloaded.
 * Slot assignment (Section III-C: a reusable loading buffer is refilled once the
-  GPU signals it is done with the previous layer).  The k-th layer load of the
-  stage's life (k = 0, 1, ...) goes to slot k mod S.  Each call loads each
-  streamed layer once, in ascending layer order, and runs it for every
-  micro-batch of the call before its slot is reused.
+  GPU signals it is done with the previous layer).  A layer with any offloaded
+  block is streamed.  The k-th layer load of the stage's life (k = 0, 1, ...)
+  goes to slot k mod S.  Each call loads each streamed layer once, in ascending
+  layer order, and runs it for every micro-batch of the call before its slot is
+  reused.
 * Residency schedule (Section III-E, online memory-aware planner: progressive
   offloading at token-length thresholds TS^j).  Before a call, let c be the
   longest sequence length in the stage once the call's tokens are appended.
-  Every threshold TS^j <= c not yet applied demotes one resident layer, the
-  highest id first, so a prefix of layers stays resident.
+  Every threshold TS^j <= c not yet applied offloads both blocks of one layer
+  that still has a resident block, the highest id first, so with whole-layer
+  residency a prefix of layers stays resident.
 """
 from __future__ import annotations
 
 import heapq
-from typing import Dict, Hashable, Iterable, List, Sequence, Tuple
+from typing import Dict, Hashable, Iterable, List, Optional, Sequence, Tuple
+
+OFFLOADED, RESIDENT, MHA_OFFLOADED, MLP_OFFLOADED = 0, 1, 2, 3
 
 
 class BlockAllocator:
@@ -90,25 +98,37 @@ class SlotSchedule:
 
 
 class ResidencySchedule:
-    """Resident set of layers and its threshold-driven shrinking."""
+    """Residency code of every layer and its threshold-driven shrinking.
 
-    def __init__(self, n_layers: int, resident: Iterable[int], thresholds: Sequence[int] = ()):
+    ``resident`` lists the wholly resident layers (the others offloaded), unless ``codes``
+    gives every layer's code."""
+
+    def __init__(self, n_layers: int, resident: Iterable[int] = (), thresholds: Sequence[int] = (),
+                 codes: Optional[Sequence[int]] = None):
         self.n_layers = n_layers
-        self.resident = set(resident)
+        keep = set(resident)
+        self.codes = list(codes) if codes is not None else [RESIDENT if l in keep else OFFLOADED
+                                                            for l in range(n_layers)]
+        assert len(self.codes) == n_layers
         self.thresholds = list(thresholds)
         self.applied = 0
         self.log: List[Tuple[int, int]] = []        # (call number, demoted layer)
+
+    @property
+    def resident(self) -> set:
+        return {l for l, c in enumerate(self.codes) if c == RESIDENT}
 
     def before_call(self, call_no: int, longest_after_call: int) -> List[int]:
         demoted = []
         while self.applied < len(self.thresholds) and self.thresholds[self.applied] <= longest_after_call:
             self.applied += 1
-            if self.resident:
-                layer = max(self.resident)
-                self.resident.remove(layer)
+            holders = [l for l, c in enumerate(self.codes) if c != OFFLOADED]
+            if holders:
+                layer = max(holders)
+                self.codes[layer] = OFFLOADED
                 demoted.append(layer)
                 self.log.append((call_no, layer))
         return demoted
 
     def streamed(self) -> List[int]:
-        return [l for l in range(self.n_layers) if l not in self.resident]
+        return [l for l, c in enumerate(self.codes) if c != RESIDENT]

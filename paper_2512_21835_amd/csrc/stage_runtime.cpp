@@ -2,24 +2,28 @@
 // residency schedule and the per-layer launch sequence.  Implements include/stage.h.
 //
 // Memory plan (one stage, one GPU):
-//   * every layer is one blob of bf16 tensors at 256-byte aligned offsets:
-//       Wqkv [(Hq + 2 Hkv) d, H] (q rows, then k rows, then v rows) | Wo [H, Hq d] |
-//       Wg [F, H] | Wu [F, H] | Wd [H, F] | g1 [H] | g2 [H]
+//   * every layer is two blocks (Section III-D: a layer splits into its MHA and MLP blocks, each
+//     offloadable on its own), each a run of bf16 tensors at 256-byte aligned offsets:
+//       MHA block: Wqkv [(Hq + 2 Hkv) d, H] (q rows, then k rows, then v rows) | Wo [H, Hq d] | g1 [H]
+//       MLP block: Wg [F, H] | Wu [F, H] | Wd [H, F] | g2 [H]
 //     so a loaded layer is described once by fixed offsets (the paper's proxy modules,
 //     Section III-C: structure bound once, later loads only refill the bytes);
-//   * resident layers own an HBM blob; offloaded layers own a pinned host blob (hipHostMalloc)
-//     and are copied into one of n_stream_slots HBM slots when a call needs them;
+//   * a resident block owns HBM; an offloaded block owns pinned host memory (hipHostMalloc) and
+//     is copied into one of n_stream_slots HBM slots when a call needs it.  A slot holds one
+//     layer: its MHA block at offset 0, its MLP block after it;
 //   * the KV cache is one pool of 16-token blocks per layer, [block][K|V][Hkv][16][d], shared by
 //     all sequences through per-sequence block tables (one table row per sequence, the same block
 //     ids in every layer);
 //   * RoPE cos/sin tables [max_context][d/2] (fp32, computed in double on the host).
 //
-// Streaming (Section III-A/III-C): in each call the offloaded layers are loaded once, in
-// ascending order; load k of the stage's life goes to slot k mod S.  The copy stream waits on
-// the slot's "free" event (recorded by the compute stream after the last kernel that read the
-// slot's previous layer), copies the blob and records "ready"; the compute stream waits on
-// "ready" before the layer's first kernel.  With S slots the next S-1 loads proceed while a
-// layer computes, and the first loads of a call overlap the call's resident layers.
+// Streaming (Section III-A/III-C): in each call the layers with an offloaded block are loaded
+// once, in ascending order; load k of the stage's life goes to slot k mod S.  The copy stream
+// waits on the slot's "free" event (recorded by the compute stream after the last kernel that
+// read the slot's previous layer), copies the offloaded blocks, MHA first, and records a "ready"
+// event per block; the compute stream waits on the MHA block's event before the layer's first
+// kernel and on the MLP block's before the MLP kernels, so attention runs while the MLP block
+// is still on the link.  With S slots the next S-1 loads proceed while a layer computes, and the
+// first loads of a call overlap the call's resident layers.
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
@@ -43,12 +47,35 @@ constexpr int kTimeAll = STAGE_TIME_CALLS | STAGE_TIME_GATEUP | STAGE_TIME_LAYER
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-struct Layer {
-    int state = -1;       // -1 not loaded, 0 offloaded (pinned host blob), 1 resident (HBM blob)
-    void *dev = nullptr;  // HBM blob when resident
-    void *host = nullptr; // pinned host blob when offloaded
-    void *host_dev = nullptr;  // the same blob as kernels address it (zero-copy decode)
+constexpr int kMha = 0, kMlp = 1;  // block index: MHA (Wqkv, Wo, g1), MLP (Wg, Wu, Wd, g2)
+
+struct Block {
+    bool resident = false;
+    void *dev = nullptr;       // HBM copy when resident
+    void *host = nullptr;      // pinned host copy when offloaded
+    void *host_dev = nullptr;  // the pinned copy as kernels address it (zero copy)
 };
+
+struct Layer {
+    bool loaded = false;
+    Block blk[2];
+    // any block offloaded: the layer takes a slot load in every staged call
+    bool streams() const { return loaded && !(blk[kMha].resident && blk[kMlp].resident); }
+};
+
+// Residency codes of the C ABI (STAGE_RES_*), per block.
+bool code_keeps(int code, int b) {
+    return code == STAGE_RES_RESIDENT || (code == STAGE_RES_MHA_OFFLOADED && b == kMlp) ||
+           (code == STAGE_RES_MLP_OFFLOADED && b == kMha);
+}
+
+int code_of(const Layer &ly) {
+    if (!ly.loaded) return -1;
+    const bool a = ly.blk[kMha].resident, m = ly.blk[kMlp].resident;
+    if (a && m) return STAGE_RES_RESIDENT;
+    if (!a && !m) return STAGE_RES_OFFLOADED;
+    return a ? STAGE_RES_MLP_OFFLOADED : STAGE_RES_MHA_OFFLOADED;
+}
 
 struct TimeRec {
     int kind, layer;
@@ -64,12 +91,14 @@ struct stage {
     hipStream_t cs = nullptr, xs = nullptr;
     bool own_cs = false, own_xs = false;
 
+    // offsets inside the MHA block (wqkv, wo, g1) and inside the MLP block (wg, wu, wd, g2)
     size_t off_wqkv = 0, off_wo = 0, off_wg = 0, off_wu = 0, off_wd = 0, off_g1 = 0, off_g2 = 0;
-    size_t blob_bytes = 0;
+    size_t blk_bytes[2] = {0, 0};
+    size_t blob_bytes = 0;  // one layer: both blocks
     std::vector<Layer> layers;
 
     std::vector<void *> slots;
-    std::vector<hipEvent_t> slot_ready, slot_free;
+    std::vector<hipEvent_t> slot_ready[2], slot_free;
     long long loads = 0, calls = 0;
     std::vector<int> slot_log, demotion_log;
     int thresholds_applied = 0;
@@ -95,10 +124,11 @@ struct stage {
     size_t ws_dense_bytes = 0;
 
     std::vector<TimeRec> recs;
+    TimeRec open_rec{0, 0, nullptr, nullptr};  // block-kernel interval being timed
     std::vector<hipEvent_t> ev_pool;
 
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
-    long long bytes_direct = 0;   // offloaded-layer bytes read by zero-copy decode kernels
+    long long bytes_direct = 0;   // offloaded-block bytes read in place by zero-copy kernels
     std::string err;
 
     int fail(int code, const char *fmt, ...) {
@@ -168,75 +198,126 @@ int ensure_slots(stage *s) {
     const int S = s->cfg.n_stream_slots;
     if (S < 1) return s->fail(STAGE_EINVAL, "a layer is offloaded but n_stream_slots is 0");
     std::vector<void *> sl(S, nullptr);
-    std::vector<hipEvent_t> rd(S, nullptr), fr(S, nullptr);
+    std::vector<hipEvent_t> ra(S, nullptr), rm(S, nullptr), fr(S, nullptr);
     for (int i = 0; i < S; ++i) {
         if (hipMalloc(&sl[i], s->blob_bytes) != hipSuccess ||
-            hipEventCreateWithFlags(&rd[i], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&ra[i], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&rm[i], hipEventDisableTiming) != hipSuccess ||
             hipEventCreateWithFlags(&fr[i], hipEventDisableTiming) != hipSuccess) {
             (void)hipGetLastError();
             for (int j = 0; j <= i; ++j) {
                 if (sl[j]) (void)hipFree(sl[j]);
-                if (rd[j]) (void)hipEventDestroy(rd[j]);
-                if (fr[j]) (void)hipEventDestroy(fr[j]);
+                for (hipEvent_t e : {ra[j], rm[j], fr[j]})
+                    if (e) (void)hipEventDestroy(e);
             }
             return s->fail(STAGE_ENOMEM, "cannot allocate %d stream slots of %zu bytes", S, s->blob_bytes);
         }
     }
     s->slots = sl;
-    s->slot_ready = rd;
+    s->slot_ready[kMha] = ra;
+    s->slot_ready[kMlp] = rm;
     s->slot_free = fr;
     return STAGE_OK;
 }
 
-int n_resident(const stage *s) {
-    int n = 0;
-    for (const Layer &l : s->layers) n += (l.state == 1);
+// HBM bytes held by resident blocks.
+size_t resident_bytes(const stage *s) {
+    size_t n = 0;
+    for (const Layer &l : s->layers)
+        for (int b = 0; b < 2; ++b)
+            if (l.loaded && l.blk[b].resident) n += s->blk_bytes[b];
     return n;
 }
 
-// Moves a loaded layer between HBM and pinned host memory (the planner's offload action).
-int set_residency(stage *s, int layer, int resident) {
-    Layer &ly = s->layers[layer];
-    if (ly.state == resident) return STAGE_OK;
+// The weight budget: n_resident_max whole layers' worth of HBM, spent block by block.
+size_t budget_bytes(const stage *s) { return (size_t)s->cfg.n_resident_max * s->blob_bytes; }
+
+void free_block(Block &k) {
+    if (k.dev) (void)hipFree(k.dev);
+    if (k.host) (void)hipHostFree(k.host);
+    k = Block();
+}
+
+// A new home for block b: HBM if resident, else pinned host memory (mapped for zero copy).
+int alloc_block(stage *s, int b, bool resident, Block *out) {
+    Block k;
+    k.resident = resident;
+    const size_t bytes = s->blk_bytes[b];
     if (resident) {
-        if (n_resident(s) + 1 > s->cfg.n_resident_max)
-            return s->fail(STAGE_ENOMEM, "HBM weight budget of %d resident layers reached", s->cfg.n_resident_max);
-        void *dev = nullptr;
-        if (hipMalloc(&dev, s->blob_bytes) != hipSuccess) {
+        if (hipMalloc(&k.dev, bytes) != hipSuccess) {
             (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte weight block failed", bytes);
         }
-        int rc = sync_all(s);
-        if (rc) { (void)hipFree(dev); return rc; }
-        HIP_TRY(hipMemcpy(dev, ly.host, s->blob_bytes, hipMemcpyHostToDevice));
-        HIP_TRY(hipHostFree(ly.host));
-        ly.host = nullptr;
-        ly.host_dev = nullptr;
-        ly.dev = dev;
-        ly.state = 1;
     } else {
-        int rc = s->cfg.zero_copy ? STAGE_OK : ensure_slots(s);
-        if (rc) return rc;
-        void *host = nullptr, *host_dev = nullptr;
-        if (hipHostMalloc(&host, s->blob_bytes, hipHostMallocDefault) != hipSuccess) {
+        if (hipHostMalloc(&k.host, bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
+            return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte weight block failed", bytes);
         }
         if (s->cfg.zero_copy) {
-            hipError_t e = hipHostGetDevicePointer(&host_dev, host, 0);
+            hipError_t e = hipHostGetDevicePointer(&k.host_dev, k.host, 0);
             if (e != hipSuccess) {
-                (void)hipHostFree(host);
+                free_block(k);
                 return s->fail_hip(e, "hipHostGetDevicePointer");
             }
         }
-        rc = sync_all(s);
-        if (rc) { (void)hipHostFree(host); return rc; }
-        HIP_TRY(hipMemcpy(host, ly.dev, s->blob_bytes, hipMemcpyDeviceToHost));
-        HIP_TRY(hipFree(ly.dev));
-        ly.dev = nullptr;
-        ly.host = host;
-        ly.host_dev = host_dev;
-        ly.state = 0;
+    }
+    *out = k;
+    return STAGE_OK;
+}
+
+// Checks that moving layer `layer` to residency `code` fits the budget and has slots to stream
+// through; changes nothing.
+int check_residency(stage *s, int layer, int code) {
+    const Layer &ly = s->layers[layer];
+    size_t bytes = resident_bytes(s);
+    for (int b = 0; b < 2; ++b) {
+        if (ly.loaded && ly.blk[b].resident) bytes -= s->blk_bytes[b];
+        if (code_keeps(code, b)) bytes += s->blk_bytes[b];
+    }
+    if (bytes > budget_bytes(s))
+        return s->fail(STAGE_ENOMEM, "HBM weight budget of %d layers (%zu bytes) exceeded", s->cfg.n_resident_max,
+                       budget_bytes(s));
+    if (code != STAGE_RES_RESIDENT && !s->cfg.zero_copy) return ensure_slots(s);
+    return STAGE_OK;
+}
+
+// Moves the blocks of a loaded layer between HBM and pinned host memory (the planner's offload
+// action, Section III-E; block granularity, Section III-D).  New homes are allocated before
+// anything moves, so a failed allocation leaves the layer as it was.
+int set_residency(stage *s, int layer, int code) {
+    Layer &ly = s->layers[layer];
+    if (code_of(ly) == code) return STAGE_OK;
+    int rc = check_residency(s, layer, code);
+    if (rc) return rc;
+    Block fresh[2];
+    bool moves[2];
+    for (int b = 0; b < 2; ++b) {
+        moves[b] = code_keeps(code, b) != ly.blk[b].resident;
+        if (!moves[b]) continue;
+        rc = alloc_block(s, b, code_keeps(code, b), &fresh[b]);
+        if (rc) {
+            free_block(fresh[0]);
+            return rc;
+        }
+    }
+    rc = sync_all(s);
+    if (rc) {
+        for (Block &k : fresh) free_block(k);
+        return rc;
+    }
+    for (int b = 0; b < 2; ++b) {
+        if (!moves[b]) continue;
+        Block &old = ly.blk[b];
+        void *dst = fresh[b].resident ? fresh[b].dev : fresh[b].host;
+        const void *src = old.resident ? old.dev : old.host;
+        hipError_t e = hipMemcpy(dst, src, s->blk_bytes[b], hipMemcpyDefault);
+        if (e != hipSuccess) {
+            for (Block &k : fresh) free_block(k);
+            return s->fail_hip(e, "moving a weight block");
+        }
+        free_block(old);
+        old = fresh[b];
+        fresh[b] = Block();
     }
     return STAGE_OK;
 }
@@ -351,47 +432,81 @@ int record_event(stage *s, hipStream_t st, hipEvent_t *out) {
     return STAGE_OK;
 }
 
+// Copies the offloaded blocks of `layer` into `slot`, MHA block first, each followed by its
+// ready event.
 int enqueue_copy(stage *s, int layer, int slot) {
-    TimeRec rec{1, layer, nullptr, nullptr};
     HIP_TRY(hipStreamWaitEvent(s->xs, s->slot_free[slot], 0));
-    if (s->cfg.timing & STAGE_TIME_CALLS) {
-        int rc = record_event(s, s->xs, &rec.a);
-        if (rc) return rc;
+    for (int b = 0; b < 2; ++b) {
+        const Block &k = s->layers[layer].blk[b];
+        if (k.resident) continue;
+        TimeRec rec{b == kMha ? 1 : 4, layer, nullptr, nullptr};
+        if (s->cfg.timing & STAGE_TIME_CALLS) {
+            int rc = record_event(s, s->xs, &rec.a);
+            if (rc) return rc;
+        }
+        char *dst = static_cast<char *>(s->slots[slot]) + (b == kMha ? 0 : s->blk_bytes[kMha]);
+        HIP_TRY(hipMemcpyAsync(dst, k.host, s->blk_bytes[b], hipMemcpyHostToDevice, s->xs));
+        HIP_TRY(hipEventRecord(s->slot_ready[b][slot], s->xs));
+        if (s->cfg.timing & STAGE_TIME_CALLS) {
+            int rc = record_event(s, s->xs, &rec.b);
+            if (rc) return rc;
+            s->recs.push_back(rec);
+        }
+        s->bytes_streamed += (long long)s->blk_bytes[b];
     }
-    HIP_TRY(hipMemcpyAsync(s->slots[slot], s->layers[layer].host, s->blob_bytes, hipMemcpyHostToDevice, s->xs));
-    HIP_TRY(hipEventRecord(s->slot_ready[slot], s->xs));
-    if (s->cfg.timing & STAGE_TIME_CALLS) {
-        int rc = record_event(s, s->xs, &rec.b);
-        if (rc) return rc;
-        s->recs.push_back(rec);
-    }
-    s->bytes_streamed += (long long)s->blob_bytes;
     return STAGE_OK;
 }
 
-int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+// Where one layer's kernels find its weights: the MHA and MLP block bases, and the event the
+// MLP kernels wait on (the MLP block still arriving in a slot) or null.
+struct LayerWeights {
+    const uint16_t *mha = nullptr, *mlp = nullptr;
+    hipEvent_t mlp_ready = nullptr;
+};
+
+int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int T, const CallMeta *meta,
                       int grid_splits, const float *x_src, float *x_dst);
 
-// One layer's kernels, bracketed by events when STAGE_TIME_LAYERS is set.
-int run_layer(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+// One layer's kernels.  Under STAGE_TIME_LAYERS the MHA-block kernels and the MLP-block kernels
+// are bracketed by events separately, so that a wait for the MLP block between them is not
+// counted as compute.
+int run_layer(stage *s, int layer, const LayerWeights &w, int rows, int T, const CallMeta *meta,
               int grid_splits, const float *x_src, float *x_dst) {
     if (!(s->cfg.timing & STAGE_TIME_LAYERS))
-        return run_layer_kernels(s, layer, blob, rows, T, meta, grid_splits, x_src, x_dst);
-    TimeRec rec{3, layer, nullptr, nullptr};
-    int rc = record_event(s, s->cs, &rec.a);
+        return run_layer_kernels(s, layer, w, rows, T, meta, grid_splits, x_src, x_dst);
+    s->open_rec = TimeRec{3, layer, nullptr, nullptr};
+    int rc = record_event(s, s->cs, &s->open_rec.a);
     if (rc) return rc;
-    rc = run_layer_kernels(s, layer, blob, rows, T, meta, grid_splits, x_src, x_dst);
+    rc = run_layer_kernels(s, layer, w, rows, T, meta, grid_splits, x_src, x_dst);
     if (rc) return rc;
-    rc = record_event(s, s->cs, &rec.b);
+    rc = record_event(s, s->cs, &s->open_rec.b);
     if (rc) return rc;
-    s->recs.push_back(rec);
+    s->recs.push_back(s->open_rec);
+    return STAGE_OK;
+}
+
+// Between a layer's MHA-block and MLP-block kernels: closes the MHA timing record, waits for the
+// MLP block if it is still arriving in a slot, opens the MLP timing record.
+int mlp_boundary(stage *s, int layer, const LayerWeights &w) {
+    const bool timed = s->cfg.timing & STAGE_TIME_LAYERS;
+    if (timed) {
+        int rc = record_event(s, s->cs, &s->open_rec.b);
+        if (rc) return rc;
+        s->recs.push_back(s->open_rec);
+    }
+    if (w.mlp_ready) HIP_TRY(hipStreamWaitEvent(s->cs, w.mlp_ready, 0));
+    if (timed) {
+        s->open_rec = TimeRec{5, layer, nullptr, nullptr};
+        int rc = record_event(s, s->cs, &s->open_rec.a);
+        if (rc) return rc;
+    }
     return STAGE_OK;
 }
 
 // Prefill (T >= 2): projections on the matrix cores with bf16 hi/lo operand pairs.
-int run_layer_prefill(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int T, const CallMeta *meta,
                       const float *x_src, float *x_dst) {
-    const uint16_t *base = static_cast<const uint16_t *>(blob);
+    const uint16_t *base = w.mha;
     const int H = s->H, F = s->F, qd = s->Hq * s->D;
     const float eps = s->cfg.rms_eps;
 
@@ -436,6 +551,9 @@ int run_layer_prefill(stage *s, int layer, const void *blob, int rows, int T, co
     o.M = rows; o.N = H; o.K = qd;
     HIP_TRY(launch_gemm(GEMM_RESIDUAL, o, 1, s->cs));
 
+    base = w.mlp;
+    int rc = mlp_boundary(s, layer, w);
+    if (rc) return rc;
     HIP_TRY(launch_rmsnorm_split(x_dst, base + s->off_g2 / 2, eps, rows, H, s->ws_hi, s->ws_lo, s->cs));
     GemmArgs gu{};
     gu.a_hi = s->ws_hi; gu.a_lo = s->ws_lo; gu.lda = H;
@@ -456,12 +574,12 @@ int run_layer_prefill(stage *s, int layer, const void *blob, int rows, int T, co
     return STAGE_OK;
 }
 
-int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, const CallMeta *meta,
+int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int T, const CallMeta *meta,
                       int grid_splits, const float *x_src, float *x_dst) {
-    if (T >= 2) return run_layer_prefill(s, layer, blob, rows, T, meta, x_src, x_dst);
+    if (T >= 2) return run_layer_prefill(s, layer, w, rows, T, meta, x_src, x_dst);
     if ((size_t)rows > s->part_rows || !s->ws_part_o || !s->ws_part_ml)
         return s->fail(STAGE_ESTATE, "attention partials sized for %zu rows, call has %d", s->part_rows, rows);
-    const uint16_t *base = static_cast<const uint16_t *>(blob);
+    const uint16_t *base = w.mha, *mlp = w.mlp;
     const size_t qd = (size_t)s->Hq * s->D;
 
     GemvArgs q{};
@@ -508,11 +626,11 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     o.rows = rows;
 
     GemvArgs gu{};
-    gu.w = base + s->off_wg / 2;
-    gu.w2 = base + s->off_wu / 2;
+    gu.w = mlp + s->off_wg / 2;
+    gu.w2 = mlp + s->off_wu / 2;
     gu.act = x_dst;
     gu.act_ld = s->H;
-    gu.gain = base + s->off_g2 / 2;
+    gu.gain = mlp + s->off_g2 / 2;
     gu.out = s->ws_h;
     gu.out_ld = s->F;
     gu.N = s->F;
@@ -521,7 +639,7 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     gu.eps = s->cfg.rms_eps;
 
     GemvArgs dn{};
-    dn.w = base + s->off_wd / 2;
+    dn.w = mlp + s->off_wd / 2;
     dn.act = s->ws_h;
     dn.act_ld = s->F;
     dn.res = x_dst;
@@ -542,6 +660,8 @@ int run_layer_kernels(stage *s, int layer, const void *blob, int rows, int T, co
     HIP_TRY(launch_gemv(GEMV_NORM_ROPE_KV, q, s->cs));
     HIP_TRY(launch_attention(at, s->cs));
     HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, o, s->cs));
+    int rc = mlp_boundary(s, layer, w);
+    if (rc) return rc;
     HIP_TRY(launch_gemv(GEMV_NORM_SWIGLU, gu, s->cs, rec.a, rec.b));
     HIP_TRY(launch_gemv(GEMV_PLAIN_RESIDUAL, dn, s->cs));
     if (rec.a) s->recs.push_back(rec);
@@ -567,7 +687,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         for (int b = 0; b < B; ++b) slots.push_back(seq_slot(s, mb, b));
     }
     for (int l = 0; l < s->L; ++l)
-        if (s->layers[l].state < 0) return s->fail(STAGE_EINVAL, "layer %d is not loaded", l);
+        if (!s->layers[l].loaded) return s->fail(STAGE_EINVAL, "layer %d is not loaded", l);
     int longest = 0;
     for (int len : s->lengths) longest = std::max(longest, len);
     int need_blocks = 0;
@@ -593,7 +713,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     const bool direct = c.zero_copy && T == 1;
     if (!direct && s->slots.empty()) {
         bool may_stream = s->thresholds_applied < c.n_thresholds;
-        for (const Layer &ly : s->layers) may_stream = may_stream || ly.state == 0;
+        for (const Layer &ly : s->layers) may_stream = may_stream || ly.streams();
         if (may_stream) {
             rc = ensure_slots(s);
             if (rc) return rc;
@@ -606,9 +726,9 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         s->thresholds_applied++;
         int victim = -1;
         for (int l = s->L - 1; l >= 0; --l)
-            if (s->layers[l].state == 1) { victim = l; break; }
+            if (s->layers[l].blk[kMha].resident || s->layers[l].blk[kMlp].resident) { victim = l; break; }
         if (victim < 0) continue;
-        rc = set_residency(s, victim, 0);
+        rc = set_residency(s, victim, STAGE_RES_OFFLOADED);
         if (rc) return rc;
         s->demotion_log.push_back((int)call_no);
         s->demotion_log.push_back(victim);
@@ -640,7 +760,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     // streamed layers of this call, ascending; load j -> slot (loads + j) mod S
     std::vector<int> streamed;
     for (int l = 0; l < s->L; ++l)
-        if (s->layers[l].state == 0 && !direct) streamed.push_back(l);
+        if (s->layers[l].streams() && !direct) streamed.push_back(l);
     const int S = c.n_stream_slots;
     const long long load0 = s->loads;
     auto slot_of = [&](int j) { return (int)((load0 + j) % S); };
@@ -660,15 +780,28 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     for (int l = 0; l < s->L; ++l) {
         const float *src = (l == 0) ? x_in : x_out;
         const Layer &ly = s->layers[l];
-        if (ly.state == 1 || direct) {
-            if (ly.state == 0) s->bytes_direct += (long long)s->blob_bytes;
-            rc = run_layer(s, l, ly.state == 1 ? ly.dev : ly.host_dev, (int)rows, T, s->d_meta, grid_splits, src, x_out);
+        LayerWeights w;
+        const uint16_t **base[2] = {&w.mha, &w.mlp};
+        if (!ly.streams() || direct) {
+            for (int b = 0; b < 2; ++b) {
+                const Block &k = ly.blk[b];
+                if (!k.resident) s->bytes_direct += (long long)s->blk_bytes[b];
+                *base[b] = static_cast<const uint16_t *>(k.resident ? k.dev : k.host_dev);
+            }
+            rc = run_layer(s, l, w, (int)rows, T, s->d_meta, grid_splits, src, x_out);
             if (rc) return rc;
             continue;
         }
         const int sl = slot_of(j);
-        HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[sl], 0));
-        rc = run_layer(s, l, s->slots[sl], (int)rows, T, s->d_meta, grid_splits, src, x_out);
+        const char *slot = static_cast<const char *>(s->slots[sl]);
+        for (int b = 0; b < 2; ++b) {
+            const Block &k = ly.blk[b];
+            *base[b] = reinterpret_cast<const uint16_t *>(
+                k.resident ? static_cast<const char *>(k.dev) : slot + (b == kMha ? 0 : s->blk_bytes[kMha]));
+        }
+        if (!ly.blk[kMha].resident) HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[kMha][sl], 0));
+        if (!ly.blk[kMlp].resident) w.mlp_ready = s->slot_ready[kMlp][sl];
+        rc = run_layer(s, l, w, (int)rows, T, s->d_meta, grid_splits, src, x_out);
         if (rc) return rc;
         HIP_TRY(hipEventRecord(s->slot_free[sl], s->cs));
         if (j + S < n_str) {
@@ -745,15 +878,18 @@ int stage_init(const stage_config *cfg, stage **out) {
     s->D = c.head_dim; s->F = c.ffn;
     s->qkv_rows = (s->Hq + 2 * s->Hkv) * s->D;
     const size_t H = s->H, F = s->F, qd = (size_t)s->Hq * s->D;
-    size_t off = 0;
+    size_t off = 0;  // MHA block
     s->off_wqkv = off; off = align256(off + (size_t)s->qkv_rows * H * 2);
     s->off_wo = off;   off = align256(off + H * qd * 2);
+    s->off_g1 = off;   off = align256(off + H * 2);
+    s->blk_bytes[kMha] = off;
+    off = 0;         // MLP block
     s->off_wg = off;   off = align256(off + F * H * 2);
     s->off_wu = off;   off = align256(off + F * H * 2);
     s->off_wd = off;   off = align256(off + H * F * 2);
-    s->off_g1 = off;   off = align256(off + H * 2);
     s->off_g2 = off;   off = align256(off + H * 2);
-    s->blob_bytes = off;
+    s->blk_bytes[kMlp] = off;
+    s->blob_bytes = s->blk_bytes[kMha] + s->blk_bytes[kMlp];
     s->layers.assign(s->L, Layer());
 
     s->n_seq_slots = c.max_microbatches * c.max_batch;
@@ -808,12 +944,11 @@ int stage_destroy(stage *s) {
     DeviceGuard dg(s->cfg.device);
     if (s->cs) (void)hipStreamSynchronize(s->cs);
     if (s->xs) (void)hipStreamSynchronize(s->xs);
-    for (Layer &l : s->layers) {
-        if (l.dev) (void)hipFree(l.dev);
-        if (l.host) (void)hipHostFree(l.host);
-    }
+    for (Layer &l : s->layers)
+        for (Block &k : l.blk) free_block(k);
     for (void *p : s->slots) (void)hipFree(p);
-    for (hipEvent_t e : s->slot_ready) (void)hipEventDestroy(e);
+    for (auto &v : s->slot_ready)
+        for (hipEvent_t e : v) (void)hipEventDestroy(e);
     for (hipEvent_t e : s->slot_free) (void)hipEventDestroy(e);
     for (TimeRec &r : s->recs) {
         if (r.a) (void)hipEventDestroy(r.a);
@@ -834,64 +969,52 @@ int stage_destroy(stage *s) {
 int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int32_t resident) {
     if (!s) return STAGE_EINVAL;
     s->err.clear();
-    if (layer < 0 || layer >= s->L || (resident != 0 && resident != 1))
+    if (layer < 0 || layer >= s->L || resident < STAGE_RES_OFFLOADED || resident > STAGE_RES_MLP_OFFLOADED)
         return s->fail(STAGE_EINVAL, "bad layer %d or residency %d", layer, resident);
     DeviceGuard dg(s->cfg.device);
     Layer &ly = s->layers[layer];
     if (!w) {
-        if (ly.state < 0) return s->fail(STAGE_ESTATE, "layer %d was never loaded", layer);
+        if (!ly.loaded) return s->fail(STAGE_ESTATE, "layer %d was never loaded", layer);
         return set_residency(s, layer, resident);
     }
     const void *src[9] = {w->wq, w->wk, w->wv, w->wo, w->wg, w->wu, w->wd, w->g1, w->g2};
     for (const void *p : src)
         if (!p) return s->fail(STAGE_EINVAL, "null weight pointer");
-    if (resident && ly.state != 1 && n_resident(s) + 1 > s->cfg.n_resident_max)
-        return s->fail(STAGE_ENOMEM, "HBM weight budget of %d resident layers reached", s->cfg.n_resident_max);
-    if (!resident && !s->cfg.zero_copy) {
-        int rc = ensure_slots(s);
-        if (rc) return rc;
-    }
-    void *dst = nullptr;
-    if (resident) {
-        if (hipMalloc(&dst, s->blob_bytes) != hipSuccess) {
-            (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte layer blob failed", s->blob_bytes);
-        }
-    } else if (hipHostMalloc(&dst, s->blob_bytes, hipHostMallocDefault) != hipSuccess) {
-        (void)hipGetLastError();
-        return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte layer blob failed", s->blob_bytes);
-    }
-    void *dst_dev = nullptr;
-    if (!resident && s->cfg.zero_copy) {
-        hipError_t e = hipHostGetDevicePointer(&dst_dev, dst, 0);
-        if (e != hipSuccess) {
-            (void)hipHostFree(dst);
-            return s->fail_hip(e, "hipHostGetDevicePointer");
+    int rc = check_residency(s, layer, resident);
+    if (rc) return rc;
+    Block fresh[2];
+    for (int b = 0; b < 2; ++b) {
+        rc = alloc_block(s, b, code_keeps(resident, b), &fresh[b]);
+        if (rc) {
+            free_block(fresh[0]);
+            return rc;
         }
     }
-    int rc = sync_all(s);
+    rc = sync_all(s);
     if (rc) {
-        if (resident) (void)hipFree(dst); else (void)hipHostFree(dst);
+        for (Block &k : fresh) free_block(k);
         return rc;
     }
     const size_t H = s->H, F = s->F, qd = (size_t)s->Hq * s->D, kvd = (size_t)s->Hkv * s->D;
+    const int blk_of[9] = {kMha, kMha, kMha, kMha, kMlp, kMlp, kMlp, kMha, kMlp};
     const size_t offs[9] = {s->off_wqkv, s->off_wqkv + qd * H * 2, s->off_wqkv + (qd + kvd) * H * 2,
                             s->off_wo, s->off_wg, s->off_wu, s->off_wd, s->off_g1, s->off_g2};
     const size_t bytes[9] = {qd * H * 2, kvd * H * 2, kvd * H * 2, H * qd * 2, F * H * 2,
                              F * H * 2, H * F * 2, H * 2, H * 2};
     for (int i = 0; i < 9; ++i) {
-        hipError_t e = hipMemcpy(static_cast<char *>(dst) + offs[i], src[i], bytes[i], hipMemcpyDefault);
+        const Block &k = fresh[blk_of[i]];
+        char *dst = static_cast<char *>(k.resident ? k.dev : k.host);
+        hipError_t e = hipMemcpy(dst + offs[i], src[i], bytes[i], hipMemcpyDefault);
         if (e != hipSuccess) {
-            if (resident) (void)hipFree(dst); else (void)hipHostFree(dst);
+            for (Block &f : fresh) free_block(f);
             return s->fail_hip(e, "copying layer weights");
         }
     }
-    if (ly.dev) (void)hipFree(ly.dev);
-    if (ly.host) (void)hipHostFree(ly.host);
-    ly.dev = resident ? dst : nullptr;
-    ly.host = resident ? nullptr : dst;
-    ly.host_dev = dst_dev;
-    ly.state = resident;
+    for (int b = 0; b < 2; ++b) {
+        free_block(ly.blk[b]);
+        ly.blk[b] = fresh[b];
+    }
+    ly.loaded = true;
     return STAGE_OK;
 }
 
@@ -1035,7 +1158,7 @@ int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length) {
 
 int stage_get_residency(stage *s, int32_t *out) {
     if (!s || !out) return STAGE_EINVAL;
-    for (int l = 0; l < s->L; ++l) out[l] = s->layers[l].state;
+    for (int l = 0; l < s->L; ++l) out[l] = code_of(s->layers[l]);
     return STAGE_OK;
 }
 
@@ -1094,17 +1217,25 @@ int stage_set_timing(stage *s, int32_t flags) {
 
 int stage_get_stats(stage *s, char *buf, int32_t cap) {
     if (!s || !buf || cap < 1) return STAGE_EINVAL;
-    const int res = n_resident(s);
-    int streamed = 0;
-    for (const Layer &l : s->layers) streamed += (l.state == 0);
-    const size_t hbm_w = (size_t)res * s->blob_bytes + s->slots.size() * s->blob_bytes;
+    int res = 0, streamed = 0, off_mha = 0, off_mlp = 0;
+    for (const Layer &l : s->layers) {
+        if (!l.loaded) continue;
+        res += code_of(l) == STAGE_RES_RESIDENT;
+        streamed += l.streams();
+        off_mha += !l.blk[kMha].resident;
+        off_mlp += !l.blk[kMlp].resident;
+    }
+    const size_t hbm_w = resident_bytes(s) + s->slots.size() * s->blob_bytes;
     const int written = snprintf(
         buf, cap,
         "{\"calls\": %lld, \"prefill_tokens\": %lld, \"decode_tokens\": %lld, \"layer_loads\": %lld, "
-        "\"bytes_streamed\": %lld, \"bytes_direct\": %lld, \"layer_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
+        "\"bytes_streamed\": %lld, \"bytes_direct\": %lld, \"layer_bytes\": %zu, \"mha_block_bytes\": %zu, "
+        "\"mlp_block_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
+        "\"offloaded_mha_blocks\": %d, \"offloaded_mlp_blocks\": %d, "
         "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, \"kv_blocks\": %d, "
         "\"kv_blocks_free\": %d}",
-        s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes, res, streamed,
+        s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes,
+        s->blk_bytes[kMha], s->blk_bytes[kMlp], res, streamed, off_mha, off_mlp,
         s->slots.size(), hbm_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }

@@ -23,9 +23,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstage.so
 
 STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE = 0, -1, -2, -3, -4, -5
 STAGE_MAX_THRESHOLDS = 32
+STAGE_MAX_SEQS_PER_CALL = 64
+STAGE_MAX_CONTEXT = 16384
 STAGE_TIME_CALLS = 1
 STAGE_TIME_GATEUP = 2
 STAGE_TIME_LAYERS = 4
+STAGE_RES_OFFLOADED, STAGE_RES_RESIDENT, STAGE_RES_MHA_OFFLOADED, STAGE_RES_MLP_OFFLOADED = 0, 1, 2, 3
 
 EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",

@@ -63,13 +63,23 @@ class Scenario:
     max_context: Optional[int] = None
     timing: int = 0
     zero_copy: bool = False
+    residency: Optional[Tuple[int, ...]] = None   # per-layer STAGE_RES_* codes (block granularity)
 
     @property
     def shape(self):
         return self.wl.shape
 
     def resident_layers(self) -> int:
+        """The weight budget in layers: enough for every block the scenario keeps resident."""
+        if self.residency is not None:
+            return sum(1 for c in self.residency if c != 0)
         return self.shape.n_layers if self.n_resident is None else self.n_resident
+
+    def codes(self) -> List[int]:
+        if self.residency is not None:
+            return list(self.residency)
+        r = self.resident_layers()
+        return [1 if l < r else 0 for l in range(self.shape.n_layers)]
 
     def ctx(self) -> int:
         return self.max_context or (self.prefill + self.decode_steps)
@@ -160,8 +170,8 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
     h = P.stage_init(cfg)
     res = RunResult()
     try:
-        for l in range(shape.n_layers):
-            P.stage_load_layer(h, l, weights(l), 1 if l < sc.resident_layers() else 0)
+        for l, code in enumerate(sc.codes()):
+            P.stage_load_layer(h, l, weights(l), code)
         prev: Dict[Tuple[int, int], np.ndarray] = {}
         outs = []
         for kind, mbs, step in sc.call_plan():
@@ -215,7 +225,7 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
     n_blocks = wl.n_mb * wl.batch * math.ceil(sc.ctx() / 16)
     alloc = BlockAllocator(n_blocks, 16)
     slots = SlotSchedule(sc.slots)
-    resid = ResidencySchedule(shape.n_layers, range(sc.resident_layers()), sc.thresholds)
+    resid = ResidencySchedule(shape.n_layers, thresholds=sc.thresholds, codes=sc.codes())
     res = RunResult()
     prev: Dict[Tuple[int, int], np.ndarray] = {}
     # Without feedback every call's inputs are known up front, so the oracle runs once over each
@@ -272,7 +282,7 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
             res.block_tables[(m, b)] = alloc.table((m, b))
     res.slot_log = list(slots.log)
     res.demotion_log = list(resid.log)
-    res.residency = [1 if l in resid.resident else 0 for l in range(shape.n_layers)]
+    res.residency = list(resid.codes)
     res._oracle = orc
     return res
 

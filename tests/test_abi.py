@@ -32,6 +32,15 @@ def test_library_exports_every_declared_symbol():
     assert sorted(P.EXPORTED) == declared_functions()
 
 
+def test_binding_constants_match_header():
+    """Every #define STAGE_* of the header is exported by the package with the same value."""
+    import paper_2512_21835_amd as P
+    defines = re.findall(r"^#define (STAGE_\w+) (-?\d+)", open(HEADER).read(), flags=re.M)
+    assert len(defines) >= 10
+    for name, value in defines:
+        assert getattr(P, name, None) == int(value), name
+
+
 def test_struct_layout_matches_binding(tmp_path):
     import paper_2512_21835_amd as P
     fields = [f[0] for f in P.StageConfig._fields_]

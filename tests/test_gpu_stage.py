@@ -98,6 +98,126 @@ def test_zero_copy_decode_equals_slot_staging(wl, prefill, steps):
     assert ref.stats["bytes_direct"] == 0
 
 
+@pytest.mark.parametrize("wl,prefill,steps,codes,zero_copy", [
+    (TINY_RAGGED, 37, 6, (2, 3), False),
+    (TINY_RAGGED, 37, 6, (3, 0), True),
+    (LLAMA8B_MULTI, 24, 3, (1, 2, 3, 0, 2, 3, 1, 0), False),
+])
+def test_block_offload_is_lossless(wl, prefill, steps, codes, zero_copy):
+    """MHA-only and MLP-only offloading (Section III-D) give the all-resident outputs bit for bit;
+    every layer with an offloaded block takes one slot load per staged call, and exactly the
+    offloaded blocks cross the host link."""
+    _gpu()
+    base = Scenario(wl, prefill=prefill, decode_steps=steps, calls="all")
+    ref = run_gpu(base)
+    sc = dataclasses.replace(base, residency=codes, zero_copy=zero_copy)
+    got = run_gpu(sc)
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    orc = run_oracle(sc, floats=False)
+    assert got.slot_log == orc.slot_log
+    assert got.residency == list(codes)
+    st = got.stats
+    per_call = sum((c in (0, 2)) * st["mha_block_bytes"] + (c in (0, 3)) * st["mlp_block_bytes"] for c in codes)
+    staged_calls = 1 if zero_copy else 1 + steps
+    assert st["bytes_streamed"] == staged_calls * per_call
+    assert st["bytes_direct"] == (steps * per_call if zero_copy else 0)
+    assert st["offloaded_mha_blocks"] == sum(c in (0, 2) for c in codes)
+    assert st["offloaded_mlp_blocks"] == sum(c in (0, 3) for c in codes)
+
+
+def test_block_residency_changes_between_calls_and_budget():
+    """Blocks move between HBM and host memory between calls without changing a bit; the weight
+    budget is counted in bytes, so one layer's worth holds the MHA block of one layer and the MLP
+    block of another."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape = synth.TINY
+    w = weights_of(shape)
+    wl = TINY_RAGGED
+    cs = compute_stream().__enter__()
+    x = torch.from_numpy(synth.prefill_inputs(wl, 0, 0, 37)).cuda()
+    steps = [torch.from_numpy(synth.decode_input(wl, 0, 0, t)[None]).cuda() for t in range(4)]
+
+    def run(budget, codes_per_call):
+        cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=budget,
+                           compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        try:
+            for l in range(2):
+                P.stage_load_layer(h, l, w(l), codes_per_call[0][l])
+            P.stage_prefill(h, [0], 1, 37, x, torch.empty_like(x))
+            outs = []
+            for t, xt in enumerate(steps):
+                for l, c in enumerate(codes_per_call[t + 1]):
+                    P.stage_load_layer(h, l, None, c)
+                y = torch.empty_like(xt)
+                P.stage_decode(h, [0], 1, xt, y)
+                outs.append(y)
+            P.stage_sync(h)
+            return [o.cpu() for o in outs], P.stage_get_residency(h, 2), P.stage_get_stats(h)
+        finally:
+            P.stage_destroy(h)
+
+    ref, _, _ = run(2, [(1, 1)] * 5)
+    plan = [(1, 1), (2, 3), (3, 2), (0, 1), (1, 0)]
+    got, res, _ = run(2, plan)
+    assert res == [1, 0]
+    for a, b in zip(got, ref):
+        assert torch.equal(a, b)
+    # budget of one layer: MHA of layer 0 plus MLP of layer 1 fit, a whole extra layer does not
+    got, res, st = run(1, [(3, 2)] * 5)
+    assert res == [3, 2] and st["hbm_weight_bytes"] == st["layer_bytes"] * (1 + st["stream_slots"])
+    for a, b in zip(got, ref):
+        assert torch.equal(a, b)
+    cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=1,
+                       compute_stream=cs.handle)
+    h = P.stage_init(cfg)
+    try:
+        P.stage_load_layer(h, 0, w(0), P.STAGE_RES_MLP_OFFLOADED)
+        P.stage_load_layer(h, 1, w(1), P.STAGE_RES_MHA_OFFLOADED)
+        with pytest.raises(P.StageError) as e:
+            P.stage_load_layer(h, 0, None, P.STAGE_RES_RESIDENT)
+        assert e.value.code == P.STAGE_ENOMEM
+        assert P.stage_get_residency(h, 2) == [3, 2]
+        with pytest.raises(P.StageError) as e:
+            P.stage_load_layer(h, 0, None, 4)
+        assert e.value.code == P.STAGE_EINVAL
+    finally:
+        P.stage_destroy(h)
+        cs.__exit__(None, None, None)
+
+
+def test_attention_starts_before_the_mlp_block_arrives():
+    """Per-block readiness: a streamed layer's kernels start once its MHA block is in the slot,
+    while its MLP block is still being copied, and finish after that copy (8B-shaped layers, all
+    streamed, events on both streams)."""
+    _gpu()
+    import paper_2512_21835_amd as P
+    wl = LLAMA8B_MULTI
+    sc = Scenario(wl, prefill=24, decode_steps=2, calls="all", n_resident=0,
+                  timing=P.STAGE_TIME_CALLS | P.STAGE_TIME_LAYERS)
+    got = run_gpu(sc)
+    ref = run_gpu(dataclasses.replace(sc, n_resident=None, timing=0))
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    tl = got.timeline
+    ends = [i for i, r in enumerate(tl) if r[0] == 0]
+    seg = tl[ends[-2] + 1: ends[-1] + 1]          # the last decode call
+    mha_copy = {int(l): (a, b) for k, l, a, b in seg if k == 1}
+    mlp_copy = {int(l): (a, b) for k, l, a, b in seg if k == 4}
+    mha_comp = {int(l): (a, b) for k, l, a, b in seg if k == 3}
+    mlp_comp = {int(l): (a, b) for k, l, a, b in seg if k == 5}
+    layers = list(range(wl.shape.n_layers))
+    assert sorted(mha_copy) == sorted(mlp_copy) == sorted(mha_comp) == sorted(mlp_comp) == layers
+    for l in layers:
+        assert mha_copy[l][1] <= mha_comp[l][0] + 1e-3    # MHA block in place before attention starts
+        assert mha_comp[l][1] < mlp_copy[l][1]            # attention done while the MLP block streams
+        assert mlp_comp[l][0] >= mlp_copy[l][1] - 1e-3    # the MLP kernels waited for it
+        assert mlp_comp[l][0] >= mha_comp[l][1] - 1e-3
+
+
 def _one_vs_all(wl, prefill, steps):
     a = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="one"))
     b = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="all"))

@@ -76,6 +76,20 @@ def test_residency_one_demotion_per_round():
     assert [r.before_call(c, 32 + c) for c in range(5)] == [[], [3], [2], [1], []]
 
 
+def test_residency_codes_block_granular():
+    """Layers with one offloaded block stream; a threshold offloads both blocks of the highest
+    layer holding any resident block."""
+    r = ResidencySchedule(5, thresholds=[10, 20, 30], codes=[1, 1, 2, 3, 0])
+    assert r.streamed() == [2, 3, 4] and r.resident == {0, 1}
+    assert r.before_call(0, 10) == [3]
+    assert r.codes == [1, 1, 2, 0, 0]
+    assert r.before_call(1, 30) == [2, 1]
+    assert r.codes == [1, 0, 0, 0, 0] and r.streamed() == [1, 2, 3, 4]
+    s = SlotSchedule(n_slots=2)
+    s.call(0, r.streamed())
+    assert s.log == [(0, 1, 0), (0, 2, 1), (0, 3, 0), (0, 4, 1)]
+
+
 # ----------------------------------------------------------------- generator
 def test_splitmix64_matches_published_reference():
     ref = [int(l) for l in open(os.path.join(GOLDEN, "splitmix64_seed1234567.txt")) if l.strip() and l[0] != "#"]
