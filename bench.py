@@ -297,6 +297,94 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
     return res
 
 
+def planner_leg(calls: int = 3, ctx: int = 2048, n_steps: int = 6):
+    """The 70B-shaped stage, all 16 layers allocated resident, 4 micro-batches of batch 1 decoded
+    in one call each step, under the online planner (Eq. (7), stage_plan_offload): the memory left
+    for the cache holds the four sequences at context `ctx` plus 64 tokens (so TS^1 = 4*ctx + 64,
+    Eq. (6)), each offloaded block frees its bytes once (#Stage = 2) and a block's loading time is
+    its bytes.  The cache is grown through stage_kv_append (random K/V) to each of the first
+    `n_steps` thresholds in turn; at each, the first decode call applies the step (its extra wall
+    time is the switch), then `calls` more calls give the step's call time.  Weights are random
+    bf16 generated on the device (timing only; parity of planner-driven residency is covered by
+    the tests)."""
+    import torch
+
+    import synth
+    import paper_2512_21835_amd as P
+
+    shape = synth.LLAMA70B_STAGE
+    dev = torch.device("cuda", 0)
+    cstream = torch.cuda.current_stream(dev)
+    xstream = torch.cuda.Stream(dev)
+    L, n_mb = shape.n_layers, 4
+    kv_token = 2 * shape.kv_dim * 2 * L            # bytes of one token's K and V over the stage
+    probe = P.stage_init(P.config_for(shape, max_microbatches=1, max_batch=1, max_context=16, n_resident_max=L,
+                                      compute_stream=cstream.cuda_stream))
+    try:
+        st = P.stage_get_stats(probe)
+    finally:
+        P.stage_destroy(probe)
+    mha, mlp = st["mha_block_bytes"], st["mlp_block_bytes"]
+    steps, capacity = P.stage_plan_offload((n_mb * ctx + 64) * kv_token, kv_token, mha, mlp, mha, mlp, L, L, 2)
+    steps = steps[:n_steps]
+    max_ctx = ctx + (steps[-1][0] - n_mb * ctx) // n_mb + 2 * (calls + 2) + 16
+    cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=max_ctx, n_resident_max=L,
+                       compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream, plan=steps)
+    h = P.stage_init(cfg)
+    gen = torch.Generator(device=dev).manual_seed(2514)
+    out = []
+    try:
+        for l in range(L):
+            w = {}
+            for name, shp in synth.layer_weight_shapes(shape).items():
+                t = torch.randn(shp, generator=gen, device=dev) * 0.02 + (1.0 if name in ("g1", "g2") else 0.0)
+                w[name] = t.to(torch.bfloat16).view(torch.int16).contiguous()
+            P.stage_load_layer(h, l, w, 1)
+            del w
+
+        def grow(per_seq):
+            if per_seq <= 0:
+                return
+            for m in range(n_mb):
+                kv = [torch.randn(L, per_seq, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
+                      .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)]
+                P.stage_kv_append(h, m, 0, per_seq, kv[0], kv[1])
+
+        def held():
+            return sum(P.stage_get_length(h, m, 0) for m in range(n_mb))
+
+        grow(ctx)
+        x = torch.randn(n_mb, 1, shape.hidden, generator=gen, device=dev)
+        y = torch.empty_like(x)
+
+        def call():
+            t0 = time.perf_counter()
+            P.stage_decode(h, list(range(n_mb)), 1, x, y)
+            P.stage_sync(h)
+            return (time.perf_counter() - t0) * 1e3
+
+        for k, (tokens, alpha, beta) in enumerate(steps):
+            if k > 0:
+                grow(-(-(tokens - n_mb - held()) // n_mb))
+            first = call()
+            steady = [call() for _ in range(calls)]
+            per = sum(steady) / len(steady)
+            out.append({"tokens": held(), "threshold": tokens, "alpha": alpha, "beta": beta,
+                        "residency": "".join(map(str, P.stage_get_residency(h, L))), "first_call_ms": first,
+                        "call_ms": per,
+                        "switch_ms": first - per, "offloaded_GB_per_call": (alpha * mha + beta * mlp) / 1e9})
+        log = P.stage_get_residency_log(h)
+    finally:
+        P.stage_destroy(h)
+    return {
+        "workload": f"llama70b planner: 16 layers (hidden 8192, 64/8 heads, ffn 28672) allocated resident, 4 "
+                    f"micro-batches of batch 1 per decode call, cache grown from context {ctx} through the "
+                    f"first {len(steps)} steps of the online planner (Eq. (7), #Stage 2, cost = block bytes)",
+        "mha_block_bytes": mha, "mlp_block_bytes": mlp, "kv_bytes_per_token": kv_token,
+        "capacity_tokens": capacity, "steps": out, "residency_changes": len(log),
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -305,6 +393,8 @@ def main() -> int:
     ap.add_argument("--prefill", type=int, default=1024)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
+    ap.add_argument("--planner-calls", type=int, default=3,
+                    help="timed calls per planner step of the 70B planner leg (0 = skip)")
     ap.add_argument("--resident70b-rounds", type=int, default=8,
                     help="timed decode rounds of the resident 70B leg (0 = skip)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -404,6 +494,8 @@ def main() -> int:
     }
     if args.resident70b_rounds > 0:
         out["resident70b"] = resident70b_leg(args.resident70b_rounds)
+    if args.planner_calls > 0:
+        out["planner"] = planner_leg(args.planner_calls)
     if args.offload_calls > 0:
         out["offload"] = offload_leg(args.offload_calls)
         out["offload_zero_copy"] = offload_leg(args.offload_calls, zero_copy=True)

@@ -108,6 +108,19 @@ typedef struct {
        prefills still stage through the slots, since their GEMMs re-read every weight tile.
        Outputs are identical in both modes. */
     int32_t zero_copy;
+    /* Residency schedule mode.  0: the thresholds above (longest sequence; each offloads one more
+       layer).  1: steps of the online memory-aware planner (Section III-E, Eq. (7); computed by
+       stage_plan_offload, include/stage_planner.h): thresholds[j] counts the tokens the stage
+       holds over all sequences once the call's tokens are appended, ascending from >= 0.  While
+       it holds at least thresholds[j] tokens (and fewer than thresholds[j+1]), the plan_alpha[j]
+       highest-id layers whose MHA block the loaded allocation keeps resident have it offloaded,
+       and likewise plan_beta[j] MLP blocks (all of them if fewer); below thresholds[0] the
+       allocation stands.  The allocation is the residency last set by stage_load_layer.  The plan
+       follows the token count both ways: a cache that shrinks (stage_kv_export_tail with drop,
+       stage_reset_sequence) reloads blocks at the next call. */
+    int32_t plan_mode;
+    int32_t plan_alpha[STAGE_MAX_THRESHOLDS];
+    int32_t plan_beta[STAGE_MAX_THRESHOLDS];
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
@@ -196,9 +209,15 @@ int stage_get_residency(stage *s, int32_t *out);
    Writes min(cap, count) triples (3*cap ints), *n = count. */
 int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
-/* Demotions made by the residency schedule: (call number, layer) pairs, like the slot log.  A
-   demotion offloads both blocks of the highest-id layer that still has a resident block. */
+/* Demotions made by the threshold schedule (plan_mode 0): (call number, layer) pairs, like the
+   slot log.  A demotion offloads both blocks of the highest-id layer that still has a resident
+   block. */
 int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
+
+/* Every residency change made by the schedule, in either plan_mode: (call number, layer, new
+   STAGE_RES_* code) triples in the order applied (within a call, ascending layer).  Writes
+   min(cap, count) triples (3*cap ints), *n = count. */
+int stage_get_residency_log(stage *s, int32_t *entries, int32_t cap, int32_t *n);
 
 /* Timeline recorded under stage_config.timing, then cleared.  Synchronises.  Each record is
    four floats: kind (0 call, 1 slot copy of an MHA block, 2 gate/up kernel, 3 a layer's

@@ -9,5 +9,7 @@ read their inputs from ``synth`` (shapes, seeds, random numbers only).
 * ``policies``: independent re-implementations of the integer policies (paged
   KV block allocation, slot assignment of streamed layers, residency schedule)
   whose results the HIP runtime must reproduce bit-exactly.
+* ``planner``: the online memory-aware planner (Eq. (7)) by brute force over
+  every (alpha, beta), one token count at a time.
 """
-from . import stage_oracle, policies  # noqa: F401
+from . import stage_oracle, policies, planner  # noqa: F401

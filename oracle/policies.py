@@ -27,6 +27,14 @@ open; the readings are:
   Every threshold TS^j <= c not yet applied offloads both blocks of one layer
   that still has a resident block, the highest id first, so with whole-layer
   residency a prefix of layers stays resident.
+* Planner steps (Section III-E, Eq. (7): alpha more MHA blocks and beta more MLP
+  blocks offloaded once the cache reaches a threshold; plans are not nested).
+  Before a call, let h be the tokens the stage holds over all sequences once the
+  call's tokens are appended; the last step with threshold <= h gives (alpha,
+  beta), none below the first.  Starting from the allocation (the codes the
+  layers were loaded with), the alpha highest-id layers whose MHA block it keeps
+  resident offload that block, likewise beta MLP blocks; layers whose code
+  differs from this target change, ascending, each change logged.
 """
 from __future__ import annotations
 
@@ -104,15 +112,42 @@ class ResidencySchedule:
     gives every layer's code."""
 
     def __init__(self, n_layers: int, resident: Iterable[int] = (), thresholds: Sequence[int] = (),
-                 codes: Optional[Sequence[int]] = None):
+                 codes: Optional[Sequence[int]] = None, plan: Optional[Sequence[Tuple[int, int, int]]] = None):
         self.n_layers = n_layers
         keep = set(resident)
         self.codes = list(codes) if codes is not None else [RESIDENT if l in keep else OFFLOADED
                                                             for l in range(n_layers)]
         assert len(self.codes) == n_layers
+        self.allocation = list(self.codes)
         self.thresholds = list(thresholds)
+        self.plan = None if plan is None else [tuple(p) for p in plan]
         self.applied = 0
-        self.log: List[Tuple[int, int]] = []        # (call number, demoted layer)
+        self.log: List[Tuple[int, int]] = []        # (call number, demoted layer), threshold schedule
+        self.changes: List[Tuple[int, int, int]] = []   # (call number, layer, new code), either schedule
+
+    def _plan_target(self, alpha: int, beta: int) -> List[int]:
+        mha = [c in (RESIDENT, MLP_OFFLOADED) for c in self.allocation]   # MHA block resident
+        mlp = [c in (RESIDENT, MHA_OFFLOADED) for c in self.allocation]
+        for keep, count in ((mha, alpha), (mlp, beta)):
+            for layer in reversed(range(self.n_layers)):
+                if count == 0:
+                    break
+                if keep[layer]:
+                    keep[layer] = False
+                    count -= 1
+        table = {(True, True): RESIDENT, (False, False): OFFLOADED, (False, True): MHA_OFFLOADED,
+                 (True, False): MLP_OFFLOADED}
+        return [table[(a, m)] for a, m in zip(mha, mlp)]
+
+    def before_call_planned(self, call_no: int, held_after_call: int) -> None:
+        alpha = beta = 0
+        for tokens, a, b in self.plan:
+            if tokens <= held_after_call:
+                alpha, beta = a, b
+        for layer, code in enumerate(self._plan_target(alpha, beta)):
+            if code != self.codes[layer]:
+                self.codes[layer] = code
+                self.changes.append((call_no, layer, code))
 
     @property
     def resident(self) -> set:
@@ -128,6 +163,7 @@ class ResidencySchedule:
                 self.codes[layer] = OFFLOADED
                 demoted.append(layer)
                 self.log.append((call_no, layer))
+                self.changes.append((call_no, layer, OFFLOADED))
         return demoted
 
     def streamed(self) -> List[int]:

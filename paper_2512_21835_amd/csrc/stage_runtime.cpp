@@ -51,8 +51,8 @@ constexpr int kMha = 0, kMlp = 1;  // block index: MHA (Wqkv, Wo, g1), MLP (Wg, 
 
 struct Block {
     bool resident = false;
-    void *dev = nullptr;       // HBM copy when resident
-    void *host = nullptr;      // pinned host copy when offloaded
+    void *dev = nullptr;       // HBM copy, exactly when resident
+    void *host = nullptr;      // pinned host copy: always when offloaded, kept once made
     void *host_dev = nullptr;  // the pinned copy as kernels address it (zero copy)
 };
 
@@ -100,8 +100,9 @@ struct stage {
     std::vector<void *> slots;
     std::vector<hipEvent_t> slot_ready[2], slot_free;
     long long loads = 0, calls = 0;
-    std::vector<int> slot_log, demotion_log;
+    std::vector<int> slot_log, demotion_log, residency_log;
     int thresholds_applied = 0;
+    std::vector<int> base_code;  // the allocation: residency last set by stage_load_layer
 
     void *kv_pool = nullptr;
     size_t kv_block_bytes = 0, kv_layer_stride = 0;
@@ -238,29 +239,39 @@ void free_block(Block &k) {
     k = Block();
 }
 
-// A new home for block b: HBM if resident, else pinned host memory (mapped for zero copy).
+int alloc_dev(stage *s, int b, void **dev) {
+    if (hipMalloc(dev, s->blk_bytes[b]) != hipSuccess) {
+        (void)hipGetLastError();
+        *dev = nullptr;
+        return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte weight block failed", s->blk_bytes[b]);
+    }
+    return STAGE_OK;
+}
+
+// Pinned host memory for block b, with its device address for zero copy.
+int alloc_host(stage *s, int b, Block *k) {
+    if (hipHostMalloc(&k->host, s->blk_bytes[b], hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        k->host = nullptr;
+        return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte weight block failed", s->blk_bytes[b]);
+    }
+    if (s->cfg.zero_copy) {
+        hipError_t e = hipHostGetDevicePointer(&k->host_dev, k->host, 0);
+        if (e != hipSuccess) {
+            (void)hipHostFree(k->host);
+            k->host = k->host_dev = nullptr;
+            return s->fail_hip(e, "hipHostGetDevicePointer");
+        }
+    }
+    return STAGE_OK;
+}
+
+// A new home for block b at load time: HBM if resident, else pinned host memory.
 int alloc_block(stage *s, int b, bool resident, Block *out) {
     Block k;
     k.resident = resident;
-    const size_t bytes = s->blk_bytes[b];
-    if (resident) {
-        if (hipMalloc(&k.dev, bytes) != hipSuccess) {
-            (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "hipMalloc of a %zu-byte weight block failed", bytes);
-        }
-    } else {
-        if (hipHostMalloc(&k.host, bytes, hipHostMallocDefault) != hipSuccess) {
-            (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "hipHostMalloc of a %zu-byte weight block failed", bytes);
-        }
-        if (s->cfg.zero_copy) {
-            hipError_t e = hipHostGetDevicePointer(&k.host_dev, k.host, 0);
-            if (e != hipSuccess) {
-                free_block(k);
-                return s->fail_hip(e, "hipHostGetDevicePointer");
-            }
-        }
-    }
+    int rc = resident ? alloc_dev(s, b, &k.dev) : alloc_host(s, b, &k);
+    if (rc) return rc;
     *out = k;
     return STAGE_OK;
 }
@@ -282,42 +293,62 @@ int check_residency(stage *s, int layer, int code) {
 }
 
 // Moves the blocks of a loaded layer between HBM and pinned host memory (the planner's offload
-// action, Section III-E; block granularity, Section III-D).  New homes are allocated before
-// anything moves, so a failed allocation leaves the layer as it was.
+// action, Section III-E; block granularity, Section III-D).  Weights never change, so a block's
+// pinned host copy, once made, is kept: offloading it again only frees its HBM copy, and only a
+// reload moves bytes.  Everything a move needs is allocated before anything moves, so a failed
+// allocation leaves the layer as it was.
 int set_residency(stage *s, int layer, int code) {
     Layer &ly = s->layers[layer];
     if (code_of(ly) == code) return STAGE_OK;
     int rc = check_residency(s, layer, code);
     if (rc) return rc;
-    Block fresh[2];
+    Block fresh[2];  // new HBM copies (reloads) or first host copies (first offloads)
     bool moves[2];
+    auto release = [&]() {
+        for (Block &k : fresh) free_block(k);
+    };
     for (int b = 0; b < 2; ++b) {
-        moves[b] = code_keeps(code, b) != ly.blk[b].resident;
+        const Block &k = ly.blk[b];
+        moves[b] = code_keeps(code, b) != k.resident;
         if (!moves[b]) continue;
-        rc = alloc_block(s, b, code_keeps(code, b), &fresh[b]);
+        rc = k.resident ? (k.host ? STAGE_OK : alloc_host(s, b, &fresh[b])) : alloc_dev(s, b, &fresh[b].dev);
         if (rc) {
-            free_block(fresh[0]);
+            release();
             return rc;
         }
     }
-    rc = sync_all(s);
+    rc = sync_all(s);  // no kernel or copy may still read what is freed below
     if (rc) {
-        for (Block &k : fresh) free_block(k);
+        release();
         return rc;
     }
     for (int b = 0; b < 2; ++b) {
         if (!moves[b]) continue;
-        Block &old = ly.blk[b];
-        void *dst = fresh[b].resident ? fresh[b].dev : fresh[b].host;
-        const void *src = old.resident ? old.dev : old.host;
-        hipError_t e = hipMemcpy(dst, src, s->blk_bytes[b], hipMemcpyDefault);
-        if (e != hipSuccess) {
-            for (Block &k : fresh) free_block(k);
-            return s->fail_hip(e, "moving a weight block");
+        Block &k = ly.blk[b];
+        if (k.resident) {
+            if (fresh[b].host) {
+                hipError_t e = hipMemcpy(fresh[b].host, k.dev, s->blk_bytes[b], hipMemcpyDeviceToHost);
+                if (e != hipSuccess) {
+                    release();
+                    return s->fail_hip(e, "copying a weight block to host memory");
+                }
+                k.host = fresh[b].host;
+                k.host_dev = fresh[b].host_dev;
+                fresh[b].host = fresh[b].host_dev = nullptr;
+            }
+            (void)hipFree(k.dev);
+            k.dev = nullptr;
+            k.resident = false;
+        } else {
+            hipError_t e = hipMemcpy(fresh[b].dev, k.host, s->blk_bytes[b], hipMemcpyHostToDevice);
+            if (e != hipSuccess) {
+                release();
+                return s->fail_hip(e, "copying a weight block to HBM");
+            }
+            k.dev = fresh[b].dev;
+            fresh[b].dev = nullptr;
+            k.resident = true;
         }
-        free_block(old);
-        old = fresh[b];
-        fresh[b] = Block();
     }
     return STAGE_OK;
 }
@@ -668,6 +699,36 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     return STAGE_OK;
 }
 
+// Planner steps (plan_mode 1): the step that holds `held` tokens offloads alpha MHA and beta MLP
+// blocks beyond the allocation, the highest-id layers first (Section III-E, Eq. (7)); layers whose
+// residency differs from that target move, ascending.  The target keeps a subset of the
+// allocation's resident blocks, so it always fits the budget the allocation fits.
+int apply_plan(stage *s, long long call_no, long long held) {
+    const stage_config &c = s->cfg;
+    int step = -1;
+    for (int j = 0; j < c.n_thresholds; ++j)
+        if (c.thresholds[j] <= held) step = j;
+    int alpha = step < 0 ? 0 : c.plan_alpha[step], beta = step < 0 ? 0 : c.plan_beta[step];
+    std::vector<bool> keep_a(s->L), keep_m(s->L);
+    for (int l = 0; l < s->L; ++l) {
+        keep_a[l] = code_keeps(s->base_code[l], kMha);
+        keep_m[l] = code_keeps(s->base_code[l], kMlp);
+    }
+    for (int l = s->L - 1; l >= 0 && alpha > 0; --l)
+        if (keep_a[l]) { keep_a[l] = false; --alpha; }
+    for (int l = s->L - 1; l >= 0 && beta > 0; --l)
+        if (keep_m[l]) { keep_m[l] = false; --beta; }
+    for (int l = 0; l < s->L; ++l) {
+        const int code = keep_a[l] ? (keep_m[l] ? STAGE_RES_RESIDENT : STAGE_RES_MLP_OFFLOADED)
+                                   : (keep_m[l] ? STAGE_RES_MHA_OFFLOADED : STAGE_RES_OFFLOADED);
+        if (code == code_of(s->layers[l])) continue;
+        int rc = set_residency(s, l, code);
+        if (rc) return rc;
+        for (int v : {(int)call_no, l, code}) s->residency_log.push_back(v);
+    }
+    return STAGE_OK;
+}
+
 // Shared body of prefill and decode.
 int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
              bool decode) {
@@ -712,7 +773,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     // stages nothing; in zero-copy mode the slots are allocated by the first call that stages.
     const bool direct = c.zero_copy && T == 1;
     if (!direct && s->slots.empty()) {
-        bool may_stream = s->thresholds_applied < c.n_thresholds;
+        bool may_stream = c.plan_mode ? c.n_thresholds > 0 : s->thresholds_applied < c.n_thresholds;
         for (const Layer &ly : s->layers) may_stream = may_stream || ly.streams();
         if (may_stream) {
             rc = ensure_slots(s);
@@ -721,8 +782,15 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     }
 
     const long long call_no = s->calls;
-    // residency schedule: thresholds reached by this call demote resident layers, highest first
-    while (s->thresholds_applied < c.n_thresholds && c.thresholds[s->thresholds_applied] <= longest) {
+    if (c.plan_mode) {
+        long long held = (long long)rows;
+        for (int len : s->lengths) held += len;
+        rc = apply_plan(s, call_no, held);
+        if (rc) return rc;
+    }
+    // threshold schedule: thresholds reached by this call demote resident layers, highest first
+    while (!c.plan_mode && s->thresholds_applied < c.n_thresholds &&
+           c.thresholds[s->thresholds_applied] <= longest) {
         s->thresholds_applied++;
         int victim = -1;
         for (int l = s->L - 1; l >= 0; --l)
@@ -732,6 +800,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         if (rc) return rc;
         s->demotion_log.push_back((int)call_no);
         s->demotion_log.push_back(victim);
+        for (int v : {(int)call_no, victim, (int)STAGE_RES_OFFLOADED}) s->residency_log.push_back(v);
     }
 
     rc = allocate_blocks(s, slots, T);
@@ -863,8 +932,12 @@ int stage_init(const stage_config *cfg, stage **out) {
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
                         (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1);
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
-    for (int i = 0; i < c.n_thresholds; ++i)
-        if (c.thresholds[i] < 1 || (i > 0 && c.thresholds[i] < c.thresholds[i - 1])) return STAGE_EINVAL;
+    if (c.plan_mode != 0 && c.plan_mode != 1) return STAGE_EINVAL;
+    for (int i = 0; i < c.n_thresholds; ++i) {
+        if (c.thresholds[i] < (c.plan_mode ? 0 : 1) || (i > 0 && c.thresholds[i] < c.thresholds[i - 1]))
+            return STAGE_EINVAL;
+        if (c.plan_mode && (c.plan_alpha[i] < 0 || c.plan_beta[i] < 0)) return STAGE_EINVAL;
+    }
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || c.device < 0 || c.device >= ndev) {
         (void)hipGetLastError();
@@ -891,6 +964,7 @@ int stage_init(const stage_config *cfg, stage **out) {
     s->blk_bytes[kMlp] = off;
     s->blob_bytes = s->blk_bytes[kMha] + s->blk_bytes[kMlp];
     s->layers.assign(s->L, Layer());
+    s->base_code.assign(s->L, STAGE_RES_OFFLOADED);
 
     s->n_seq_slots = c.max_microbatches * c.max_batch;
     s->max_blocks = (c.max_context + kBlockTokens - 1) / kBlockTokens;
@@ -975,7 +1049,9 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
     Layer &ly = s->layers[layer];
     if (!w) {
         if (!ly.loaded) return s->fail(STAGE_ESTATE, "layer %d was never loaded", layer);
-        return set_residency(s, layer, resident);
+        int rc = set_residency(s, layer, resident);
+        if (rc == STAGE_OK) s->base_code[layer] = resident;
+        return rc;
     }
     const void *src[9] = {w->wq, w->wk, w->wv, w->wo, w->wg, w->wu, w->wd, w->g1, w->g2};
     for (const void *p : src)
@@ -1015,6 +1091,7 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
         ly.blk[b] = fresh[b];
     }
     ly.loaded = true;
+    s->base_code[layer] = resident;
     return STAGE_OK;
 }
 
@@ -1175,6 +1252,11 @@ int stage_get_slot_log(stage *s, int32_t *entries, int32_t cap, int32_t *n) {
     return copy_log(s->slot_log, 3, entries, cap, n);
 }
 
+int stage_get_residency_log(stage *s, int32_t *entries, int32_t cap, int32_t *n) {
+    if (!s) return STAGE_EINVAL;
+    return copy_log(s->residency_log, 3, entries, cap, n);
+}
+
 int stage_get_demotion_log(stage *s, int32_t *entries, int32_t cap, int32_t *n) {
     if (!s) return STAGE_EINVAL;
     return copy_log(s->demotion_log, 2, entries, cap, n);
@@ -1218,8 +1300,10 @@ int stage_set_timing(stage *s, int32_t flags) {
 int stage_get_stats(stage *s, char *buf, int32_t cap) {
     if (!s || !buf || cap < 1) return STAGE_EINVAL;
     int res = 0, streamed = 0, off_mha = 0, off_mlp = 0;
+    size_t host_w = 0;
     for (const Layer &l : s->layers) {
         if (!l.loaded) continue;
+        for (int b = 0; b < 2; ++b) host_w += l.blk[b].host ? s->blk_bytes[b] : 0;
         res += code_of(l) == STAGE_RES_RESIDENT;
         streamed += l.streams();
         off_mha += !l.blk[kMha].resident;
@@ -1232,11 +1316,11 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
         "\"bytes_streamed\": %lld, \"bytes_direct\": %lld, \"layer_bytes\": %zu, \"mha_block_bytes\": %zu, "
         "\"mlp_block_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
         "\"offloaded_mha_blocks\": %d, \"offloaded_mlp_blocks\": %d, "
-        "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, \"kv_blocks\": %d, "
-        "\"kv_blocks_free\": %d}",
+        "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"host_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, "
+        "\"kv_blocks\": %d, \"kv_blocks_free\": %d}",
         s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes,
         s->blk_bytes[kMha], s->blk_bytes[kMlp], res, streamed, off_mha, off_mlp,
-        s->slots.size(), hbm_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
+        s->slots.size(), hbm_w, host_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }
 

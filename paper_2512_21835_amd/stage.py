@@ -13,7 +13,7 @@ from __future__ import annotations
 import ctypes
 import json
 import os
-from ctypes import POINTER, c_char_p, c_float, c_int32, c_void_p
+from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_void_p
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -34,8 +34,8 @@ EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",
     "stage_decode", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
-    "stage_get_demotion_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats", "stage_last_error",
-    "stage_strerror",
+    "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
+    "stage_last_error", "stage_strerror", "stage_plan_offload",
 )
 
 
@@ -50,7 +50,22 @@ class StageConfig(ctypes.Structure):
         ("n_thresholds", c_int32), ("thresholds", c_int32 * STAGE_MAX_THRESHOLDS),
         ("device", c_int32), ("compute_stream", c_void_p), ("copy_stream", c_void_p),
         ("timing", c_int32), ("zero_copy", c_int32),
+        ("plan_mode", c_int32), ("plan_alpha", c_int32 * STAGE_MAX_THRESHOLDS),
+        ("plan_beta", c_int32 * STAGE_MAX_THRESHOLDS),
     ]
+
+
+class StagePlanInput(ctypes.Structure):
+    """stage_plan_input of include/stage_planner.h."""
+    _fields_ = [
+        ("mem_left", c_int64), ("kv_bytes_per_token", c_int64), ("mha_bytes", c_int64), ("mlp_bytes", c_int64),
+        ("mha_cost", c_int64), ("mlp_cost", c_int64),
+        ("mha_free", c_int32), ("mlp_free", c_int32), ("n_stage", c_int32),
+    ]
+
+
+class StagePlanStep(ctypes.Structure):
+    _fields_ = [("tokens", c_int64), ("alpha", c_int32), ("beta", c_int32)]
 
 
 class StageLayerWeights(ctypes.Structure):
@@ -92,6 +107,9 @@ def lib():
         "stage_get_residency": (c_int32, [c_void_p, ip]),
         "stage_get_slot_log": (c_int32, [c_void_p, ip, c_int32, ip]),
         "stage_get_demotion_log": (c_int32, [c_void_p, ip, c_int32, ip]),
+        "stage_get_residency_log": (c_int32, [c_void_p, ip, c_int32, ip]),
+        "stage_plan_offload": (c_int32, [POINTER(StagePlanInput), POINTER(StagePlanStep), c_int32, ip,
+                                         POINTER(c_int64)]),
         "stage_get_timeline": (c_int32, [c_void_p, POINTER(c_float), c_int32, ip]),
         "stage_set_timing": (c_int32, [c_void_p, c_int32]),
         "stage_get_stats": (c_int32, [c_void_p, c_char_p, c_int32]),
@@ -220,6 +238,23 @@ def stage_get_demotion_log(h) -> List[Tuple[int, int]]:
     return _log(lib().stage_get_demotion_log, h, 2)
 
 
+def stage_get_residency_log(h) -> List[Tuple[int, int, int]]:
+    return _log(lib().stage_get_residency_log, h, 3)
+
+
+def stage_plan_offload(mem_left: int, kv_bytes_per_token: int, mha_bytes: int, mlp_bytes: int, mha_cost: int,
+                       mlp_cost: int, mha_free: int, mlp_free: int, n_stage: int
+                       ) -> Tuple[List[Tuple[int, int, int]], int]:
+    """The online planner's steps [(tokens, alpha, beta)] and the capacity in tokens."""
+    inp = StagePlanInput(mem_left, kv_bytes_per_token, mha_bytes, mlp_bytes, mha_cost, mlp_cost, mha_free, mlp_free,
+                         n_stage)
+    n, capacity = c_int32(), c_int64()
+    _check(lib().stage_plan_offload(ctypes.byref(inp), None, 0, ctypes.byref(n), ctypes.byref(capacity)))
+    buf = (StagePlanStep * max(1, n.value))()
+    _check(lib().stage_plan_offload(ctypes.byref(inp), buf, n.value, ctypes.byref(n), ctypes.byref(capacity)))
+    return [(buf[i].tokens, buf[i].alpha, buf[i].beta) for i in range(n.value)], capacity.value
+
+
 def stage_get_timeline(h) -> List[Tuple[int, int, float, float]]:
     n = c_int32()
     cap = 1 << 16
@@ -246,8 +281,10 @@ def stage_strerror(code: int) -> str:
 def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int, n_resident_max: int,
                n_stream_slots: int = 2, kv_fp32: bool = False, thresholds: Sequence[int] = (),
                kv_pool_blocks: int = 0, device: int = 0, compute_stream=None, copy_stream=None,
-               timing: int = 0, zero_copy: bool = False) -> StageConfig:
-    """A StageConfig for a stage shape (any object with the StageShape fields)."""
+               timing: int = 0, zero_copy: bool = False,
+               plan: Optional[Sequence[Tuple[int, int, int]]] = None) -> StageConfig:
+    """A StageConfig for a stage shape (any object with the StageShape fields).  ``plan``:
+    planner steps [(tokens, alpha, beta)] (plan_mode 1), instead of ``thresholds``."""
     cfg = stage_config_default()
     cfg.n_layers, cfg.hidden = shape.n_layers, shape.hidden
     cfg.n_q_heads, cfg.n_kv_heads = shape.n_q_heads, shape.n_kv_heads
@@ -257,6 +294,13 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
     cfg.kv_pool_blocks = kv_pool_blocks
     cfg.kv_fp32 = int(bool(kv_fp32))
     cfg.n_resident_max, cfg.n_stream_slots = n_resident_max, n_stream_slots
+    if plan is not None:
+        if thresholds:
+            raise ValueError("give thresholds or a plan, not both")
+        cfg.plan_mode = 1
+        thresholds = [t for t, _, _ in plan]
+        for i, (_, a, b) in enumerate(plan[:STAGE_MAX_THRESHOLDS]):
+            cfg.plan_alpha[i], cfg.plan_beta[i] = int(a), int(b)
     if len(thresholds) > STAGE_MAX_THRESHOLDS:
         raise ValueError("too many thresholds")
     cfg.n_thresholds = len(thresholds)

@@ -64,6 +64,7 @@ class Scenario:
     timing: int = 0
     zero_copy: bool = False
     residency: Optional[Tuple[int, ...]] = None   # per-layer STAGE_RES_* codes (block granularity)
+    plan: Optional[Tuple[Tuple[int, int, int], ...]] = None   # planner steps (tokens, alpha, beta)
 
     @property
     def shape(self):
@@ -102,6 +103,7 @@ class RunResult:
     block_tables: Dict[Tuple[int, int], List[int]] = field(default_factory=dict)
     slot_log: List[Tuple[int, int, int]] = field(default_factory=list)
     demotion_log: List[Tuple[int, int]] = field(default_factory=list)
+    residency_log: List[Tuple[int, int, int]] = field(default_factory=list)
     residency: List[int] = field(default_factory=list)
     stats: dict = field(default_factory=dict)
     timeline: list = field(default_factory=list)
@@ -166,7 +168,8 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
     cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=sc.ctx(),
                        n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
                        thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
-                       copy_stream=copy_stream.cuda_stream, timing=sc.timing, zero_copy=sc.zero_copy)
+                       copy_stream=copy_stream.cuda_stream, timing=sc.timing, zero_copy=sc.zero_copy,
+                       plan=sc.plan)
     h = P.stage_init(cfg)
     res = RunResult()
     try:
@@ -199,6 +202,7 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
                 res.block_tables[(m, b)] = P.stage_get_block_table(h, m, b)
         res.slot_log = P.stage_get_slot_log(h)
         res.demotion_log = P.stage_get_demotion_log(h)
+        res.residency_log = P.stage_get_residency_log(h)
         res.residency = P.stage_get_residency(h, shape.n_layers)
         res.stats = P.stage_get_stats(h)
         if sc.timing:
@@ -225,7 +229,7 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
     n_blocks = wl.n_mb * wl.batch * math.ceil(sc.ctx() / 16)
     alloc = BlockAllocator(n_blocks, 16)
     slots = SlotSchedule(sc.slots)
-    resid = ResidencySchedule(shape.n_layers, thresholds=sc.thresholds, codes=sc.codes())
+    resid = ResidencySchedule(shape.n_layers, thresholds=sc.thresholds, codes=sc.codes(), plan=sc.plan)
     res = RunResult()
     prev: Dict[Tuple[int, int], np.ndarray] = {}
     # Without feedback every call's inputs are known up front, so the oracle runs once over each
@@ -238,7 +242,10 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
         T = x.shape[2]
         keys = [(m, b) for m in mbs for b in range(wl.batch)]
         longest = max([alloc.lengths.get(k, 0) for k in alloc.lengths] + [alloc.lengths.get(k, 0) + T for k in keys])
-        resid.before_call(call_no, longest)
+        if sc.plan is not None:
+            resid.before_call_planned(call_no, sum(alloc.lengths.values()) + T * len(keys))
+        else:
+            resid.before_call(call_no, longest)
         alloc.call([(k, T) for k in keys])
         # zero-copy access (Section III-C): a call with one token per sequence reads offloaded
         # layers where they are, in host memory, so it stages nothing through the slots
@@ -282,6 +289,7 @@ def run_oracle(sc: Scenario, weights=None, floats: bool = True, kv_jitter: float
             res.block_tables[(m, b)] = alloc.table((m, b))
     res.slot_log = list(slots.log)
     res.demotion_log = list(resid.log)
+    res.residency_log = list(resid.changes)
     res.residency = list(resid.codes)
     res._oracle = orc
     return res

@@ -2,6 +2,7 @@
 its structs have the layout the binding assumes, and argument validation that
 needs no GPU rejects bad input."""
 import ctypes
+import glob
 import os
 import re
 import subprocess
@@ -10,10 +11,11 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "stage.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(stage_\w+)\s*\(", text)))
 
@@ -35,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 def test_binding_constants_match_header():
     """Every #define STAGE_* of the header is exported by the package with the same value."""
     import paper_2512_21835_amd as P
-    defines = re.findall(r"^#define (STAGE_\w+) (-?\d+)", open(HEADER).read(), flags=re.M)
+    defines = [d for h in HEADERS for d in re.findall(r"^#define (STAGE_\w+) (-?\d+)", open(h).read(), flags=re.M)]
     assert len(defines) >= 10
     for name, value in defines:
         assert getattr(P, name, None) == int(value), name
@@ -43,19 +45,24 @@ def test_binding_constants_match_header():
 
 def test_struct_layout_matches_binding(tmp_path):
     import paper_2512_21835_amd as P
-    fields = [f[0] for f in P.StageConfig._fields_]
+    structs = [("stage_config", P.StageConfig), ("stage_layer_weights", P.StageLayerWeights),
+               ("stage_plan_input", P.StagePlanInput), ("stage_plan_step", P.StagePlanStep)]
     src = tmp_path / "layout.c"
-    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "stage.h"', 'int main(void) {',
-             'printf("%zu %zu\\n", sizeof(stage_config), sizeof(stage_layer_weights));']
-    lines += [f'printf("%zu\\n", offsetof(stage_config, {f}));' for f in fields]
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "stage.h"', '#include "stage_planner.h"',
+             'int main(void) {']
+    want = []
+    for cname, py in structs:
+        lines.append(f'printf("%zu\\n", sizeof({cname}));')
+        want.append(ctypes.sizeof(py))
+        for f in py._fields_:
+            lines.append(f'printf("%zu\\n", offsetof({cname}, {f[0]}));')
+            want.append(getattr(py, f[0]).offset)
     lines += ['return 0; }']
     src.write_text("\n".join(lines))
     exe = tmp_path / "layout"
     subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
     out = subprocess.check_output([str(exe)]).decode().split()
-    assert int(out[0]) == ctypes.sizeof(P.StageConfig)
-    assert int(out[1]) == ctypes.sizeof(P.StageLayerWeights)
-    assert [int(x) for x in out[2:]] == [getattr(P.StageConfig, f).offset for f in fields]
+    assert [int(x) for x in out] == want
 
 
 def test_defaults_and_status_strings():

@@ -43,6 +43,7 @@ def check(name, sc, got, ref, tol_abs=TOL_ABS):
     assert got.block_tables == ref.block_tables
     assert got.slot_log == ref.slot_log
     assert got.demotion_log == ref.demotion_log
+    assert got.residency_log == ref.residency_log
     assert got.residency == ref.residency
     return m
 
@@ -160,10 +161,12 @@ def test_block_residency_changes_between_calls_and_budget():
         finally:
             P.stage_destroy(h)
 
-    ref, _, _ = run(2, [(1, 1)] * 5)
+    ref, _, st = run(2, [(1, 1)] * 5)
+    assert st["host_weight_bytes"] == 0
     plan = [(1, 1), (2, 3), (3, 2), (0, 1), (1, 0)]
-    got, res, _ = run(2, plan)
+    got, res, st = run(2, plan)
     assert res == [1, 0]
+    assert st["host_weight_bytes"] == 2 * st["layer_bytes"]     # host copies kept once made
     for a, b in zip(got, ref):
         assert torch.equal(a, b)
     # budget of one layer: MHA of layer 0 plus MLP of layer 1 fit, a whole extra layer does not
@@ -216,6 +219,63 @@ def test_attention_starts_before_the_mlp_block_arrives():
         assert mha_comp[l][1] < mlp_copy[l][1]            # attention done while the MLP block streams
         assert mlp_comp[l][0] >= mlp_copy[l][1] - 1e-3    # the MLP kernels waited for it
         assert mlp_comp[l][0] >= mha_comp[l][1] - 1e-3
+
+
+@pytest.mark.parametrize("zero_copy", [False, True])
+def test_planner_steps_drive_block_residency(zero_copy):
+    """Steps of the online planner (Eq. (7), computed by stage_plan_offload for a device whose
+    cache takes 8 KiB per token) applied while six ragged sequences grow: blocks leave and come
+    back (an MHA block is reloaded when the plan swaps it for an MLP block) exactly as the
+    oracle's policy says, and no output bit changes."""
+    _gpu()
+    import paper_2512_21835_amd as P
+    base = Scenario(TINY_RAGGED, prefill=37, decode_steps=20, calls="one")
+    ref = run_gpu(base)
+    st = ref.stats
+    steps, _ = P.stage_plan_offload(120 * 8192, 8192, st["mha_block_bytes"], st["mlp_block_bytes"],
+                                    st["mha_block_bytes"], st["mlp_block_bytes"], 2, 2, 2)
+    assert any(b[1] < a[1] for a, b in zip(steps, steps[1:]))     # a later step reloads MHA blocks
+    sc = dataclasses.replace(base, plan=tuple(steps), zero_copy=zero_copy)
+    got = run_gpu(sc)
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    orc = run_oracle(sc, floats=False)
+    assert got.residency_log == orc.residency_log and len(got.residency_log) >= 4
+    assert got.slot_log == orc.slot_log
+    assert got.residency == orc.residency
+    assert got.demotion_log == []
+
+
+def test_planner_reloads_blocks_when_the_cache_shrinks():
+    """The plan follows the token count down: dropping a sequence brings offloaded blocks back
+    at the next call."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape = synth.TINY
+    w = weights_of(shape)
+    wl = TINY_RAGGED
+    cs = compute_stream().__enter__()
+    cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=64, n_resident_max=2,
+                       compute_stream=cs.handle, plan=[(0, 0, 0), (60, 1, 0), (70, 2, 1)])
+    h = P.stage_init(cfg)
+    try:
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 1)
+        x = torch.from_numpy(synth.prefill_inputs(wl, 0, 0, 37)).cuda()
+        P.stage_prefill(h, [0], 1, 37, x, torch.empty_like(x))           # 37 tokens: allocation
+        assert P.stage_get_residency(h, 2) == [1, 1]
+        P.stage_prefill(h, [1], 1, 37, x, torch.empty_like(x))           # 74: two MHA + one MLP out
+        assert P.stage_get_residency(h, 2) == [2, 0]
+        P.stage_reset_sequence(h, 1, 0)
+        xt = torch.from_numpy(synth.decode_input(wl, 0, 0, 0)[None]).cuda()
+        P.stage_decode(h, [0], 1, xt, torch.empty_like(xt))               # 38: back to the allocation
+        P.stage_sync(h)
+        assert P.stage_get_residency(h, 2) == [1, 1]
+        assert P.stage_get_residency_log(h) == [(1, 0, 2), (1, 1, 0), (2, 0, 1), (2, 1, 1)]
+    finally:
+        P.stage_destroy(h)
+        cs.__exit__(None, None, None)
 
 
 def _one_vs_all(wl, prefill, steps):
