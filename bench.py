@@ -220,6 +220,7 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False):
         "link_GBs": streamed / (t_call * 1e-3) / 1e9, "h2d_peak_GBs": h2d_gbs,
         "link_util": streamed / (t_call * 1e-3) / 1e9 / h2d_gbs,
         "exposed_copy_ms": t_call - t_comp, "layer_loads": stats["layer_loads"],
+        "mha_block_bytes": stats["mha_block_bytes"], "mlp_block_bytes": stats["mlp_block_bytes"],
     }
 
 
@@ -385,6 +386,37 @@ def planner_leg(calls: int = 3, ctx: int = 2048, n_steps: int = 6):
     }
 
 
+def allocation_report(resident: dict, offload: dict, device_mem_gb=(32, 24, 20, 16), n_layers: int = 80):
+    """The cost model and the allocation scheduler fed with this run's measurements.
+
+    comp = one 70B-shaped layer's decode time for 4 micro-batches in one call (the resident leg),
+    load = a block's bytes over the measured pinned host-to-HBM rate (the offload leg).  Eq. (1)
+    for one device holding the offload leg's 4 resident + 12 offloaded layers is compared with
+    that leg's measured call time; Alg. 1 then allocates an 80-layer model of the same layer
+    shape over four devices with the given weight memories (a design study: one GPU is
+    measured, the others are assumed identical to it)."""
+    import paper_2512_21835_amd as P
+
+    layer_ms = resident["4_in_one_call"]["ms_per_call"] / 16
+    rate = offload["h2d_peak_GBs"] * 1e9 / 1e3            # bytes per ms
+    mha, mlp = offload["mha_block_bytes"], offload["mlp_block_bytes"]
+    ns = lambda ms: int(round(ms * 1e6))
+    comp, load_a, load_m = ns(layer_ms), ns(mha / rate), ns(mlp / rate)
+    # Eq. (1), one device, no hops: compute of 16 layers + the loading the 4 resident layers leave uncovered
+    predicted = (16 * comp + max(0, 12 * (load_a + load_m) - 4 * comp)) / 1e6
+    devices = [(int(g * 1e9), comp, load_a, load_m) for g in device_mem_gb]
+    n_stage, t_total, plans = P.stage_allocate(n_layers, mha, mlp, 0, devices)
+    return {
+        "inputs": {"layer_ms_4_microbatches": layer_ms, "load_mha_ms": load_a / 1e6, "load_mlp_ms": load_m / 1e6},
+        "eq1_offload_leg": {"predicted_ms_per_call": predicted, "measured_ms_per_call": offload["ms_per_call"],
+                            "ratio": offload["ms_per_call"] / predicted},
+        "alg1_80_layers": {"device_weight_memory_GB": list(device_mem_gb), "n_stage": n_stage,
+                           "t_total_ms": t_total / 1e6,
+                           "devices": [dict(zip(("first_layer", "assigned", "offloaded", "mha_only", "mlp_only"), p))
+                                       for p in plans]},
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -499,6 +531,8 @@ def main() -> int:
     if args.offload_calls > 0:
         out["offload"] = offload_leg(args.offload_calls)
         out["offload_zero_copy"] = offload_leg(args.offload_calls, zero_copy=True)
+        if "resident70b" in out:
+            out["allocation"] = allocation_report(out["resident70b"], out["offload"])
     if args.cpu_tokens > 0:
         out["cpu_baseline"] = cpu_baseline(shape, lambda l: weights[l], wl, args.cpu_tokens)
     print(json.dumps(out))

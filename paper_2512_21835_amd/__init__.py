@@ -13,5 +13,6 @@ from .stage import (  # noqa: F401
     stage_kv_append, stage_kv_export_tail, stage_reset_sequence, stage_sync, stage_get_block_table,
     stage_get_length, stage_get_residency, stage_get_slot_log, stage_get_demotion_log,
     stage_get_timeline, stage_set_timing, stage_get_stats, stage_strerror, stage_get_residency_log,
-    stage_plan_offload, StagePlanInput, StagePlanStep,
+    stage_plan_offload, StagePlanInput, StagePlanStep, stage_allocate, StageAllocDevice, StageAllocInput,
+    StageAllocPlan, STAGE_ALLOC_MAX_DEVICES, STAGE_ALLOC_MAX_LAYERS,
 )

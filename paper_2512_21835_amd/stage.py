@@ -35,8 +35,10 @@ EXPORTED = (
     "stage_decode", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
     "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
-    "stage_last_error", "stage_strerror", "stage_plan_offload",
+    "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate",
 )
+STAGE_ALLOC_MAX_DEVICES = 64
+STAGE_ALLOC_MAX_LAYERS = 4096
 
 
 class StageConfig(ctypes.Structure):
@@ -66,6 +68,21 @@ class StagePlanInput(ctypes.Structure):
 
 class StagePlanStep(ctypes.Structure):
     _fields_ = [("tokens", c_int64), ("alpha", c_int32), ("beta", c_int32)]
+
+
+class StageAllocDevice(ctypes.Structure):
+    """stage_alloc_device of include/stage_alloc.h."""
+    _fields_ = [("mem_bytes", c_int64), ("comp_layer", c_int64), ("load_mha", c_int64), ("load_mlp", c_int64)]
+
+
+class StageAllocInput(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("mha_bytes", c_int64), ("mlp_bytes", c_int64), ("comm", c_int64),
+                ("n_devices", c_int32), ("devices", POINTER(StageAllocDevice))]
+
+
+class StageAllocPlan(ctypes.Structure):
+    _fields_ = [("first_layer", c_int32), ("assigned", c_int32), ("offloaded", c_int32), ("mha_only", c_int32),
+                ("mlp_only", c_int32)]
 
 
 class StageLayerWeights(ctypes.Structure):
@@ -110,6 +127,7 @@ def lib():
         "stage_get_residency_log": (c_int32, [c_void_p, ip, c_int32, ip]),
         "stage_plan_offload": (c_int32, [POINTER(StagePlanInput), POINTER(StagePlanStep), c_int32, ip,
                                          POINTER(c_int64)]),
+        "stage_allocate": (c_int32, [POINTER(StageAllocInput), POINTER(StageAllocPlan), ip, POINTER(c_int64)]),
         "stage_get_timeline": (c_int32, [c_void_p, POINTER(c_float), c_int32, ip]),
         "stage_set_timing": (c_int32, [c_void_p, c_int32]),
         "stage_get_stats": (c_int32, [c_void_p, c_char_p, c_int32]),
@@ -253,6 +271,18 @@ def stage_plan_offload(mem_left: int, kv_bytes_per_token: int, mha_bytes: int, m
     buf = (StagePlanStep * max(1, n.value))()
     _check(lib().stage_plan_offload(ctypes.byref(inp), buf, n.value, ctypes.byref(n), ctypes.byref(capacity)))
     return [(buf[i].tokens, buf[i].alpha, buf[i].beta) for i in range(n.value)], capacity.value
+
+
+def stage_allocate(n_layers: int, mha_bytes: int, mlp_bytes: int, comm: int,
+                   devices: Sequence[Tuple[int, int, int, int]]) -> Tuple[int, int, List[Tuple[int, ...]]]:
+    """Alg. 1: (#Stage, T_total, [(first_layer, assigned, offloaded, mha_only, mlp_only)] per
+    device); devices are (mem_bytes, comp_layer, load_mha, load_mlp)."""
+    devs = (StageAllocDevice * len(devices))(*[StageAllocDevice(*d) for d in devices])
+    inp = StageAllocInput(n_layers, mha_bytes, mlp_bytes, comm, len(devices), devs)
+    out = (StageAllocPlan * len(devices))()
+    n_stage, t = c_int32(), c_int64()
+    _check(lib().stage_allocate(ctypes.byref(inp), out, ctypes.byref(n_stage), ctypes.byref(t)))
+    return n_stage.value, t.value, [(o.first_layer, o.assigned, o.offloaded, o.mha_only, o.mlp_only) for o in out]
 
 
 def stage_get_timeline(h) -> List[Tuple[int, int, float, float]]:

@@ -46,10 +46,12 @@ def test_binding_constants_match_header():
 def test_struct_layout_matches_binding(tmp_path):
     import paper_2512_21835_amd as P
     structs = [("stage_config", P.StageConfig), ("stage_layer_weights", P.StageLayerWeights),
-               ("stage_plan_input", P.StagePlanInput), ("stage_plan_step", P.StagePlanStep)]
+               ("stage_plan_input", P.StagePlanInput), ("stage_plan_step", P.StagePlanStep),
+               ("stage_alloc_device", P.StageAllocDevice), ("stage_alloc_input", P.StageAllocInput),
+               ("stage_alloc_plan", P.StageAllocPlan)]
     src = tmp_path / "layout.c"
-    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "stage.h"', '#include "stage_planner.h"',
-             'int main(void) {']
+    lines = ['#include <stdio.h>', '#include <stddef.h>'] + [f'#include "{os.path.basename(h)}"' for h in HEADERS]
+    lines += ['int main(void) {']
     want = []
     for cname, py in structs:
         lines.append(f'printf("%zu\\n", sizeof({cname}));')
