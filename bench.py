@@ -386,6 +386,79 @@ def planner_leg(calls: int = 3, ctx: int = 2048, n_steps: int = 6):
     }
 
 
+def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
+    """The KV transfer protocol on one GPU (Alg. 2, pinned host memory as the peer): the
+    8B-shaped stage, all 8 layers resident, 4 micro-batches of batch 1 at context `ctx` (filled
+    through stage_kv_append with random K/V), decoded round robin, one micro-batch per call.
+    Without parking, then with it: before micro-batch m's call the next micro-batch's tail is
+    requested back (stage_kv_unpark, copy stream), and after the call m's last n_park tokens
+    move out (stage_kv_park), for each n_park in `n_parks`.  Reports the call time each way, the
+    bytes each call moves over the host link, and the KV blocks held in HBM after the last call."""
+    import torch
+
+    import synth
+    import paper_2512_21835_amd as P
+
+    shape = synth.LLAMA8B_STAGE
+    dev = torch.device("cuda", 0)
+    cstream = torch.cuda.current_stream(dev)
+    xstream = torch.cuda.Stream(dev)
+    L, n_mb = shape.n_layers, 4
+    gen = torch.Generator(device=dev).manual_seed(2515)
+    weights = []
+    for l in range(L):
+        w = {}
+        for name, shp in synth.layer_weight_shapes(shape).items():
+            t = torch.randn(shp, generator=gen, device=dev) * 0.02 + (1.0 if name in ("g1", "g2") else 0.0)
+            w[name] = t.to(torch.bfloat16).view(torch.int16).contiguous()
+        weights.append(w)
+    kv = [[torch.randn(L, ctx, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
+           .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)] for _ in range(n_mb)]
+    x = torch.randn(n_mb, 1, 1, shape.hidden, generator=gen, device=dev)
+    res = {}
+    for n_park in (0,) + tuple(n_parks):
+        park = n_park > 0
+        cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + rounds + 8, n_resident_max=L,
+                           compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream,
+                           kv_park_tokens=n_park)
+        h = P.stage_init(cfg)
+        try:
+            for l in range(L):
+                P.stage_load_layer(h, l, weights[l], 1)
+            for m in range(n_mb):
+                P.stage_kv_append(h, m, 0, ctx, kv[m][0], kv[m][1])
+            ys = [torch.empty_like(x[m]) for m in range(n_mb)]
+
+            def step(m):
+                if park:
+                    P.stage_kv_unpark(h, [(m + 1) % n_mb])
+                P.stage_decode(h, [m], 1, x[m], ys[m])
+                if park:
+                    P.stage_kv_park(h, [m], n_park)
+
+            for m in range(n_mb):          # warm-up round (the first parks)
+                step(m)
+            P.stage_sync(h)
+            t0 = time.perf_counter()
+            for i in range(rounds * n_mb):
+                step(i % n_mb)
+            P.stage_sync(h)
+            dt = time.perf_counter() - t0
+            st = P.stage_get_stats(h)
+        finally:
+            P.stage_destroy(h)
+        key = f"park_{n_park}" if park else "plain"
+        res[key] = {
+            "ms_per_call": dt * 1e3 / (rounds * n_mb), "kv_blocks_in_hbm": st["kv_blocks"] - st["kv_blocks_free"],
+            "host_link_MB_per_call": (st["bytes_parked"] + st["bytes_unparked"]) / 1e6 / ((rounds + 1) * n_mb)}
+        if park:
+            res[key]["overhead"] = res[key]["ms_per_call"] / res["plain"]["ms_per_call"] - 1
+    res["workload"] = (f"llama8b_stage decode: 8 layers resident, 4 micro-batches of batch 1 at context {ctx}, round "
+                       f"robin one per call; parking moves the last n tokens of each micro-batch between its calls "
+                       f"and fetches the next one's back ahead of its call")
+    return res
+
+
 def allocation_report(resident: dict, offload: dict, device_mem_gb=(32, 24, 20, 16), n_layers: int = 80):
     """The cost model and the allocation scheduler fed with this run's measurements.
 
@@ -425,6 +498,8 @@ def main() -> int:
     ap.add_argument("--prefill", type=int, default=1024)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
+    ap.add_argument("--parking-rounds", type=int, default=32,
+                    help="timed round-robin rounds of the KV parking leg (0 = skip)")
     ap.add_argument("--planner-calls", type=int, default=3,
                     help="timed calls per planner step of the 70B planner leg (0 = skip)")
     ap.add_argument("--resident70b-rounds", type=int, default=8,
@@ -526,6 +601,8 @@ def main() -> int:
     }
     if args.resident70b_rounds > 0:
         out["resident70b"] = resident70b_leg(args.resident70b_rounds)
+    if args.parking_rounds > 0:
+        out["kv_parking"] = parking_leg(args.parking_rounds)
     if args.planner_calls > 0:
         out["planner"] = planner_leg(args.planner_calls)
     if args.offload_calls > 0:

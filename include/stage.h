@@ -121,6 +121,10 @@ typedef struct {
     int32_t plan_mode;
     int32_t plan_alpha[STAGE_MAX_THRESHOLDS];
     int32_t plan_beta[STAGE_MAX_THRESHOLDS];
+    /* Most tokens stage_kv_park moves out per sequence (0 = parking off).  Sizes one pinned host
+       buffer per parked sequence, 2 * n_layers * kv_park_tokens * n_kv_heads * head_dim KV
+       elements, which the parking kernels read and write directly over the host link. */
+    int32_t kv_park_tokens;
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
@@ -185,8 +189,32 @@ int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const voi
 int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void *k, void *v,
                          int32_t drop);
 
-/* Forgets sequence (mb, b): its blocks return to the pool and its length becomes 0. */
+/* Forgets sequence (mb, b): its blocks return to the pool, a parked tail is dropped and its length
+   becomes 0.  Waits for both streams. */
 int stage_reset_sequence(stage *s, int32_t mb, int32_t b);
+
+/* KV transfer protocol, the single-GPU half (Section III-E, Alg. 2: a device ships the tail of a
+   stage's cache away after the stage runs and receives it back before the stage runs again),
+   with pinned host memory as the peer.  Between two calls of a micro-batch its tails need no
+   HBM, so the pool serves more sequences, and the copies overlap other micro-batches' compute.
+
+   stage_kv_park enqueues on the copy stream, after all work enqueued so far on the compute
+   stream, the move of the last min(n_tokens, length) tokens of every sequence of the listed
+   micro-batches into pinned host memory, and returns their emptied blocks to the pool at once
+   (compute-stream work enqueued later waits for these copies before it can write a block).
+   A sequence keeps its length (stage_get_length counts parked tokens); its block table shrinks.
+   The residency schedules count only tokens in HBM.  Returns before the copies run.
+   1 <= n_tokens <= kv_park_tokens.  ESTATE: parking is off, or a listed sequence already has a
+   parked tail; ENOMEM: the pinned buffer cannot be allocated (nothing changes). */
+int stage_kv_park(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t n_tokens);
+
+/* Enqueues on the copy stream the return of the listed micro-batches' parked tails into new
+   blocks (taken lowest id first, sequence by sequence), without waiting for the compute stream,
+   so that it overlaps compute already enqueued (the paper's asynchronous receive of the next
+   stage's cache); the next compute on a returned sequence waits for its copy.  A call, append
+   or export on a parked sequence returns its tail itself first.  Sequences without a parked
+   tail are skipped.  ENOMEM: the pool lacks the blocks (nothing changes). */
+int stage_kv_unpark(stage *s, int32_t n_mb, const int32_t *mb_ids);
 
 /* Waits for the compute and copy streams; reports asynchronous HIP errors. */
 int stage_sync(stage *s);
@@ -198,7 +226,7 @@ int stage_sync(stage *s);
 int stage_get_block_table(stage *s, int32_t mb, int32_t b, int32_t *blocks, int32_t cap,
                           int32_t *n);
 
-/* Current length (tokens stored) of sequence (mb, b). */
+/* Current length of sequence (mb, b): tokens stored, in HBM or parked. */
 int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length);
 
 /* Residency of every layer: a STAGE_RES_* code, -1 if not loaded; out has n_layers entries. */
@@ -230,7 +258,8 @@ int stage_get_timeline(stage *s, float *records, int32_t cap, int32_t *n);
 int stage_set_timing(stage *s, int32_t flags);
 
 /* JSON object with counters: calls, tokens, layer loads, bytes streamed through slots and read in
-   place (zero copy), block sizes, residency counts, HBM bytes in use. */
+   place (zero copy), block sizes, residency counts, HBM bytes in use, parked tokens and bytes
+   moved by parking. */
 int stage_get_stats(stage *s, char *buf, int32_t cap);
 
 /* Message of the last error on this handle ("" if none); valid until the next call. */

@@ -11,6 +11,7 @@ from .stage import (  # noqa: F401
     STAGE_RES_OFFLOADED, STAGE_RES_RESIDENT, STAGE_RES_MHA_OFFLOADED, STAGE_RES_MLP_OFFLOADED,
     stage_config_default, stage_init, stage_destroy, stage_load_layer, stage_prefill, stage_decode,
     stage_kv_append, stage_kv_export_tail, stage_reset_sequence, stage_sync, stage_get_block_table,
+    stage_kv_park, stage_kv_unpark,
     stage_get_length, stage_get_residency, stage_get_slot_log, stage_get_demotion_log,
     stage_get_timeline, stage_set_timing, stage_get_stats, stage_strerror, stage_get_residency_log,
     stage_plan_offload, StagePlanInput, StagePlanStep, stage_allocate, StageAllocDevice, StageAllocInput,

@@ -104,7 +104,57 @@ __global__ __launch_bounds__(256) void kv_copy_kernel(KvCopyArgs a) {
     }
 }
 
+// 16-byte chunks, four in flight per lane, on kParkWorkgroups workgroups: the traffic crosses
+// the host link at a few tens of GB/s, and a full-grid copy would hold every compute unit's
+// memory pipeline behind slow host accesses while decode kernels wait for HBM.
+__global__ __launch_bounds__(256) void kv_park_kernel(KvParkArgs a) {
+    const int row_chunks = a.head_dim * a.elem_bytes / 16;  // one (token, head) vector
+    const size_t per_layer = (size_t)a.n * a.n_kv_heads * row_chunks;
+    const size_t total = 2 * (size_t)a.n_layers * per_layer;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    const size_t head_bytes = (size_t)kBlockTokens * a.head_dim * a.elem_bytes;
+    char *pool = static_cast<char *>(a.pool_base);
+    uint4 *host = static_cast<uint4 *>(a.host);
+    auto pool_chunk = [&](size_t c) -> uint4 * {
+        const int j = (int)(c % row_chunks);
+        size_t r = c / row_chunks;
+        const int g = (int)(r % a.n_kv_heads);
+        r /= a.n_kv_heads;
+        const int t = (int)(r % a.n);
+        r /= a.n;
+        const int layer = (int)(r % a.n_layers);
+        const int kv = (int)(r / a.n_layers);
+        const int pos = a.pos0 + t;
+        const int block = a.block_table[(size_t)a.slot * a.max_blocks + pos / kBlockTokens];
+        const size_t off = (size_t)layer * a.layer_stride + (((size_t)block * 2 + kv) * a.n_kv_heads + g) * head_bytes +
+                           (size_t)(pos % kBlockTokens) * a.head_dim * a.elem_bytes + (size_t)j * 16;
+        return reinterpret_cast<uint4 *>(pool + off);
+    };
+    for (size_t c0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c0 < total; c0 += 4 * stride) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t c = c0 + u * stride;
+            if (c < total) v[u] = a.to_pool ? host[c] : *pool_chunk(c);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t c = c0 + u * stride;
+            if (c < total) {
+                if (a.to_pool) *pool_chunk(c) = v[u];
+                else host[c] = v[u];
+            }
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_kv_park(const KvParkArgs &a, hipStream_t st) {
+    if (a.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(kv_park_kernel, dim3(kParkWorkgroups), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st) {
     if (a.rows <= 0) return hipSuccess;

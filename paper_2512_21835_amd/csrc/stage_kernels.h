@@ -136,4 +136,20 @@ struct KvCopyArgs {
 };
 hipError_t launch_kv_copy(const KvCopyArgs &a, hipStream_t st);
 
+// One sequence's KV tail between the paged pool and a dense [K|V][layer][token][head][d] buffer
+// in pinned host memory, addressed by the device (KV parking).
+struct KvParkArgs {
+    void *pool_base;        // layer 0 pool; layer l at pool_base + l * layer_stride bytes
+    size_t layer_stride;
+    const int *block_table;
+    int max_blocks;
+    int n_kv_heads, head_dim, elem_bytes;
+    int n_layers;
+    int slot, pos0, n;
+    void *host;             // device address of the pinned buffer
+    int to_pool;
+};
+constexpr int kParkWorkgroups = 32;  // few compute units: the host link is the bound
+hipError_t launch_kv_park(const KvParkArgs &a, hipStream_t st);
+
 }  // namespace stg

@@ -30,6 +30,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <memory>
 #include <queue>
 #include <string>
 #include <vector>
@@ -82,6 +83,14 @@ struct TimeRec {
     hipEvent_t a, b;
 };
 
+// An event recorded after one park's copies, shared by the blocks that park freed.
+struct ParkEvent {
+    hipEvent_t e = nullptr;
+    ~ParkEvent() {
+        if (e) (void)hipEventDestroy(e);
+    }
+};
+
 }  // namespace
 
 struct stage {
@@ -127,6 +136,16 @@ struct stage {
     std::vector<TimeRec> recs;
     TimeRec open_rec{0, 0, nullptr, nullptr};  // block-kernel interval being timed
     std::vector<hipEvent_t> ev_pool;
+
+    // KV tails parked between calls (Alg. 2 with pinned host memory as the peer)
+    std::vector<int> parked;            // tokens parked per sequence
+    std::vector<void *> park_host;      // pinned K then V, [L][n][Hkv][d] each, per sequence
+    std::vector<void *> park_host_dev;  // the same buffers as kernels address them
+    std::vector<hipEvent_t> ready_ev;   // the sequence's unpark finished (copy stream)
+    std::vector<char> ready_pending;
+    // per KV block: the event of the park whose copies may still read it, until it is taken again
+    std::vector<std::shared_ptr<ParkEvent>> block_park;
+    long long bytes_parked = 0, bytes_unparked = 0;
 
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
     long long bytes_direct = 0;   // offloaded-block bytes read in place by zero-copy kernels
@@ -429,30 +448,117 @@ int blocks_needed(const stage *s, int slot, int n) {
 }
 
 // Takes blocks (lowest free id first) for the listed sequences in order and mirrors the new
-// table entries on the device.  The caller has checked that the pool suffices.
-int allocate_blocks(stage *s, const std::vector<int> &slots, int n) {
+// table entries on the device, on stream `st` (the compute stream unless given).  The caller has
+// checked that the pool suffices.
+int allocate_blocks(stage *s, const std::vector<int> &slots, int n, hipStream_t st = nullptr) {
     std::vector<int> idx, val;
     for (int slot : slots) {
         const int need = blocks_needed(s, slot, n);
         for (int i = 0; i < need; ++i) {
             const int blk = s->free_blocks.top();
             s->free_blocks.pop();
+            // a park that freed this block may still be copying it out: compute waits for it
+            // (the copy stream runs the park first anyway)
+            if (s->block_park[blk]) {
+                if (!st || st == s->cs) HIP_TRY(hipStreamWaitEvent(s->cs, s->block_park[blk]->e, 0));
+                s->block_park[blk].reset();
+            }
             idx.push_back(slot * s->max_blocks + (int)s->tables[slot].size());
             val.push_back(blk);
             s->tables[slot].push_back(blk);
         }
     }
-    if (!idx.empty()) HIP_TRY(launch_table_write(s->d_table, idx.data(), val.data(), (int)idx.size(), s->cs));
+    if (!idx.empty())
+        HIP_TRY(launch_table_write(s->d_table, idx.data(), val.data(), (int)idx.size(), st ? st : s->cs));
     return STAGE_OK;
 }
 
-void release_tail_blocks(stage *s, int slot) {
+void release_tail_blocks(stage *s, int slot, const std::shared_ptr<ParkEvent> &park = nullptr) {
     const int keep = (s->lengths[slot] + kBlockTokens - 1) / kBlockTokens;
     std::vector<int> &t = s->tables[slot];
     while ((int)t.size() > keep) {
         s->free_blocks.push(t.back());
+        if (park) s->block_park[t.back()] = park;
         t.pop_back();
     }
+}
+
+// K (or V) bytes of n tokens over all layers, dense [L][n][Hkv][d].
+size_t tail_bytes(const stage *s, int n) {
+    return (size_t)s->L * n * s->Hkv * s->D * (s->cfg.kv_fp32 ? 4 : 2);
+}
+
+KvParkArgs kv_park_args(const stage *s, int slot, int pos0, int n, bool to_pool) {
+    KvParkArgs a{};
+    a.pool_base = s->kv_pool;
+    a.layer_stride = s->kv_layer_stride;
+    a.block_table = s->d_table;
+    a.max_blocks = s->max_blocks;
+    a.n_kv_heads = s->Hkv;
+    a.head_dim = s->D;
+    a.elem_bytes = s->cfg.kv_fp32 ? 4 : 2;
+    a.n_layers = s->L;
+    a.slot = slot;
+    a.pos0 = pos0;
+    a.n = n;
+    a.host = s->park_host_dev[slot];
+    a.to_pool = to_pool;
+    return a;
+}
+
+KvCopyArgs kv_copy_args(const stage *s, int slot, int pos0, int n, void *dense, bool to_pool) {
+    KvCopyArgs a{};
+    a.pool_base = s->kv_pool;
+    a.layer_stride = s->kv_layer_stride;
+    a.block_table = s->d_table;
+    a.max_blocks = s->max_blocks;
+    a.n_kv_heads = s->Hkv;
+    a.head_dim = s->D;
+    a.kv_fp32 = s->cfg.kv_fp32;
+    a.n_layers = s->L;
+    a.slot = slot;
+    a.pos0 = pos0;
+    a.n = n;
+    a.to_pool = to_pool;
+    a.k = dense;
+    a.v = static_cast<char *>(dense) + tail_bytes(s, n);
+    return a;
+}
+
+// Copy stream: the parked tail of `slot` returns into new blocks (taken like a call's); its ready
+// event is what the sequence's next compute waits on.  The caller has checked the pool.  Blocks
+// in the pool are never still read by the compute stream (calls only free blocks through a park,
+// whose copies this stream runs first, or synchronously), so nothing here waits for compute.
+int enqueue_unpark(stage *s, int slot) {
+    const int n = s->parked[slot];
+    int rc = allocate_blocks(s, {slot}, n, s->xs);
+    if (rc) return rc;
+    HIP_TRY(launch_kv_park(kv_park_args(s, slot, s->lengths[slot], n, true), s->xs));
+    if (!s->ready_ev[slot] && hipEventCreateWithFlags(&s->ready_ev[slot], hipEventDisableTiming) != hipSuccess)
+        return s->fail(STAGE_EHIP, "hipEventCreate failed");
+    HIP_TRY(hipEventRecord(s->ready_ev[slot], s->xs));
+    s->ready_pending[slot] = 1;
+    s->lengths[slot] += n;
+    s->parked[slot] = 0;
+    s->bytes_unparked += (long long)(2 * tail_bytes(s, n));
+    return STAGE_OK;
+}
+
+// Before compute-stream work on the listed sequences: their parked tails come back, and the
+// compute stream waits for their copies.  (Blocks the work takes from the pool carry their own
+// wait, in allocate_blocks.)
+int prepare_sequences(stage *s, const std::vector<int> &slots) {
+    for (int sl : slots)
+        if (s->parked[sl] > 0) {
+            int rc = enqueue_unpark(s, sl);
+            if (rc) return rc;
+        }
+    for (int sl : slots)
+        if (s->ready_pending[sl]) {
+            HIP_TRY(hipStreamWaitEvent(s->cs, s->ready_ev[sl], 0));
+            s->ready_pending[sl] = 0;
+        }
+    return STAGE_OK;
 }
 
 int record_event(stage *s, hipStream_t st, hipEvent_t *out) {
@@ -753,12 +859,13 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
     for (int len : s->lengths) longest = std::max(longest, len);
     int need_blocks = 0;
     for (int sl : slots) {
-        if (decode && s->lengths[sl] < 1)
+        const int len = s->lengths[sl] + s->parked[sl];  // a parked tail comes back first
+        if (decode && len < 1)
             return s->fail(STAGE_ESTATE, "decode on an empty sequence (slot %d)", sl);
-        if (s->lengths[sl] + T > c.max_context)
+        if (len + T > c.max_context)
             return s->fail(STAGE_ERANGE, "sequence would exceed max_context %d", c.max_context);
-        need_blocks += blocks_needed(s, sl, T);
-        longest = std::max(longest, s->lengths[sl] + T);
+        need_blocks += blocks_needed(s, sl, s->parked[sl] + T);
+        longest = std::max(longest, len + T);
     }
     if (need_blocks > (int)s->free_blocks.size())
         return s->fail(STAGE_ENOMEM, "KV pool exhausted (%d blocks needed, %d free)", need_blocks,
@@ -780,6 +887,9 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
             if (rc) return rc;
         }
     }
+
+    rc = prepare_sequences(s, slots);
+    if (rc) return rc;
 
     const long long call_no = s->calls;
     if (c.plan_mode) {
@@ -930,7 +1040,8 @@ int stage_init(const stage_config *cfg, stage **out) {
                         (c.kv_fp32 == 0 || c.kv_fp32 == 1) && c.n_resident_max >= 0 &&
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
-                        (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1);
+                        (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1) &&
+                        c.kv_park_tokens >= 0 && c.kv_park_tokens <= c.max_context;
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     if (c.plan_mode != 0 && c.plan_mode != 1) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i) {
@@ -974,6 +1085,11 @@ int stage_init(const stage_config *cfg, stage **out) {
     s->max_splits = (c.max_context + kDecodeSplitKeys - 1) / kDecodeSplitKeys;
     s->tables.assign(s->n_seq_slots, {});
     s->lengths.assign(s->n_seq_slots, 0);
+    s->parked.assign(s->n_seq_slots, 0);
+    s->park_host.assign(s->n_seq_slots, nullptr);
+    s->park_host_dev.assign(s->n_seq_slots, nullptr);
+    s->ready_ev.assign(s->n_seq_slots, nullptr);
+    s->ready_pending.assign(s->n_seq_slots, 0);
     for (int b = 0; b < s->n_blocks; ++b) s->free_blocks.push(b);
 
     auto cleanup = [&](int code) {
@@ -995,6 +1111,7 @@ int stage_init(const stage_config *cfg, stage **out) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);
     }
+    s->block_park.assign(s->n_blocks, nullptr);
     if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
         return cleanup(STAGE_EHIP);
     // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
@@ -1029,6 +1146,11 @@ int stage_destroy(stage *s) {
         if (r.b) (void)hipEventDestroy(r.b);
     }
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+    for (hipEvent_t e : s->ready_ev)
+        if (e) (void)hipEventDestroy(e);
+    s->block_park.clear();
+    for (void *p : s->park_host)
+        if (p) (void)hipHostFree(p);
     for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_hi, (void *)s->ws_lo,
@@ -1110,9 +1232,9 @@ int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const voi
     if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch || n_tokens < 1 || !k || !v)
         return s->fail(STAGE_EINVAL, "bad kv_append arguments");
     const int slot = seq_slot(s, mb, b);
-    if (s->lengths[slot] + n_tokens > s->cfg.max_context)
+    if (s->lengths[slot] + s->parked[slot] + n_tokens > s->cfg.max_context)
         return s->fail(STAGE_ERANGE, "sequence would exceed max_context");
-    if (blocks_needed(s, slot, n_tokens) > (int)s->free_blocks.size())
+    if (blocks_needed(s, slot, s->parked[slot] + n_tokens) > (int)s->free_blocks.size())
         return s->fail(STAGE_ENOMEM, "KV pool exhausted");
     DeviceGuard dg(s->cfg.device);
     const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
@@ -1122,27 +1244,15 @@ int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const voi
         int rc = ensure_dense(s, 2 * bytes);
         if (rc) return rc;
     }
-    int rc = allocate_blocks(s, {slot}, n_tokens);
+    int rc = prepare_sequences(s, {slot});
     if (rc) return rc;
-    KvCopyArgs a{};
-    a.pool_base = s->kv_pool;
-    a.layer_stride = s->kv_layer_stride;
-    a.block_table = s->d_table;
-    a.max_blocks = s->max_blocks;
-    a.n_kv_heads = s->Hkv;
-    a.head_dim = s->D;
-    a.kv_fp32 = s->cfg.kv_fp32;
-    a.n_layers = s->L;
-    a.slot = slot;
-    a.pos0 = s->lengths[slot];
-    a.n = n_tokens;
-    a.to_pool = 1;
+    rc = allocate_blocks(s, {slot}, n_tokens);
+    if (rc) return rc;
+    KvCopyArgs a = kv_copy_args(s, slot, s->lengths[slot], n_tokens, s->ws_dense, true);
     if (dev) {
         a.k = const_cast<void *>(k);
         a.v = const_cast<void *>(v);
     } else {
-        a.k = s->ws_dense;
-        a.v = static_cast<char *>(s->ws_dense) + bytes;
         HIP_TRY(hipMemcpyAsync(a.k, k, bytes, hipMemcpyHostToDevice, s->cs));
         HIP_TRY(hipMemcpyAsync(a.v, v, bytes, hipMemcpyHostToDevice, s->cs));
     }
@@ -1158,8 +1268,10 @@ int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void
     if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch || n_tokens < 1 || !k || !v)
         return s->fail(STAGE_EINVAL, "bad kv_export_tail arguments");
     const int slot = seq_slot(s, mb, b);
-    if (n_tokens > s->lengths[slot])
-        return s->fail(STAGE_ESTATE, "sequence holds %d tokens, %d requested", s->lengths[slot], n_tokens);
+    const int len = s->lengths[slot] + s->parked[slot];
+    if (n_tokens > len) return s->fail(STAGE_ESTATE, "sequence holds %d tokens, %d requested", len, n_tokens);
+    if (blocks_needed(s, slot, s->parked[slot]) > (int)s->free_blocks.size())
+        return s->fail(STAGE_ENOMEM, "KV pool exhausted");
     DeviceGuard dg(s->cfg.device);
     const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
     const size_t bytes = (size_t)s->L * n_tokens * s->Hkv * s->D * elem;
@@ -1168,21 +1280,13 @@ int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void
         int rc = ensure_dense(s, 2 * bytes);
         if (rc) return rc;
     }
-    KvCopyArgs a{};
-    a.pool_base = s->kv_pool;
-    a.layer_stride = s->kv_layer_stride;
-    a.block_table = s->d_table;
-    a.max_blocks = s->max_blocks;
-    a.n_kv_heads = s->Hkv;
-    a.head_dim = s->D;
-    a.kv_fp32 = s->cfg.kv_fp32;
-    a.n_layers = s->L;
-    a.slot = slot;
-    a.pos0 = s->lengths[slot] - n_tokens;
-    a.n = n_tokens;
-    a.to_pool = 0;
-    a.k = dev ? k : s->ws_dense;
-    a.v = dev ? v : static_cast<char *>(s->ws_dense) + bytes;
+    int rc = prepare_sequences(s, {slot});
+    if (rc) return rc;
+    KvCopyArgs a = kv_copy_args(s, slot, s->lengths[slot] - n_tokens, n_tokens, s->ws_dense, false);
+    if (dev) {
+        a.k = k;
+        a.v = v;
+    }
     HIP_TRY(launch_kv_copy(a, s->cs));
     if (!dev) {
         HIP_TRY(hipMemcpyAsync(k, a.k, bytes, hipMemcpyDeviceToHost, s->cs));
@@ -1202,8 +1306,106 @@ int stage_reset_sequence(stage *s, int32_t mb, int32_t b) {
     if (mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch)
         return s->fail(STAGE_EINVAL, "bad sequence (%d, %d)", mb, b);
     const int slot = seq_slot(s, mb, b);
+    DeviceGuard dg(s->cfg.device);
+    int rc = sync_all(s);  // freed blocks may be written by the copy stream without waiting for compute
+    if (rc) return rc;
     s->lengths[slot] = 0;
+    s->parked[slot] = 0;
+    s->ready_pending[slot] = 0;
     release_tail_blocks(s, slot);
+    return STAGE_OK;
+}
+
+int stage_kv_park(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t n_tokens) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    const stage_config &c = s->cfg;
+    if (c.kv_park_tokens < 1) return s->fail(STAGE_ESTATE, "parking needs kv_park_tokens > 0");
+    if (n_mb < 1 || n_mb > c.max_microbatches || !mb_ids || n_tokens < 1 || n_tokens > c.kv_park_tokens)
+        return s->fail(STAGE_EINVAL, "bad kv_park arguments (n_mb=%d n_tokens=%d)", n_mb, n_tokens);
+    std::vector<int> slots;
+    std::vector<char> seen(c.max_microbatches, 0);
+    for (int k = 0; k < n_mb; ++k) {
+        const int mb = mb_ids[k];
+        if (mb < 0 || mb >= c.max_microbatches || seen[mb])
+            return s->fail(STAGE_EINVAL, "micro-batch id %d out of range or repeated", mb);
+        seen[mb] = 1;
+        for (int b = 0; b < c.max_batch; ++b) {
+            const int sl = seq_slot(s, mb, b);
+            if (s->parked[sl] > 0) return s->fail(STAGE_ESTATE, "sequence (%d, %d) is already parked", mb, b);
+            if (s->lengths[sl] > 0) slots.push_back(sl);
+        }
+    }
+    DeviceGuard dg(c.device);
+    for (int sl : slots) {
+        if (s->park_host[sl]) continue;
+        void *hbuf = nullptr, *dbuf = nullptr;
+        if (hipHostMalloc(&hbuf, 2 * tail_bytes(s, c.kv_park_tokens), hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "pinned parking buffer of %zu bytes", 2 * tail_bytes(s, c.kv_park_tokens));
+        }
+        hipError_t e = hipHostGetDevicePointer(&dbuf, hbuf, 0);
+        if (e != hipSuccess) {
+            (void)hipHostFree(hbuf);
+            return s->fail_hip(e, "hipHostGetDevicePointer");
+        }
+        s->park_host[sl] = hbuf;
+        s->park_host_dev[sl] = dbuf;
+    }
+    if (slots.empty()) return STAGE_OK;
+    auto done = std::make_shared<ParkEvent>();
+    if (hipEventCreateWithFlags(&done->e, hipEventDisableTiming) != hipSuccess) {
+        done->e = nullptr;
+        return s->fail(STAGE_EHIP, "hipEventCreate failed");
+    }
+    hipEvent_t after = nullptr;
+    int rc = record_event(s, s->cs, &after);  // the copies follow everything enqueued for compute
+    if (rc) return rc;
+    HIP_TRY(hipStreamWaitEvent(s->xs, after, 0));
+    s->ev_pool.push_back(after);
+    for (int sl : slots) {
+        const int n = std::min(n_tokens, s->lengths[sl]);
+        HIP_TRY(launch_kv_park(kv_park_args(s, sl, s->lengths[sl] - n, n, false), s->xs));
+    }
+    HIP_TRY(hipEventRecord(done->e, s->xs));
+    for (int sl : slots) {
+        const int n = std::min(n_tokens, s->lengths[sl]);
+        s->lengths[sl] -= n;
+        s->parked[sl] = n;
+        release_tail_blocks(s, sl, done);
+        s->bytes_parked += (long long)(2 * tail_bytes(s, n));
+    }
+    return STAGE_OK;
+}
+
+int stage_kv_unpark(stage *s, int32_t n_mb, const int32_t *mb_ids) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    const stage_config &c = s->cfg;
+    if (n_mb < 1 || n_mb > c.max_microbatches || !mb_ids) return s->fail(STAGE_EINVAL, "bad kv_unpark arguments");
+    std::vector<int> slots;
+    std::vector<char> seen(c.max_microbatches, 0);
+    int need = 0;
+    for (int k = 0; k < n_mb; ++k) {
+        const int mb = mb_ids[k];
+        if (mb < 0 || mb >= c.max_microbatches || seen[mb])
+            return s->fail(STAGE_EINVAL, "micro-batch id %d out of range or repeated", mb);
+        seen[mb] = 1;
+        for (int b = 0; b < c.max_batch; ++b) {
+            const int sl = seq_slot(s, mb, b);
+            if (s->parked[sl] > 0) {
+                slots.push_back(sl);
+                need += blocks_needed(s, sl, s->parked[sl]);
+            }
+        }
+    }
+    if (need > (int)s->free_blocks.size())
+        return s->fail(STAGE_ENOMEM, "KV pool exhausted (%d blocks needed, %d free)", need, (int)s->free_blocks.size());
+    DeviceGuard dg(c.device);
+    for (int sl : slots) {
+        int rc = enqueue_unpark(s, sl);
+        if (rc) return rc;
+    }
     return STAGE_OK;
 }
 
@@ -1229,7 +1431,7 @@ int stage_get_block_table(stage *s, int32_t mb, int32_t b, int32_t *blocks, int3
 int stage_get_length(stage *s, int32_t mb, int32_t b, int32_t *length) {
     if (!s || !length || mb < 0 || mb >= s->cfg.max_microbatches || b < 0 || b >= s->cfg.max_batch)
         return STAGE_EINVAL;
-    *length = s->lengths[seq_slot(s, mb, b)];
+    *length = s->lengths[seq_slot(s, mb, b)] + s->parked[seq_slot(s, mb, b)];
     return STAGE_OK;
 }
 
@@ -1301,6 +1503,8 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
     if (!s || !buf || cap < 1) return STAGE_EINVAL;
     int res = 0, streamed = 0, off_mha = 0, off_mlp = 0;
     size_t host_w = 0;
+    long long parked = 0;
+    for (int p : s->parked) parked += p;
     for (const Layer &l : s->layers) {
         if (!l.loaded) continue;
         for (int b = 0; b < 2; ++b) host_w += l.blk[b].host ? s->blk_bytes[b] : 0;
@@ -1317,10 +1521,12 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
         "\"mlp_block_bytes\": %zu, \"resident_layers\": %d, \"streamed_layers\": %d, "
         "\"offloaded_mha_blocks\": %d, \"offloaded_mlp_blocks\": %d, "
         "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"host_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, "
-        "\"kv_blocks\": %d, \"kv_blocks_free\": %d}",
+        "\"kv_blocks\": %d, \"kv_blocks_free\": %d, \"parked_tokens\": %lld, \"bytes_parked\": %lld, "
+        "\"bytes_unparked\": %lld}",
         s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes,
         s->blk_bytes[kMha], s->blk_bytes[kMlp], res, streamed, off_mha, off_mlp,
-        s->slots.size(), hbm_w, host_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size());
+        s->slots.size(), hbm_w, host_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size(),
+        parked, s->bytes_parked, s->bytes_unparked);
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }
 

@@ -35,7 +35,7 @@ EXPORTED = (
     "stage_decode", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
     "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
-    "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate",
+    "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate", "stage_kv_park", "stage_kv_unpark",
 )
 STAGE_ALLOC_MAX_DEVICES = 64
 STAGE_ALLOC_MAX_LAYERS = 4096
@@ -53,7 +53,7 @@ class StageConfig(ctypes.Structure):
         ("device", c_int32), ("compute_stream", c_void_p), ("copy_stream", c_void_p),
         ("timing", c_int32), ("zero_copy", c_int32),
         ("plan_mode", c_int32), ("plan_alpha", c_int32 * STAGE_MAX_THRESHOLDS),
-        ("plan_beta", c_int32 * STAGE_MAX_THRESHOLDS),
+        ("plan_beta", c_int32 * STAGE_MAX_THRESHOLDS), ("kv_park_tokens", c_int32),
     ]
 
 
@@ -118,6 +118,8 @@ def lib():
         "stage_kv_append": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_export_tail": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_int32]),
         "stage_reset_sequence": (c_int32, [c_void_p, c_int32, c_int32]),
+        "stage_kv_park": (c_int32, [c_void_p, c_int32, ip, c_int32]),
+        "stage_kv_unpark": (c_int32, [c_void_p, c_int32, ip]),
         "stage_sync": (c_int32, [c_void_p]),
         "stage_get_block_table": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, ip]),
         "stage_get_length": (c_int32, [c_void_p, c_int32, c_int32, ip]),
@@ -216,6 +218,14 @@ def stage_reset_sequence(h, mb: int, b: int) -> None:
     _check(lib().stage_reset_sequence(h, mb, b), h)
 
 
+def stage_kv_park(h, mb_ids: Sequence[int], n_tokens: int) -> None:
+    _check(lib().stage_kv_park(h, len(mb_ids), _ids(mb_ids), n_tokens), h)
+
+
+def stage_kv_unpark(h, mb_ids: Sequence[int]) -> None:
+    _check(lib().stage_kv_unpark(h, len(mb_ids), _ids(mb_ids)), h)
+
+
 def stage_sync(h) -> None:
     _check(lib().stage_sync(h), h)
 
@@ -312,7 +322,7 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
                n_stream_slots: int = 2, kv_fp32: bool = False, thresholds: Sequence[int] = (),
                kv_pool_blocks: int = 0, device: int = 0, compute_stream=None, copy_stream=None,
                timing: int = 0, zero_copy: bool = False,
-               plan: Optional[Sequence[Tuple[int, int, int]]] = None) -> StageConfig:
+               plan: Optional[Sequence[Tuple[int, int, int]]] = None, kv_park_tokens: int = 0) -> StageConfig:
     """A StageConfig for a stage shape (any object with the StageShape fields).  ``plan``:
     planner steps [(tokens, alpha, beta)] (plan_mode 1), instead of ``thresholds``."""
     cfg = stage_config_default()
@@ -341,4 +351,5 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
     cfg.copy_stream = copy_stream
     cfg.timing = timing
     cfg.zero_copy = int(bool(zero_copy))
+    cfg.kv_park_tokens = kv_park_tokens
     return cfg

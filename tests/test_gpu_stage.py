@@ -439,6 +439,143 @@ def test_zero_copy_decode_only_stage_needs_no_slots():
         cs.__exit__(None, None, None)
 
 
+def _parking_run(park: bool, pool_blocks: int, rounds: int = 6, n_park: int = 32):
+    """Three micro-batches of two sequences (tiny shape): prefill 37 each, then decode rounds
+    one micro-batch per call.  With `park`, each call is followed by parking the micro-batch's
+    tails (Alg. 2) and by the prefetch of the next micro-batch's tails; the same steps drive the
+    oracle's block allocator."""
+    import torch
+    import paper_2512_21835_amd as P
+    from oracle.policies import BlockAllocator
+    shape, wl = synth.TINY, TINY_RAGGED
+    w = weights_of(shape)
+    cs = compute_stream().__enter__()
+    cfg = P.config_for(shape, max_microbatches=3, max_batch=2, max_context=64, n_resident_max=2,
+                       kv_pool_blocks=pool_blocks, compute_stream=cs.handle, kv_park_tokens=n_park if park else 0)
+    h = P.stage_init(cfg)
+    alloc = BlockAllocator(pool_blocks, 16)
+    parked = {}
+
+    def model_call(m, n):
+        keys = [(m, b) for b in range(2)]
+        for k in keys:                       # a parked tail comes back first
+            if parked.get(k):
+                alloc.call([(k, parked.pop(k))])
+        alloc.call([(k, n) for k in keys])
+
+    def model_park(m):
+        for b in range(2):
+            k = (m, b)
+            n = min(n_park, alloc.lengths[k])
+            alloc.truncate(k, n)
+            parked[k] = n
+
+    def model_unpark(m):
+        for b in range(2):
+            if parked.get((m, b)):
+                alloc.call([((m, b), parked.pop((m, b)))])
+
+    outs = []
+    try:
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 1)
+        plan = [("prefill", m, -1) for m in range(3)] + [("decode", m, t) for t in range(rounds) for m in range(3)]
+        for kind, m, t in plan:
+            if kind == "prefill":
+                x = np.stack([synth.prefill_inputs(wl, m, b, 37) for b in range(2)])[None]
+                xi = torch.from_numpy(x).cuda()
+                y = torch.empty_like(xi)
+                P.stage_prefill(h, [m], 2, 37, xi, y)
+                model_call(m, 37)
+            else:
+                x = np.stack([synth.decode_input(wl, m, b, t) for b in range(2)])[None]
+                xi = torch.from_numpy(x).cuda()
+                y = torch.empty_like(xi)
+                P.stage_decode(h, [m], 2, xi, y)
+                model_call(m, 1)
+            outs.append(y)
+            if park:
+                P.stage_kv_park(h, [m], n_park)
+                model_park(m)
+                if kind == "decode":
+                    P.stage_kv_unpark(h, [(m + 1) % 3])     # prefetch the next micro-batch's tails
+                    model_unpark((m + 1) % 3)
+        P.stage_sync(h)
+        tables = {(m, b): P.stage_get_block_table(h, m, b) for m in range(3) for b in range(2)}
+        lengths = {(m, b): P.stage_get_length(h, m, b) for m in range(3) for b in range(2)}
+        st = P.stage_get_stats(h)
+        return [o.cpu().numpy() for o in outs], tables, lengths, st, alloc, parked
+    finally:
+        P.stage_destroy(h)
+        cs.__exit__(None, None, None)
+
+
+def test_kv_parking_is_lossless_and_fits_a_smaller_pool():
+    """Alg. 2 on one GPU: tails parked in host memory between a micro-batch's calls and fetched
+    back ahead of its next call leave every output bit unchanged, let 12 KV blocks serve six
+    sequences that need 18 without parking, and take blocks exactly as the oracle's allocator
+    does."""
+    _gpu()
+    import paper_2512_21835_amd as P
+    ref, _, ref_len, _, _, _ = _parking_run(False, 18)
+    got, tables, lengths, st, alloc, parked = _parking_run(True, 12)
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+    assert lengths == ref_len
+    for k, t in tables.items():
+        assert t == alloc.table(k), k
+    assert st["parked_tokens"] == sum(parked.values()) > 0
+    assert st["bytes_parked"] > 0 and st["bytes_unparked"] > 0
+    with pytest.raises(P.StageError) as e:
+        _parking_run(False, 12)
+    assert e.value.code == P.STAGE_ENOMEM
+
+
+def test_kv_parking_errors_and_automatic_return():
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    shape, wl = synth.TINY, TINY_RAGGED
+    w = weights_of(shape)
+    cs = compute_stream().__enter__()
+    cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=64, n_resident_max=2,
+                       compute_stream=cs.handle, kv_park_tokens=16)
+    h = P.stage_init(cfg)
+    try:
+        for l in range(2):
+            P.stage_load_layer(h, l, w(l), 1)
+        x = torch.from_numpy(synth.prefill_inputs(wl, 0, 0, 37)[None, None]).cuda()
+        P.stage_prefill(h, [0], 1, 37, x, torch.empty_like(x))
+        with pytest.raises(P.StageError) as e:
+            P.stage_kv_park(h, [0], 17)                     # beyond kv_park_tokens
+        assert e.value.code == P.STAGE_EINVAL
+        k_ref = np.zeros((2, 37, 2, 64), np.uint16)
+        v_ref = np.zeros_like(k_ref)
+        P.stage_kv_export_tail(h, 0, 0, 37, k_ref, v_ref, False)
+        P.stage_kv_park(h, [0, 1], 16)                      # micro-batch 1 is empty: skipped
+        with pytest.raises(P.StageError) as e:
+            P.stage_kv_park(h, [0], 4)                      # already parked
+        assert e.value.code == P.STAGE_ESTATE
+        assert P.stage_get_length(h, 0, 0) == 37 and len(P.stage_get_block_table(h, 0, 0)) == 2
+        k = np.zeros_like(k_ref)
+        v = np.zeros_like(v_ref)
+        P.stage_kv_export_tail(h, 0, 0, 37, k, v, False)    # brings the tail back first
+        assert np.array_equal(k, k_ref) and np.array_equal(v, v_ref)
+        assert P.stage_get_stats(h)["parked_tokens"] == 0
+    finally:
+        P.stage_destroy(h)
+    cfg = P.config_for(shape, max_microbatches=1, max_batch=1, max_context=64, n_resident_max=2,
+                       compute_stream=cs.handle)
+    h = P.stage_init(cfg)
+    try:
+        with pytest.raises(P.StageError) as e:
+            P.stage_kv_park(h, [0], 4)                      # parking off
+        assert e.value.code == P.STAGE_ESTATE
+    finally:
+        P.stage_destroy(h)
+        cs.__exit__(None, None, None)
+
+
 def test_error_paths_leave_stage_usable():
     _gpu()
     import torch
