@@ -32,8 +32,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, published
 # script (FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by what the counter reads for a
 # plain 1 GiB device copy in the same run).  Valid for the GEMV source it was taken on: with any
 # other source the field is reported as null.
-GATEUP_TRAFFIC = {"bytes": 235248073,
-                  "source_sha256": "2466b8caf4e484e9f91697444bb5528b1958c46ff0737afc7bf9a62e7efe29e4"}
+GATEUP_TRAFFIC = {"bytes": 235248047,
+                  "source_sha256": "214ec0b2e8d8bc234056d01c4e30847ff0e3886cda0a4e6b3d059cf293a0e1e4"}
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
 
@@ -386,6 +386,81 @@ def planner_leg(calls: int = 3, ctx: int = 2048, n_steps: int = 6):
     }
 
 
+def kvpressure_leg(contexts=(512, 4352, 8192), rounds: int = 2):
+    """The KV-pressure workload on the 70B-shaped stage: 8 micro-batches of batch 2, decoded round
+    robin one micro-batch per call, residency shrinking 16 -> 8 under the threshold schedule
+    TS_j = 512 + 960 j (one more layer streamed through 2 slots per threshold passed).  Sampled:
+    at each context in `contexts` the caches are filled to it through stage_kv_append (random
+    K/V), then `rounds` decode rounds are timed (one warm-up round first).  Reports the round
+    time, tokens/s, the resident layers, and the HBM fraction (weights of resident layers, slots
+    read once per call, KV read) when no layer streams."""
+    import torch
+
+    import synth
+    import paper_2512_21835_amd as P
+
+    wl = synth.WORKLOADS["llama70b_kvpressure"]
+    shape = wl.shape
+    dev = torch.device("cuda", 0)
+    cstream = torch.cuda.current_stream(dev)
+    xstream = torch.cuda.Stream(dev)
+    L, n_mb, B = shape.n_layers, wl.n_mb, wl.batch
+    gen = torch.Generator(device=dev).manual_seed(2516)
+    x = torch.randn(n_mb, B, shape.hidden, generator=gen, device=dev)
+    ys = [torch.empty_like(x[m:m + 1]) for m in range(n_mb)]
+    out = []
+    layer = shape.layer_bytes()
+    for ctx in contexts:
+        cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=B, max_context=ctx + rounds + 4, n_resident_max=L,
+                           n_stream_slots=2, thresholds=wl.thresholds, compute_stream=cstream.cuda_stream,
+                           copy_stream=xstream.cuda_stream)
+        h = P.stage_init(cfg)
+        try:
+            for l in range(L):
+                w = {}
+                for name, shp in synth.layer_weight_shapes(shape).items():
+                    t = torch.randn(shp, generator=gen, device=dev) * 0.02 + (1.0 if name in ("g1", "g2") else 0.0)
+                    w[name] = t.to(torch.bfloat16).view(torch.int16).contiguous()
+                P.stage_load_layer(h, l, w, 1)
+                del w
+            for m in range(n_mb):
+                for b in range(B):
+                    kv = [torch.randn(L, ctx - 1, shape.n_kv_heads, shape.head_dim, generator=gen, device=dev)
+                          .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)]
+                    P.stage_kv_append(h, m, b, ctx - 1, kv[0], kv[1])
+                    del kv
+
+            def round_():
+                for m in range(n_mb):
+                    P.stage_decode(h, [m], B, x[m:m + 1], ys[m])
+
+            round_()                                  # warm-up; applies the thresholds passed
+            P.stage_sync(h)
+            t0 = time.perf_counter()
+            for _ in range(rounds):
+                round_()
+            P.stage_sync(h)
+            dt = (time.perf_counter() - t0) / rounds
+            res = P.stage_get_residency(h, L)
+        finally:
+            P.stage_destroy(h)
+        resident = sum(1 for c in res if c == 1)
+        kv_read = n_mb * B * L * (ctx + rounds) * 2 * shape.kv_dim * 2
+        hbm = n_mb * L * layer + kv_read             # every call reads every layer once (slot or HBM)
+        entry = {"context": ctx, "resident_layers": resident, "ms_per_round": dt * 1e3,
+                 "tokens_per_s": n_mb * B / dt}
+        if resident == L:
+            entry["hbm_GBs"] = hbm / dt / 1e9
+            entry["hbm_frac"] = hbm / dt / 1e9 / HBM_PEAK_GBS
+        else:
+            entry["streamed_GB_per_round"] = n_mb * (L - resident) * layer / 1e9
+        out.append(entry)
+    return {"workload": "llama70b_kvpressure decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 8 micro-batches "
+                        "of batch 2 round robin, residency 16 -> 8 by thresholds 512 + 960 j, 2 slots; sampled "
+                        "at the listed contexts",
+            "samples": out}
+
+
 def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
     """The KV transfer protocol on one GPU (Alg. 2, pinned host memory as the peer): the
     8B-shaped stage, all 8 layers resident, 4 micro-batches of batch 1 at context `ctx` (filled
@@ -498,6 +573,8 @@ def main() -> int:
     ap.add_argument("--prefill", type=int, default=1024)
     ap.add_argument("--cpu-tokens", type=int, default=4, help="oracle decode tokens for cpu_baseline (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
+    ap.add_argument("--kvpressure-rounds", type=int, default=2,
+                    help="timed rounds per sampled context of the 70B KV-pressure leg (0 = skip)")
     ap.add_argument("--parking-rounds", type=int, default=32,
                     help="timed round-robin rounds of the KV parking leg (0 = skip)")
     ap.add_argument("--planner-calls", type=int, default=3,
@@ -601,6 +678,8 @@ def main() -> int:
     }
     if args.resident70b_rounds > 0:
         out["resident70b"] = resident70b_leg(args.resident70b_rounds)
+    if args.kvpressure_rounds > 0:
+        out["kvpressure70b"] = kvpressure_leg(rounds=args.kvpressure_rounds)
     if args.parking_rounds > 0:
         out["kv_parking"] = parking_leg(args.parking_rounds)
     if args.planner_calls > 0:
