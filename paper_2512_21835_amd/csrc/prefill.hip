@@ -3,13 +3,15 @@
 // lo = bf16(A - hi); the pair keeps ~16 bits of A's mantissa, a single bf16 only 8).  Each 16-wide
 // k step issues v_mfma_f32_32x32x16_bf16 twice per output block, hi then lo, accumulating in fp32.
 //
-// Tiling: a workgroup (4 wavefronts) computes a 128 x 128 tile of C; each wavefront a 64 x 64
-// sub-tile as 2 x 2 blocks of 32 x 32.  K advances 32 at a time.  gemm_dma_kernel (K a multiple
-// of 32) copies tiles global -> LDS directly into a ring of three stages, two tiles ahead;
-// gemm_kernel (any K) stages them through registers into two LDS stages, one tile ahead.  Tiles are stored in LDS in MFMA fragment order (lane l of a fragment at offset
-// 16 l), so every fragment read is one conflict-free ds_read_b128 per lane.  Workgroups that share
-// a weight tile are adjacent in launch order (x over M tiles), so each weight tile is read from HBM
-// once and re-served from L2.
+// Tiling: a workgroup (4 wavefronts) computes a 128 x 128 tile of C, each wavefront a 64 x 64
+// sub-tile as 2 x 2 blocks of 32 x 32; or, when the grid of 256 x 256 tiles still has a workgroup
+// for every compute unit, a 256 x 256 tile with 4 x 4 blocks per wavefront.  K advances 32 at a
+// time.  gemm_dma_kernel (K a multiple of 32) copies tiles global -> LDS directly into a ring of
+// three stages, two tiles ahead; gemm_kernel (any K) stages them through registers into two LDS
+// stages, one tile ahead.  Tiles are stored in LDS in MFMA fragment order (lane l of a fragment at
+// offset 16 l), so every fragment read is one conflict-free ds_read_b128 per lane.  Workgroups that
+// share a weight tile are adjacent in launch order (x over M tiles), so each weight tile is read
+// from HBM once and re-served from L2.
 //
 // The producers of A write the hi/lo pair directly: RMSNorm (before QKV and gate/up), the
 // attention output (before O) and the SwiGLU of the gate/up output (before down).
@@ -162,26 +164,33 @@ __device__ __forceinline__ void wait_vm() {
 // The same product as gemm_kernel (same MFMAs in the same order: bit-identical results) for K a
 // multiple of 32, with the operand tiles copied into a ring of three LDS stages by
 // global_load_lds: tile t + 2 is in flight while tile t is multiplied, and no registers stage it.
-// Wavefront w fills fragments 2w and 2w + 1 of each operand tile, one load instruction each:
-// lane l of fragment f = (32-row block f / 2, k16 half f % 2) loads row 32 (f / 2) + (l & 31),
+// Each wavefront computes WB x WB blocks of 32 x 32, so a workgroup tile is 64 WB square: WB = 2
+// gives the 128 x 128 tile, WB = 4 the 256 x 256 tile (16 accumulator blocks per wavefront, one
+// wavefront per SIMD), which reads half as many operand bytes per product from L2 and LDS.
+// Wavefront w fills fragments WB w .. WB w + WB - 1 of each operand tile, one load instruction
+// each: lane l of fragment f = (32-row block f / 2, k16 half f % 2) loads row 32 (f / 2) + (l & 31),
 // k offset 16 (f % 2) + 8 (l >> 5) -- exactly the fragment-order slot f * 64 + l.
-template <int MODE>
+template <int MODE, int WB>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     constexpr int S = 3;
-    constexpr int PER_TILE = 6;  // load instructions per wavefront per k tile
-    __shared__ uint4 lds[S][3][kFrag];
+    constexpr int TILE = 64 * WB;                 // workgroup tile rows of each operand
+    constexpr int FRAGS = (TILE / 32) * (BK / 16);  // fragments per operand tile
+    constexpr int SLOTS = FRAGS * 64;             // 16-byte slots per operand tile
+    constexpr int PER_TILE = 3 * WB;              // load instructions per wavefront per k tile
+    static_assert(FRAGS == 4 * WB, "each wavefront loads WB fragments of each operand");
+    __shared__ uint4 lds[S][3][SLOTS];
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4 *)&lds[0][0][0];
     const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const int m0 = blockIdx.x * TILE, n0 = blockIdx.y * TILE;
     const uint16_t *W = a.w[blockIdx.z];
     const int M = a.M, N = a.N, K = a.K, nk = K / BK;
 
     // rows past M or N are clamped (in bounds); their results are never stored
-    const uint16_t *src_hi[2], *src_lo[2], *src_w[2];
+    const uint16_t *src_hi[WB], *src_lo[WB], *src_w[WB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int f = wave * 2 + i, r = (f >> 1) * 32 + (lane & 31), kof = (f & 1) * 16 + (lane >> 5) * 8;
+    for (int i = 0; i < WB; ++i) {
+        const int f = wave * WB + i, r = (f >> 1) * 32 + (lane & 31), kof = (f & 1) * 16 + (lane >> 5) * 8;
         const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
         src_hi[i] = a.a_hi + (size_t)m * a.lda + kof;
         src_lo[i] = a.a_lo + (size_t)m * a.lda + kof;
@@ -190,19 +199,19 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     auto issue = [&](int t) {
         const int st = t % S, k0 = t * BK;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int f = wave * 2 + i;
-            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * kFrag + f * 64) * 16);
-            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * kFrag + f * 64) * 16);
-            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * kFrag + f * 64) * 16);
+        for (int i = 0; i < WB; ++i) {
+            const int f = wave * WB + i;
+            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + f * 64) * 16);
+            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + f * 64) * 16);
+            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + f * 64) * 16);
         }
     };
 
-    f32x16 acc[2][2];
+    f32x16 acc[WB][WB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WB; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WB; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -217,19 +226,19 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
         const uint4 *L = &lds[t % S][0][0];
 #pragma unroll
         for (int step = 0; step < BK / 16; ++step) {
-            bf16x8 ah[2], al[2], bw[2];
+            bf16x8 ah[WB], al[WB], bw[WB];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                const int sa = ((wm * 2 + b) * (BK / 16) + step) * 64 + lane;
-                const int sb = ((wn * 2 + b) * (BK / 16) + step) * 64 + lane;
+            for (int b = 0; b < WB; ++b) {
+                const int sa = ((wm * WB + b) * (BK / 16) + step) * 64 + lane;
+                const int sb = ((wn * WB + b) * (BK / 16) + step) * 64 + lane;
                 ah[b] = as_bf16x8(L[sa]);
-                al[b] = as_bf16x8(L[kFrag + sa]);
-                bw[b] = as_bf16x8(L[2 * kFrag + sb]);
+                al[b] = as_bf16x8(L[SLOTS + sa]);
+                bw[b] = as_bf16x8(L[2 * SLOTS + sb]);
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < WB; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
+                for (int j = 0; j < WB; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bw[j], acc[i][j], 0, 0, 0);
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bw[j], acc[i][j], 0, 0, 0);
                 }
@@ -238,14 +247,14 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
 
     const int col_off = a.out_col[blockIdx.z];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WB; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < WB; ++j) {
+            const int n = n0 + wn * 32 * WB + j * 32 + (lane & 31);
             if (n >= N) continue;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int m = m0 + wm * 32 * WB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 if (m >= M) continue;
                 const size_t o = (size_t)m * a.ldo + col_off + n;
                 if (MODE == GEMM_RESIDUAL)
@@ -298,19 +307,25 @@ int grid_for(size_t count) {
     return (int)(g < 8192 ? g : 8192);
 }
 
+template <int MODE>
+void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
+    dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, n_mats);
+    dim3 wide((a.M + 255) / 256, (a.N + 255) / 256, n_mats);
+    if (a.K % BK != 0)
+        hipLaunchKernelGGL(gemm_kernel<MODE>, grid, dim3(256), 0, st, a);
+    else if ((long)wide.x * wide.y * wide.z >= 256)   // the wide tiles still fill every compute unit
+        hipLaunchKernelGGL((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);
+}
+
 }  // namespace
 
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) {
     if (a.M <= 0) return hipSuccess;
-    dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, n_mats);
-    const bool dma = a.K % BK == 0;   // whole k tiles: the LDS-DMA ring (bit-identical results)
-    if (mode == GEMM_RESIDUAL) {
-        if (dma) hipLaunchKernelGGL(gemm_dma_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
-        else hipLaunchKernelGGL(gemm_kernel<GEMM_RESIDUAL>, grid, dim3(256), 0, st, a);
-    } else {
-        if (dma) hipLaunchKernelGGL(gemm_dma_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
-        else hipLaunchKernelGGL(gemm_kernel<GEMM_STORE>, grid, dim3(256), 0, st, a);
-    }
+    // every variant runs the same MFMAs in the same order: the choice never changes a bit
+    if (mode == GEMM_RESIDUAL) launch_gemm_mode<GEMM_RESIDUAL>(a, n_mats, st);
+    else launch_gemm_mode<GEMM_STORE>(a, n_mats, st);
     return hipGetLastError();
 }
 
