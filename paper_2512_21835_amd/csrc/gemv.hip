@@ -29,7 +29,11 @@
 // (lane l: row l % 16, 16 bytes at k = 32 s + 8 (l / 16)).  The same K split across the four
 // wavefronts (128-wide k chunks, chunk c to wavefront c % 4), the same wavefront-order sum in
 // LDS and the same epilogues.  Its results are independent of the row count too, but differ in
-// rounding from the vector kernel's (by ~1e-5 relative).
+// rounding from the vector kernel's (by ~1e-5 relative).  With a workspace, the QKV, O and down
+// projections run it split: 64 units per workgroup (each workgroup then re-reads the activation
+// rows, 64 bytes per k at 16 rows, for four times as many weight rows) and K cut into up to 8
+// ranges across workgroups so the grid still covers the GPU; a second launch adds the ranges in
+// ascending order and applies the epilogue.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -257,9 +261,11 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
     return r;
 }
 
-// One workgroup: RB blocks of 16 units (units blockIdx.x * 16 RB ..) for up to 16 activation rows.
-template <int MODE, int RB>
-__global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
+// One workgroup: RB blocks of 16 units (units blockIdx.x * 16 RB ..) for up to 16 activation rows;
+// SPLIT: k chunks [blockIdx.y * cps, (blockIdx.y + 1) * cps) only, partial results to the
+// workspace.
+template <int MODE, int RB, bool SPLIT = false>
+__global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     constexpr bool kNorm = Shape<MODE>::kNorm;
     constexpr int NW = Shape<MODE>::NW;
     __shared__ float part[kWaves][NW * RB][16][17];   // wavefront partial D[m][n] per weight block
@@ -285,7 +291,9 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
 #pragma unroll
         for (int b = 0; b < RB; ++b) d[w][b] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
-    for (int c = wave; c < chunks; c += kWaves) {
+    const int c_beg = SPLIT ? blockIdx.y * cps : 0;
+    const int c_end = SPLIT ? min(c_beg + cps, chunks) : chunks;
+    for (int c = c_beg + wave; c < c_end; c += kWaves) {
         uint4 wv[4][NW][RB];
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4)
@@ -335,6 +343,20 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
     }
     __syncthreads();
 
+    if (SPLIT) {  // workspace [split][w][m][units], wavefront-order sums
+        const int split = blockIdx.y;
+        for (int e = threadIdx.x; e < NW * 16 * RB * kMfmaRows; e += 256) {
+            const int m = e % kMfmaRows, r = e / kMfmaRows, ub = r % (16 * RB), w = r / (16 * RB);
+            const int u = unit0 + ub, wb = w * RB + ub / 16, n = ub % 16;
+            if (m >= rows || u >= units) continue;
+            a.split_part[(((size_t)split * NW + w) * kMfmaRows + m) * units + u] =
+                ((part[0][wb][m][n] + part[1][wb][m][n]) + part[2][wb][m][n]) + part[3][wb][m][n];
+        }
+        if (kNorm && blockIdx.x == 0 && threadIdx.x < rows)
+            a.split_ss[split * kMfmaRows + threadIdx.x] =
+                ((ssp[0][threadIdx.x] + ssp[1][threadIdx.x]) + ssp[2][threadIdx.x]) + ssp[3][threadIdx.x];
+        return;
+    }
     for (int e = threadIdx.x; e < 16 * RB * kMfmaRows; e += 256) {
         const int m = e % kMfmaRows, ub = e / kMfmaRows, b = ub / 16, n = ub % 16;
         const int u = unit0 + ub;
@@ -354,23 +376,80 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a) {
     }
 }
 
+// Adds the k ranges of a split matrix-core launch in ascending order and applies the epilogue:
+// one thread per (row, unit).
+template <int MODE>
+__global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int splits) {
+    constexpr bool kNorm = Shape<MODE>::kNorm;
+    constexpr int NW = Shape<MODE>::NW;
+    const int units = n_units<MODE>(a);
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= a.rows * units) return;
+    const int m = e / units, u = e % units;
+    float t[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        float acc = a.split_part[((size_t)w * kMfmaRows + m) * units + u];
+        for (int sp = 1; sp < splits; ++sp) acc += a.split_part[(((size_t)sp * NW + w) * kMfmaRows + m) * units + u];
+        t[w] = acc;
+    }
+    float scale = 1.f;
+    if (kNorm) {
+        float sq = a.split_ss[m];
+        for (int sp = 1; sp < splits; ++sp) sq += a.split_ss[sp * kMfmaRows + m];
+        scale = 1.f / sqrtf(sq / (float)a.K + a.eps);
+    }
+    const float y0 = t[0] * scale;
+    if (MODE == GEMV_NORM_ROPE_KV) {
+        rope_kv_epilogue(a, u, m, y0, t[NW - 1] * scale);
+    } else if (MODE == GEMV_PLAIN_RESIDUAL) {
+        a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
+    } else {
+        const float up = t[NW - 1] * scale;
+        a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
+    }
+}
+
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
 
 template <int MODE, int RB>
 void launch_mfma_rb(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int grid = (host_units(MODE, c) + 16 * RB - 1) / (16 * RB);
     if (e0 || e1)
-        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c, 0);
     else
-        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, c);
+        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, c, 0);
+}
+
+// Split launch: 64 units per workgroup, k ranges so that the grid has about 256 workgroups (up to
+// 8; swept on the 8B- and 70B-shaped QKV, O and down projections), then the epilogue launch.
+template <int MODE>
+void launch_mfma_split(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    const int units = host_units(MODE, c), chunks = c.K / kChunkK;
+    const int blocks = (units + 63) / 64;
+    int splits = (256 + blocks - 1) / blocks;
+    splits = max(1, min(splits, min(kGemvMaxSplits, chunks)));
+    const int cps = (chunks + splits - 1) / splits;
+    splits = (chunks + cps - 1) / cps;  // no empty range
+    if (e0)
+        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, 4, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
+                              c, cps);
+    else
+        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, 4, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
+    const int eg = (c.rows * units + 255) / 256;
+    if (e1)
+        hipExtLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, nullptr, e1, 0, c, splits);
+    else
+        hipLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, c, splits);
 }
 
 // Two 16-unit blocks per workgroup where that still gives at least 256 workgroups (swept on the
 // 8B- and 70B-shaped layers: fewer workgroups than compute units cost more than the block pair
-// saves), one otherwise.
+// saves), one otherwise; the split launch for the QKV, O and down projections given a workspace.
 template <int MODE>
 void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    if (host_units(MODE, c) >= 32 * 256) launch_mfma_rb<MODE, 2>(c, st, e0, e1);
+    if (MODE != GEMV_NORM_SWIGLU && c.split_part && c.split_ss) launch_mfma_split<MODE>(c, st, e0, e1);
+    else if (host_units(MODE, c) >= 32 * 256) launch_mfma_rb<MODE, 2>(c, st, e0, e1);
     else launch_mfma_rb<MODE, 1>(c, st, e0, e1);
 }
 

@@ -53,7 +53,12 @@ struct GemvArgs {
     int n_q_heads;
     int kv_fp32;
     const CallMeta *meta;  // device copy of the call's row metadata
+    // Matrix-core launches of the QKV, O and down projections split K across workgroups when
+    // given this workspace: [8][2][16][units] partial products and [8][16] partial sums of squares.
+    float *split_part;
+    float *split_ss;
 };
+constexpr int kGemvMaxSplits = 8;
 
 // y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).  K must be a
 // multiple of 8.  Non-null events are recorded at the start of the first and the end of the last

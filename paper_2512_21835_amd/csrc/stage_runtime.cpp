@@ -130,6 +130,7 @@ struct stage {
     size_t part_rows = 0;
     int max_splits = 0;
     float *ws_part_o = nullptr, *ws_part_ml = nullptr;
+    float *ws_split = nullptr, *ws_split_ss = nullptr;  // split matrix-core GEMV partials
     void *ws_dense = nullptr;
     size_t ws_dense_bytes = 0;
 
@@ -736,6 +737,8 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     q.n_q_heads = s->Hq;
     q.kv_fp32 = s->cfg.kv_fp32;
     q.meta = meta;
+    q.split_part = s->ws_split;  // matrix-core launches of QKV, O and down split K
+    q.split_ss = s->ws_split_ss;
 
     AttnArgs at{};
     at.q = s->ws_q;
@@ -761,6 +764,8 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     o.N = s->H;
     o.K = (int)qd;
     o.rows = rows;
+    o.split_part = s->ws_split;
+    o.split_ss = s->ws_split_ss;
 
     GemvArgs gu{};
     gu.w = mlp + s->off_wg / 2;
@@ -785,6 +790,8 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     dn.N = s->H;
     dn.K = s->F;
     dn.rows = rows;
+    dn.split_part = s->ws_split;
+    dn.split_ss = s->ws_split_ss;
 
     // Timed kernel: the gate/up projection of one layer per call (rotating), so that the events
     // barely perturb the step.
@@ -1107,7 +1114,10 @@ int stage_init(const stage_config *cfg, stage **out) {
         hipMalloc(&s->d_table, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
         hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
         hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
-        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess) {
+        hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess ||
+        hipMalloc(&s->ws_split, sizeof(float) * kGemvMaxSplits * 2 * 16 *
+                                    std::max<size_t>(s->qkv_rows / 2, s->H)) != hipSuccess ||
+        hipMalloc(&s->ws_split_ss, sizeof(float) * kGemvMaxSplits * 16) != hipSuccess) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);
     }
@@ -1154,7 +1164,8 @@ int stage_destroy(stage *s) {
     for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_hi, (void *)s->ws_lo,
-                    (void *)s->ws_part_o, (void *)s->ws_part_ml, s->ws_dense})
+                    (void *)s->ws_part_o, (void *)s->ws_part_ml, (void *)s->ws_split, (void *)s->ws_split_ss,
+                    s->ws_dense})
         if (p) (void)hipFree(p);
     if (s->own_cs && s->cs) (void)hipStreamDestroy(s->cs);
     if (s->own_xs && s->xs) (void)hipStreamDestroy(s->xs);
