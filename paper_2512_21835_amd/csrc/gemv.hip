@@ -22,18 +22,22 @@
 // workgroup computes what and how loads are batched, so results do not depend on how many
 // micro-batches share a call.
 //
-// Matrix-core engine (gemv_mfma_kernel), for launches of 5 to 16 activation rows, where the
-// vector kernel becomes bound by its multiply-adds (one per row per weight element): the rows
-// are the A operand of v_mfma_f32_16x16x32_bf16 (padded to 16, the fp32 activation as a bf16
-// hi + lo pair, two MFMAs), 16 weight rows of a block the B operand, read straight from memory
-// (lane l: row l % 16, 16 bytes at k = 32 s + 8 (l / 16)).  The same K split across the four
-// wavefronts (128-wide k chunks, chunk c to wavefront c % 4), the same wavefront-order sum in
-// LDS and the same epilogues.  Its results are independent of the row count too, but differ in
-// rounding from the vector kernel's (by ~1e-5 relative).  With a workspace, the QKV, O and down
-// projections run it split: 64 units per workgroup (each workgroup then re-reads the activation
-// rows, 64 bytes per k at 16 rows, for four times as many weight rows) and K cut into up to 8
-// ranges across workgroups so the grid still covers the GPU; a second launch adds the ranges in
-// ascending order and applies the epilogue.
+// Matrix-core engine (gemv_mfma_kernel), for launches of 3 to 16 activation rows (5 to 16 for
+// the square O projection), where the vector kernel falls behind (one multiply-add per row per
+// weight element): the rows are the A operand of v_mfma_f32_16x16x32_bf16 (padded to 16, the
+// fp32 activation as a bf16 hi + lo pair, two MFMAs), 16 weight rows the B operand.  A workgroup owns 64 units, each
+// wavefront 16 of them over the workgroup's K range, in chunks of 128 k.  The B layout wants 16
+// rows x 64 bytes per load instruction, which streams HBM poorly (~4 TB/s), so a wavefront loads
+// its chunk as 4 rows x 256 contiguous bytes per instruction, stores it in its own LDS tile (the
+// 16-byte k segments XOR-swizzled by row, so the stores are contiguous and the MFMA-layout reads
+// are free of bank conflicts) and reads it back as B fragments.  The A fragments of a chunk are
+// converted once per workgroup (one per thread) into a double-buffered LDS tile, one barrier per
+// chunk; the next chunk's weights and activations are loaded before the current one is used.
+// Per output element: MFMA accumulation over the chunks in ascending k.  Where the grid would not
+// cover the GPU, K is cut into up to 8 ranges across workgroups (partial products to a
+// workspace) and a second launch adds the ranges in ascending order and applies the epilogue.
+// Which of the two runs depends on the layer shape only, so results are independent of the row
+// count; they differ in rounding from the vector kernel's (by ~1e-5 relative).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -252,7 +256,6 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kMfmaRows = 16;     // activation rows per matrix-core launch
-constexpr int kMfmaMinRows = 5;   // fewer rows: the vector kernel is faster
 constexpr int kChunkK = 128;      // k per wavefront chunk (4 MFMA k steps of 32)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
@@ -261,116 +264,141 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
     return r;
 }
 
-// One workgroup: RB blocks of 16 units (units blockIdx.x * 16 RB ..) for up to 16 activation rows;
-// SPLIT: k chunks [blockIdx.y * cps, (blockIdx.y + 1) * cps) only, partial results to the
-// workspace.
-template <int MODE, int RB, bool SPLIT = false>
+// One workgroup: units 64 blockIdx.x .. + 63 (wavefront w: 16 of them) for up to 16 activation
+// rows.  SPLIT: k chunks [blockIdx.y * cps, (blockIdx.y + 1) * cps) only, partial products and
+// sums of squares to the workspace [split][w][m][units], [split][m].
+template <int MODE, bool SPLIT>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     constexpr bool kNorm = Shape<MODE>::kNorm;
     constexpr int NW = Shape<MODE>::NW;
-    __shared__ float part[kWaves][NW * RB][16][17];   // wavefront partial D[m][n] per weight block
-    __shared__ float ssp[kWaves][16];                  // wavefront partial sums of squares per row
+    __shared__ uint4 bt[kWaves][NW][256];   // wavefront B tile: row r, k segment s at 16 r + (s ^ r)
+    __shared__ uint4 at[2][4][2][64];       // A fragments [buffer][k step][hi, lo][lane]
+    __shared__ float ssp[kWaves][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int units = n_units<MODE>(a);
-    const int unit0 = blockIdx.x * 16 * RB;
+    const int u0 = blockIdx.x * 64 + 16 * wave;
     const int K = a.K, chunks = K / kChunkK, rows = a.rows;
-    const int nl = lane & 15, kq = lane >> 4;
-    const bool mvalid = nl < rows;   // this lane's A row (activation row nl)
-
-    const uint16_t *wrow[NW][RB];
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-#pragma unroll
-        for (int b = 0; b < RB; ++b)
-            wrow[w][b] = unit_row<MODE>(a, min(unit0 + 16 * b + nl, units - 1), w) + 8 * kq;
-    const float *xr = a.act + (size_t)(mvalid ? nl : 0) * a.act_ld + 8 * kq;
-
-    f32x4 d[NW][RB];
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-#pragma unroll
-        for (int b = 0; b < RB; ++b) d[w][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float ss = 0.f;
     const int c_beg = SPLIT ? blockIdx.y * cps : 0;
     const int c_end = SPLIT ? min(c_beg + cps, chunks) : chunks;
-    for (int c = c_beg + wave; c < c_end; c += kWaves) {
-        uint4 wv[4][NW][RB];
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-            for (int w = 0; w < NW; ++w)
-#pragma unroll
-                for (int b = 0; b < RB; ++b) wv[s4][w][b] = load_stream16(wrow[w][b] + kChunkK * c + 32 * s4);
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            const int k = kChunkK * c + 32 * s4;
-            const float4 x0 = *reinterpret_cast<const float4 *>(xr + k);
-            const float4 x1 = *reinterpret_cast<const float4 *>(xr + k + 4);
-            float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-            float g[8];
-            if (kNorm) unpack8(*reinterpret_cast<const uint4 *>(a.gain + k + 8 * kq), g);
-            bf16x8 xh, xl;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                float v = mvalid ? x[j] : 0.f;
-                if (kNorm) {
-                    ss = fmaf(v, v, ss);
-                    v = v * g[j];
-                }
-                xh[j] = (__bf16)v;                       // nearest even
-                xl[j] = (__bf16)(v - (float)xh[j]);
-            }
-#pragma unroll
-            for (int w = 0; w < NW; ++w)
-#pragma unroll
-                for (int b = 0; b < RB; ++b) {
-                    d[w][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, as_bf16x8(wv[s4][w][b]), d[w][b], 0, 0, 0);
-                    d[w][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl, as_bf16x8(wv[s4][w][b]), d[w][b], 0, 0, 0);
-                }
-        }
-    }
-    // result register i of lane l: D[m = 4 (l / 16) + i][n = l % 16]
+
+    // load instruction i of matrix w: lane l reads row 4 i + l / 16 of the block, k segment
+    // (l % 16) ^ row (8 bf16), i.e. 256 contiguous bytes per row; rows past the last unit are
+    // clamped to it (in bounds, results dropped)
+    const int lr = lane >> 4, lk = lane & 15;
+    const uint16_t *wp[NW][4];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
-        for (int b = 0; b < RB; ++b)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) part[wave][w * RB + b][4 * kq + i][nl] = d[w][b][i];
-    if (kNorm) {
-        ss += __shfl_xor(ss, 16, 64);
-        ss += __shfl_xor(ss, 32, 64);
-        if (lane < 16) ssp[wave][lane] = ss;
-    }
-    __syncthreads();
-
-    if (SPLIT) {  // workspace [split][w][m][units], wavefront-order sums
-        const int split = blockIdx.y;
-        for (int e = threadIdx.x; e < NW * 16 * RB * kMfmaRows; e += 256) {
-            const int m = e % kMfmaRows, r = e / kMfmaRows, ub = r % (16 * RB), w = r / (16 * RB);
-            const int u = unit0 + ub, wb = w * RB + ub / 16, n = ub % 16;
-            if (m >= rows || u >= units) continue;
-            a.split_part[(((size_t)split * NW + w) * kMfmaRows + m) * units + u] =
-                ((part[0][wb][m][n] + part[1][wb][m][n]) + part[2][wb][m][n]) + part[3][wb][m][n];
+        for (int i = 0; i < 4; ++i) {
+            const int r = 4 * i + lr;
+            wp[w][i] = unit_row<MODE>(a, min(u0 + r, units - 1), w) + 8 * (lk ^ r);
         }
-        if (kNorm && blockIdx.x == 0 && threadIdx.x < rows)
-            a.split_ss[split * kMfmaRows + threadIdx.x] =
-                ((ssp[0][threadIdx.x] + ssp[1][threadIdx.x]) + ssp[2][threadIdx.x]) + ssp[3][threadIdx.x];
-        return;
+    // this thread's A fragment: k step `wave` of the chunk, lane `lane` (row l % 16, k 8 (l / 16))
+    const int am = lane & 15, ak = 32 * wave + 8 * (lane >> 4);
+    const bool avalid = am < rows;
+    const float *xp = a.act + (size_t)(avalid ? am : 0) * a.act_ld + ak;
+    const uint16_t *gp = a.gain + ak;
+
+    f32x4 d[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) d[w] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float ss = 0.f;
+
+    struct Chunk {
+        uint4 w[NW][4];
+        float4 x0, x1;
+        uint4 g;
+    };
+    auto load = [&](int c, Chunk &b) {
+        const int k = c * kChunkK;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) b.w[w][i] = load_stream16(wp[w][i] + k);
+        b.x0 = *reinterpret_cast<const float4 *>(xp + k);
+        b.x1 = *reinterpret_cast<const float4 *>(xp + k + 4);
+        if (kNorm) b.g = *reinterpret_cast<const uint4 *>(gp + k);
+    };
+    auto compute = [&](int c, const Chunk &b) {
+        const int buf = c & 1;
+        const float x[8] = {b.x0.x, b.x0.y, b.x0.z, b.x0.w, b.x1.x, b.x1.y, b.x1.z, b.x1.w};
+        float g[8];
+        if (kNorm) unpack8(b.g, g);
+        bf16x8 xh, xl;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float v = avalid ? x[j] : 0.f;
+            if (kNorm) {
+                ss = fmaf(v, v, ss);
+                v = v * g[j];
+            }
+            xh[j] = (__bf16)v;                       // nearest even
+            xl[j] = (__bf16)(v - (float)xh[j]);
+        }
+        uint4 h4, l4;
+        __builtin_memcpy(&h4, &xh, 16);
+        __builtin_memcpy(&l4, &xl, 16);
+        at[buf][wave][0][lane] = h4;
+        at[buf][wave][1][lane] = l4;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) bt[wave][w][64 * i + lane] = b.w[w][i];
+        // A tile complete for every wavefront; the buffer written next chunk was last read
+        // before this barrier
+        __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const bf16x8 ah = as_bf16x8(at[buf][t][0][lane]);
+            const bf16x8 al = as_bf16x8(at[buf][t][1][lane]);
+#pragma unroll
+            for (int w = 0; w < NW; ++w) {
+                const bf16x8 bw = as_bf16x8(bt[wave][w][16 * lk + ((4 * t + lr) ^ lk)]);
+                d[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw, d[w], 0, 0, 0);
+                d[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, d[w], 0, 0, 0);
+            }
+        }
+    };
+    Chunk b0, b1;
+    if (c_beg < c_end) load(c_beg, b0);
+    for (int c = c_beg; c < c_end; c += 2) {
+        if (c + 1 < c_end) load(c + 1, b1);
+        compute(c, b0);
+        if (c + 1 >= c_end) break;
+        if (c + 2 < c_end) load(c + 2, b0);
+        compute(c + 1, b1);
     }
-    for (int e = threadIdx.x; e < 16 * RB * kMfmaRows; e += 256) {
-        const int m = e % kMfmaRows, ub = e / kMfmaRows, b = ub / 16, n = ub % 16;
-        const int u = unit0 + ub;
+
+    // a row's sum of squares: 16 thread partials (4 k steps x 4 k blocks) in a fixed order
+    if (kNorm) ssp[wave][lane] = ss;
+    __syncthreads();
+    auto row_ss = [&](int m) {
+        float t = 0.f;
+        for (int w = 0; w < kWaves; ++w)
+            for (int q = 0; q < 4; ++q) t += ssp[w][16 * q + m];
+        return t;
+    };
+    if (SPLIT && kNorm && blockIdx.x == 0 && threadIdx.x < kMfmaRows)
+        a.split_ss[blockIdx.y * kMfmaRows + threadIdx.x] = row_ss(threadIdx.x);
+    // result register i of lane l: D[m = 4 (l / 16) + i][n = l % 16]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = 4 * lr + i, u = u0 + lk;
         if (m >= rows || u >= units) continue;
-        auto total = [&](int wb) { return ((part[0][wb][m][n] + part[1][wb][m][n]) + part[2][wb][m][n]) + part[3][wb][m][n]; };
-        float scale = 1.f;
-        if (kNorm) scale = 1.f / sqrtf((((ssp[0][m] + ssp[1][m]) + ssp[2][m]) + ssp[3][m]) / (float)K + a.eps);
-        const float y0 = total(b) * scale;
+        if (SPLIT) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                a.split_part[(((size_t)blockIdx.y * NW + w) * kMfmaRows + m) * units + u] = d[w][i];
+            continue;
+        }
+        const float scale = kNorm ? 1.f / sqrtf(row_ss(m) / (float)K + a.eps) : 1.f;
+        const float y0 = d[0][i] * scale;
         if (MODE == GEMV_NORM_ROPE_KV) {
-            rope_kv_epilogue(a, u, m, y0, total(RB + b) * scale);
+            rope_kv_epilogue(a, u, m, y0, d[NW - 1][i] * scale);
         } else if (MODE == GEMV_PLAIN_RESIDUAL) {
             a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
         } else {
-            const float up = total(RB + b) * scale;
+            const float up = d[NW - 1][i] * scale;
             a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
         }
     }
@@ -412,45 +440,36 @@ __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int split
 
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
 
-template <int MODE, int RB>
-void launch_mfma_rb(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    const int grid = (host_units(MODE, c) + 16 * RB - 1) / (16 * RB);
-    if (e0 || e1)
-        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c, 0);
-    else
-        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, RB>), dim3(grid), dim3(256), 0, st, c, 0);
-}
-
-// Split launch: 64 units per workgroup, k ranges so that the grid has about 256 workgroups (up to
-// 8; swept on the 8B- and 70B-shaped QKV, O and down projections), then the epilogue launch.
+// K ranges: about 640 workgroups in all, at most 8 ranges and at least 2 chunks per range (swept
+// on the 8B- and 70B-shaped projections at 5, 8 and 16 rows: 70B gate/up runs unsplit with 448
+// workgroups, the 8B gate/up in 3 ranges, the O and down projections in 5-8).  Without a
+// workspace, unsplit.
 template <int MODE>
-void launch_mfma_split(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int units = host_units(MODE, c), chunks = c.K / kChunkK;
     const int blocks = (units + 63) / 64;
-    int splits = (256 + blocks - 1) / blocks;
-    splits = max(1, min(splits, min(kGemvMaxSplits, chunks)));
+    int splits = (640 + blocks / 2) / blocks;
+    splits = max(1, min(splits, min(kGemvMaxSplits, chunks / 2)));
+    if (!c.split_part || !c.split_ss) splits = 1;
+    if (splits == 1) {
+        if (e0 || e1)
+            hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, c, 0);
+        else
+            hipLaunchKernelGGL((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, c, 0);
+        return;
+    }
     const int cps = (chunks + splits - 1) / splits;
     splits = (chunks + cps - 1) / cps;  // no empty range
     if (e0)
-        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, 4, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
+        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
                               c, cps);
     else
-        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, 4, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
+        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
     const int eg = (c.rows * units + 255) / 256;
     if (e1)
         hipExtLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, nullptr, e1, 0, c, splits);
     else
         hipLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, c, splits);
-}
-
-// Two 16-unit blocks per workgroup where that still gives at least 256 workgroups (swept on the
-// 8B- and 70B-shaped layers: fewer workgroups than compute units cost more than the block pair
-// saves), one otherwise; the split launch for the QKV, O and down projections given a workspace.
-template <int MODE>
-void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-    if (MODE != GEMV_NORM_SWIGLU && c.split_part && c.split_ss) launch_mfma_split<MODE>(c, st, e0, e1);
-    else if (host_units(MODE, c) >= 32 * 256) launch_mfma_rb<MODE, 2>(c, st, e0, e1);
-    else launch_mfma_rb<MODE, 1>(c, st, e0, e1);
 }
 
 template <int M, int R, int U, int MODE>
@@ -488,9 +507,13 @@ template <int MODE>
 hipError_t launch_mode(const GemvArgs &a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
     // 16-unit blocks must not straddle the two halves of a RoPE head
     const bool mfma_ok = a.K % kChunkK == 0 && (MODE != GEMV_NORM_ROPE_KV || (a.kv.head_dim / 2) % 16 == 0);
+    // rows from which the matrix cores are faster (measured on the 8B- and 70B-shaped layers):
+    // 3, except for square plain projections (the O projection), where the vector kernel keeps up
+    // to 4 rows
+    const int mfma_min_rows = MODE == GEMV_PLAIN_RESIDUAL && a.K <= a.N ? 5 : 3;
     for (int r0 = 0, n = 0; r0 < a.rows; r0 += n) {
         const int left = a.rows - r0;
-        const bool mfma = mfma_ok && left >= kMfmaMinRows;
+        const bool mfma = mfma_ok && left >= mfma_min_rows;
         n = min(left, mfma ? kMfmaRows : kMaxRowsPerLaunch);
         GemvArgs c = a;
         c.rows = n;

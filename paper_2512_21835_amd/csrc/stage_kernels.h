@@ -53,8 +53,8 @@ struct GemvArgs {
     int n_q_heads;
     int kv_fp32;
     const CallMeta *meta;  // device copy of the call's row metadata
-    // Matrix-core launches of the QKV, O and down projections split K across workgroups when
-    // given this workspace: [8][2][16][units] partial products and [8][16] partial sums of squares.
+    // Matrix-core launches split K across workgroups when given this workspace (and the layer
+    // shape calls for it): [8][2][16][units] partial products, [8][16] partial sums of squares.
     float *split_part;
     float *split_ss;
 };

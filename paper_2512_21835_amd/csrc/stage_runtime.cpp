@@ -737,7 +737,7 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     q.n_q_heads = s->Hq;
     q.kv_fp32 = s->cfg.kv_fp32;
     q.meta = meta;
-    q.split_part = s->ws_split;  // matrix-core launches of QKV, O and down split K
+    q.split_part = s->ws_split;  // matrix-core launches may split K
     q.split_ss = s->ws_split_ss;
 
     AttnArgs at{};
@@ -779,6 +779,8 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     gu.K = s->H;
     gu.rows = rows;
     gu.eps = s->cfg.rms_eps;
+    gu.split_part = s->ws_split;
+    gu.split_ss = s->ws_split_ss;
 
     GemvArgs dn{};
     dn.w = mlp + s->off_wd / 2;
@@ -1116,7 +1118,7 @@ int stage_init(const stage_config *cfg, stage **out) {
         hipMalloc(&s->d_sin, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
         hipMalloc(&s->d_meta, sizeof(CallMeta)) != hipSuccess ||
         hipMalloc(&s->ws_split, sizeof(float) * kGemvMaxSplits * 2 * 16 *
-                                    std::max<size_t>(s->qkv_rows / 2, s->H)) != hipSuccess ||
+                                    std::max<size_t>(std::max<size_t>(s->qkv_rows / 2, s->H), s->F)) != hipSuccess ||
         hipMalloc(&s->ws_split_ss, sizeof(float) * kGemvMaxSplits * 16) != hipSuccess) {
         (void)hipGetLastError();
         return cleanup(STAGE_ENOMEM);

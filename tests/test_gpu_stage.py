@@ -23,9 +23,12 @@ TINY_RAGGED = synth.Workload("tiny_ragged", 100, synth.TINY, n_mb=3, batch=2, pr
 # 8B-shaped layers, 3 micro-batches of batch 3: 9 rows per call when all share it, 3 otherwise
 LLAMA8B_MULTI = synth.Workload("llama8b_multi", 101, synth.LLAMA8B_STAGE, n_mb=3, batch=3, prefill=24,
                                decode_steps=3)
-# row counts that stay on one decode engine under both groupings: 2 vs 4 rows (vector), 8 vs 16
-TINY_2x2 = synth.Workload("tiny_2x2", 102, synth.TINY, n_mb=2, batch=2, prefill=37, decode_steps=4)
+# row counts that stay on one decode engine under both groupings: 1 vs 2 rows (vector), 8 vs 16
+# (matrix cores); and 2 vs 6 rows, one call of each engine
+TINY_2x1 = synth.Workload("tiny_2x1", 102, synth.TINY, n_mb=2, batch=1, prefill=37, decode_steps=4)
 LLAMA8B_2x8 = synth.Workload("llama8b_2x8", 103, synth.LLAMA8B_STAGE, n_mb=2, batch=8, prefill=24,
+                             decode_steps=3)
+LLAMA8B_3x2 = synth.Workload("llama8b_3x2", 104, synth.LLAMA8B_STAGE, n_mb=3, batch=2, prefill=24,
                              decode_steps=3)
 
 
@@ -289,19 +292,19 @@ def _one_vs_all(wl, prefill, steps):
     return pairs
 
 
-@pytest.mark.parametrize("wl,prefill,steps", [(TINY_2x2, 37, 4), (LLAMA8B_2x8, 24, 3)])
+@pytest.mark.parametrize("wl,prefill,steps", [(TINY_2x1, 37, 4), (LLAMA8B_2x8, 24, 3)])
 def test_round_robin_equals_all_in_one_call_bitwise(wl, prefill, steps):
     """Per-row arithmetic does not depend on how many micro-batches share a call, as long as the
-    decode projections run on the same engine: 2 vs 4 rows per call on the vector kernels (tiny
+    decode projections run on the same engine: 1 vs 2 rows per call on the vector kernels (tiny
     shape), 8 vs 16 rows per call on the matrix cores (8B shape)."""
     _gpu()
     for one, all_ in _one_vs_all(wl, prefill, steps):
         assert np.array_equal(one, all_)
 
 
-@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 4), (LLAMA8B_MULTI, 24, 3)])
+@pytest.mark.parametrize("wl,prefill,steps", [(TINY_RAGGED, 37, 4), (LLAMA8B_3x2, 24, 3)])
 def test_vector_and_matrix_engines_agree(wl, prefill, steps):
-    """Calls of 2-3 rows (vector kernels) and of 6-9 rows (matrix cores) give the same rows up to
+    """Calls of 2 rows (vector kernels) and of 6 rows (matrix cores) give the same rows up to
     rounding: prefill bit for bit (the prefill GEMM is row-count independent), decode within the
     parity bound (the engines round differently, and a decode row's K/V can round to a neighbouring
     bf16 value, which the later steps carry)."""
