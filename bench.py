@@ -387,13 +387,14 @@ def planner_leg(calls: int = 3, ctx: int = 2048, n_steps: int = 6):
 
 
 def kvpressure_leg(contexts=(512, 4352, 8192), rounds: int = 2):
-    """The KV-pressure workload on the 70B-shaped stage: 8 micro-batches of batch 2, decoded round
-    robin one micro-batch per call, residency shrinking 16 -> 8 under the threshold schedule
-    TS_j = 512 + 960 j (one more layer streamed through 2 slots per threshold passed).  Sampled:
-    at each context in `contexts` the caches are filled to it through stage_kv_append (random
-    K/V), then `rounds` decode rounds are timed (one warm-up round first).  Reports the round
-    time, tokens/s, the resident layers, and the HBM fraction (weights of resident layers, slots
-    read once per call, KV read) when no layer streams."""
+    """The KV-pressure workload on the 70B-shaped stage: 8 micro-batches of batch 2, residency
+    shrinking 16 -> 8 under the threshold schedule TS_j = 512 + 960 j (one more layer streamed
+    through 2 slots per threshold passed).  Sampled: at each context in `contexts` the caches are
+    filled to it through stage_kv_append (random K/V), then `rounds` decode rounds are timed (one
+    warm-up round first) two ways: round robin, one micro-batch per call (every call streams the
+    offloaded layers), and all 8 micro-batches in one call (16 rows; each offloaded layer streams
+    once per round).  Reports the round time, tokens/s, the resident layers, and the HBM fraction
+    (weights of resident layers, slots read once per call, KV read) when no layer streams."""
     import torch
 
     import synth
@@ -411,7 +412,7 @@ def kvpressure_leg(contexts=(512, 4352, 8192), rounds: int = 2):
     out = []
     layer = shape.layer_bytes()
     for ctx in contexts:
-        cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=B, max_context=ctx + rounds + 4, n_resident_max=L,
+        cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=B, max_context=ctx + 2 * rounds + 6, n_resident_max=L,
                            n_stream_slots=2, thresholds=wl.thresholds, compute_stream=cstream.cuda_stream,
                            copy_stream=xstream.cuda_stream)
         h = P.stage_init(cfg)
@@ -442,6 +443,15 @@ def kvpressure_leg(contexts=(512, 4352, 8192), rounds: int = 2):
             P.stage_sync(h)
             dt = (time.perf_counter() - t0) / rounds
             res = P.stage_get_residency(h, L)
+            x_all, y_all = x.contiguous(), torch.empty_like(x)
+            P.stage_decode(h, list(range(n_mb)), B, x_all, y_all)    # warm-up of the one-call grouping
+            P.stage_sync(h)
+            t0 = time.perf_counter()
+            for _ in range(rounds):
+                P.stage_decode(h, list(range(n_mb)), B, x_all, y_all)
+            P.stage_sync(h)
+            dt1 = (time.perf_counter() - t0) / rounds
+            res1 = P.stage_get_residency(h, L)
         finally:
             P.stage_destroy(h)
         resident = sum(1 for c in res if c == 1)
@@ -454,10 +464,19 @@ def kvpressure_leg(contexts=(512, 4352, 8192), rounds: int = 2):
             entry["hbm_frac"] = hbm / dt / 1e9 / HBM_PEAK_GBS
         else:
             entry["streamed_GB_per_round"] = n_mb * (L - resident) * layer / 1e9
+        resident1 = sum(1 for c in res1 if c == 1)
+        one = {"resident_layers": resident1, "ms_per_round": dt1 * 1e3, "tokens_per_s": n_mb * B / dt1}
+        if resident1 == L:
+            hbm1 = L * layer + n_mb * B * L * (ctx + 2 * rounds + 1) * 2 * shape.kv_dim * 2
+            one["hbm_GBs"] = hbm1 / dt1 / 1e9
+            one["hbm_frac"] = hbm1 / dt1 / 1e9 / HBM_PEAK_GBS
+        else:
+            one["streamed_GB_per_round"] = (L - resident1) * layer / 1e9
+        entry["one_call"] = one
         out.append(entry)
     return {"workload": "llama70b_kvpressure decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 8 micro-batches "
-                        "of batch 2 round robin, residency 16 -> 8 by thresholds 512 + 960 j, 2 slots; sampled "
-                        "at the listed contexts",
+                        "of batch 2 round robin (one_call: all 8 in one call), residency 16 -> 8 by thresholds "
+                        "512 + 960 j, 2 slots; sampled at the listed contexts",
             "samples": out}
 
 
