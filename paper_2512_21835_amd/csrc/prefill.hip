@@ -167,17 +167,19 @@ __device__ __forceinline__ void wait_vm() {
 // Each wavefront computes WB x WB blocks of 32 x 32, so a workgroup tile is 64 WB square: WB = 2
 // gives the 128 x 128 tile, WB = 4 the 256 x 256 tile (16 accumulator blocks per wavefront, one
 // wavefront per SIMD), which reads half as many operand bytes per product from L2 and LDS.
-// Wavefront w fills fragments WB w .. WB w + WB - 1 of each operand tile, one load instruction
-// each: lane l of fragment f = (32-row block f / 2, k16 half f % 2) loads row 32 (f / 2) + (l & 31),
-// k offset 16 (f % 2) + 8 (l >> 5) -- exactly the fragment-order slot f * 64 + l.
+// An operand tile in LDS is row-major, four 16-byte k segments per row (BK = 32), segment s of row
+// r stored at slot 4 r + (s ^ ((r >> 2) & 3)): each DMA instruction then copies 16 rows x 64
+// contiguous bytes (lane l: row 16 q + l / 4 of instruction q), and the 32 x 32 fragment reads
+// (lane l: row l % 32, segment 2 step + l / 32) touch every LDS bank once per 16 lanes.  (Loading
+// in fragment order instead, 32 rows x 32 bytes per instruction, took 1.3-1.6x as long.)
 template <int MODE, int WB>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     constexpr int S = 3;
     constexpr int TILE = 64 * WB;                 // workgroup tile rows of each operand
-    constexpr int FRAGS = (TILE / 32) * (BK / 16);  // fragments per operand tile
-    constexpr int SLOTS = FRAGS * 64;             // 16-byte slots per operand tile
+    constexpr int SLOTS = TILE * (BK / 8);        // 16-byte slots per operand tile (4 per row)
     constexpr int PER_TILE = 3 * WB;              // load instructions per wavefront per k tile
-    static_assert(FRAGS == 4 * WB, "each wavefront loads WB fragments of each operand");
+    static_assert(SLOTS == 4 * WB * 64, "each wavefront loads WB instructions of each operand");
+    static_assert(BK == 32, "the segment swizzle assumes four 16-byte k segments per row");
     __shared__ uint4 lds[S][3][SLOTS];
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4 *)&lds[0][0][0];
@@ -186,24 +188,26 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     const uint16_t *W = a.w[blockIdx.z];
     const int M = a.M, N = a.N, K = a.K, nk = K / BK;
 
-    // rows past M or N are clamped (in bounds); their results are never stored
+    // instruction q = wave * WB + i of an operand: lane l copies row 16 q + l / 4, k segment
+    // (l % 4) ^ ((row >> 2) & 3) into slot 64 q + l; rows past M or N are clamped (in bounds),
+    // their results are never stored
     const uint16_t *src_hi[WB], *src_lo[WB], *src_w[WB];
 #pragma unroll
     for (int i = 0; i < WB; ++i) {
-        const int f = wave * WB + i, r = (f >> 1) * 32 + (lane & 31), kof = (f & 1) * 16 + (lane >> 5) * 8;
+        const int q = wave * WB + i, r = 16 * q + (lane >> 2), seg = (lane & 3) ^ ((r >> 2) & 3);
         const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
-        src_hi[i] = a.a_hi + (size_t)m * a.lda + kof;
-        src_lo[i] = a.a_lo + (size_t)m * a.lda + kof;
-        src_w[i] = W + (size_t)n * K + kof;
+        src_hi[i] = a.a_hi + (size_t)m * a.lda + 8 * seg;
+        src_lo[i] = a.a_lo + (size_t)m * a.lda + 8 * seg;
+        src_w[i] = W + (size_t)n * K + 8 * seg;
     }
     auto issue = [&](int t) {
         const int st = t % S, k0 = t * BK;
 #pragma unroll
         for (int i = 0; i < WB; ++i) {
-            const int f = wave * WB + i;
-            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + f * 64) * 16);
-            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + f * 64) * 16);
-            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + f * 64) * 16);
+            const int q = wave * WB + i;
+            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + q * 64) * 16);
+            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + q * 64) * 16);
+            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + q * 64) * 16);
         }
     };
 
@@ -217,6 +221,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
 
     issue(0);
     if (nk > 1) issue(1);
+    const int fr = lane & 31, fk = lane >> 5;   // fragment row and k half of this lane
     for (int t = 0; t < nk; ++t) {
         // tile t has landed when at most the next tile's loads are still in flight
         if (t + 1 < nk) wait_vm<PER_TILE>();
@@ -227,10 +232,12 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
 #pragma unroll
         for (int step = 0; step < BK / 16; ++step) {
             bf16x8 ah[WB], al[WB], bw[WB];
+            const int seg = 2 * step + fk;
 #pragma unroll
             for (int b = 0; b < WB; ++b) {
-                const int sa = ((wm * WB + b) * (BK / 16) + step) * 64 + lane;
-                const int sb = ((wn * WB + b) * (BK / 16) + step) * 64 + lane;
+                const int ra = 32 * (wm * WB + b) + fr, rb = 32 * (wn * WB + b) + fr;
+                const int sa = 4 * ra + (seg ^ ((ra >> 2) & 3));
+                const int sb = 4 * rb + (seg ^ ((rb >> 2) & 3));
                 ah[b] = as_bf16x8(L[sa]);
                 al[b] = as_bf16x8(L[SLOTS + sa]);
                 bw[b] = as_bf16x8(L[2 * SLOTS + sb]);
