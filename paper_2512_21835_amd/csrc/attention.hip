@@ -14,6 +14,7 @@
 // (attn_merge_kernel) merges each row's splits in ascending order.
 #include <hip/hip_runtime.h>
 
+#include "lanes.h"
 #include "stage_kernels.h"
 
 namespace stg {
@@ -70,7 +71,7 @@ __device__ __forceinline__ void attn_merge_group(const AttnArgs &a, int g, int r
         float mx = -INFINITY;
         for (int sp = lane; sp < nsp; sp += 64) mx = fmaxf(mx, sm.cm[h][sp]);
 #pragma unroll
-        for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
+        for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, lane_xor(mx, o2));
         float den = 0.f;
         for (int sp = lane; sp < nsp; sp += 64) {
             const float w = expf(sm.cm[h][sp] - mx);
@@ -78,7 +79,7 @@ __device__ __forceinline__ void attn_merge_group(const AttnArgs &a, int g, int r
             den = fmaf(w, sm.cl[h][sp], den);
         }
 #pragma unroll
-        for (int o2 = 32; o2 >= 1; o2 >>= 1) den += __shfl_xor(den, o2, 64);
+        for (int o2 = 32; o2 >= 1; o2 >>= 1) den += lane_xor(den, o2);
         if (lane == 0) sm.den[h] = den;
     }
     __syncthreads();
@@ -156,7 +157,7 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
 #pragma unroll
             for (int j = 0; j < 8; ++j) p = fmaf(q[h][j], kf[st][j], p);
 #pragma unroll
-            for (int o2 = LPK / 2; o2 >= 1; o2 >>= 1) p += __shfl_xor(p, o2, 64);
+            for (int o2 = LPK / 2; o2 >= 1; o2 >>= 1) p += lane_xor(p, o2);
             sc[st][h] = valid ? p : -INFINITY;
         }
     }
@@ -167,7 +168,7 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
 #pragma unroll
         for (int st = 1; st < STEPS; ++st) m = fmaxf(m, sc[st][h]);
 #pragma unroll
-        for (int o2 = 32; o2 >= LPK; o2 >>= 1) m = fmaxf(m, __shfl_xor(m, o2, 64));
+        for (int o2 = 32; o2 >= LPK; o2 >>= 1) m = fmaxf(m, lane_xor(m, o2));
         if (lane == 0) sm.wm[wave][h] = m;
     }
     __syncthreads();
@@ -195,11 +196,12 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
 #pragma unroll
     for (int h = 0; h < G; ++h) {
 #pragma unroll
-        for (int o2 = 32; o2 >= LPK; o2 >>= 1) l[h] += __shfl_xor(l[h], o2, 64);
+        for (int o2 = 32; o2 >= LPK; o2 >>= 1) l[h] += lane_xor(l[h], o2);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
 #pragma unroll
-            for (int o2 = 32; o2 >= LPK; o2 >>= 1) o[h][j] += __shfl_xor(o[h][j], o2, 64);
+            for (int o2 = 32; o2 >= LPK; o2 >>= 1)   // G >= 8: the VALU is the bound, the LDS crossbar is idle
+                o[h][j] += G >= 8 ? __shfl_xor(o[h][j], o2, 64) : lane_xor(o[h][j], o2);
     }
     if (kl == 0) {
 #pragma unroll
@@ -289,7 +291,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int h = 0; h < G; ++h)
 #pragma unroll
-                for (int o2 = LPK / 2; o2 >= 1; o2 >>= 1) part[h] += __shfl_xor(part[h], o2, 64);
+                for (int o2 = LPK / 2; o2 >= 1; o2 >>= 1) part[h] += lane_xor(part[h], o2);
             if (kk < n && sub == 0) {
 #pragma unroll
                 for (int h = 0; h < G; ++h) s_p[h][kk] = part[h];
@@ -301,13 +303,13 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             const float sv = lane < n ? s_p[h][lane] : -INFINITY;
             float mx = sv;
 #pragma unroll
-            for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
+            for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, lane_xor(mx, o2));
             const float m_old = s_m[h];
             const float m_new = fmaxf(m_old, mx);
             const float p = lane < n ? expf(sv - m_new) : 0.f;
             float sum = p;
 #pragma unroll
-            for (int o2 = 32; o2 >= 1; o2 >>= 1) sum += __shfl_xor(sum, o2, 64);
+            for (int o2 = 32; o2 >= 1; o2 >>= 1) sum += lane_xor(sum, o2);
             s_p[h][lane] = p;
             if (lane == 0) {
                 const float alpha = expf(m_old - m_new);  // 0 on the first chunk (m_old = -inf)
@@ -349,7 +351,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 8; ++j)
 #pragma unroll
-            for (int o2 = 32; o2 >= LPK; o2 >>= 1) o[h][j] += __shfl_xor(o[h][j], o2, 64);
+            for (int o2 = 32; o2 >= LPK; o2 >>= 1) o[h][j] += lane_xor(o[h][j], o2);
     if (kl == 0) {
 #pragma unroll
         for (int h = 0; h < G; ++h)
@@ -520,7 +522,7 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
             if (kp > qpos) s[i] = -INFINITY;
             mt = fmaxf(mt, s[i]);
         }
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        mt = fmaxf(mt, lane_xor(mt, 32));
         const float m_new = fmaxf(m_run, mt);
         const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
         float p[16], ps = 0.f;
@@ -529,7 +531,7 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
             p[i] = s[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i] - m_new);
             ps += p[i];
         }
-        ps += __shfl_xor(ps, 32, 64);
+        ps += lane_xor(ps, 32);
         l_run = l_run * alpha + ps;
         m_run = m_new;
         if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {   // some lane's maximum moved

@@ -41,6 +41,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include "lanes.h"
 #include "stage_kernels.h"
 
 namespace stg {
@@ -70,7 +71,7 @@ __device__ __forceinline__ void unpack8(const uint4 &v, float f[8]) {
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    for (int o = 32; o >= 1; o >>= 1) v += lane_xor(v, o);
     return v;
 }
 

@@ -17,6 +17,7 @@
 // attention output (before O) and the SwiGLU of the gate/up output (before down).
 #include <hip/hip_runtime.h>
 
+#include "lanes.h"
 #include "stage_kernels.h"
 
 namespace stg {
@@ -281,7 +282,7 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, cons
     for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
     __shared__ float red[4];
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    for (int o = 32; o >= 1; o >>= 1) ss += lane_xor(ss, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
     __syncthreads();
     const float tot = ((red[0] + red[1]) + red[2]) + red[3];
