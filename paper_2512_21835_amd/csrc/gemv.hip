@@ -112,35 +112,70 @@ __device__ __forceinline__ void store_kv(void *pool, size_t e, float v, int kv_f
         static_cast<uint16_t *>(pool)[e] = to_bf16(v);
 }
 
-// RoPE + KV store of one (row i, row i + d/2) pair of head h for activation row m.  Heads below Hq
-// are queries (rotated, to out), the next Hkv keys (rotated, to the cache), the last Hkv values.
-__device__ __forceinline__ void rope_kv_epilogue(const GemvArgs &a, int u, int m, float x1, float x2) {
-    const int d = a.kv.head_dim, half = d / 2;
-    const int h = u / half, i = u % half;
-    const int row = a.row0 + m;
-    const int sidx = row / a.meta->rows_per_seq;
-    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
-    const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
-    float r1 = x1, r2 = x2;
-    if (h < hq + hkv) {
-        const float c = a.cos_t[(size_t)pos * half + i], s = a.sin_t[(size_t)pos * half + i];
-        r1 = x1 * c - x2 * s;
-        r2 = x1 * s + x2 * c;
+// Epilogue inputs that do not depend on the dot products: the residual (O and down projections),
+// or for a RoPE unit (row i, row i + d/2 of head h) the rotation at the row's position and the
+// unit's place in the KV cache.  The vector kernel loads them before its weight stream, so their
+// dependent round trips (row metadata, then tables) overlap it instead of following it.
+struct EpiIn {
+    float res = 0.f;
+    float c = 1.f, s = 0.f;
+    size_t kv_e = 0;
+};
+
+template <int MODE>
+__device__ __forceinline__ EpiIn epi_load(const GemvArgs &a, int u, int m) {
+    EpiIn e;
+    if (MODE == GEMV_PLAIN_RESIDUAL) {
+        e.res = a.res[m * a.out_ld + u];
+    } else if (MODE == GEMV_NORM_ROPE_KV) {
+        const int d = a.kv.head_dim, half = d / 2;
+        const int h = u / half, i = u % half;
+        const int row = a.row0 + m;
+        const int sidx = row / a.meta->rows_per_seq;
+        const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+        const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
+        if (h < hq + hkv) {
+            e.c = a.cos_t[(size_t)pos * half + i];
+            e.s = a.sin_t[(size_t)pos * half + i];
+        }
+        if (h >= hq) {
+            const int slot = a.meta->seq_slot[sidx];
+            const int block = a.kv.block_table[(size_t)slot * a.kv.max_blocks + pos / kBlockTokens];
+            const int kv = h < hq + hkv ? 0 : 1;
+            const int g = h - hq - kv * hkv;
+            e.kv_e = (((size_t)block * 2 + kv) * hkv + g) * kBlockTokens * d + (size_t)(pos % kBlockTokens) * d + i;
+        }
     }
-    if (h < hq) {
-        float *q = a.out + m * a.out_ld + h * d;
-        q[i] = r1;
-        q[i + half] = r2;
-        return;
+    return e;
+}
+
+// Finishes unit u of activation row m from its (scaled) dot products y0 and y1 (second row of the
+// unit: up projection, or row i + d/2): SwiGLU; residual add; or RoPE, then queries to `out`
+// and keys/values (heads Hq .. Hq + Hkv - 1, then the last Hkv) to the cache.
+template <int MODE>
+__device__ __forceinline__ void epi_store(const GemvArgs &a, const EpiIn &e, int u, int m, float y0, float y1) {
+    if (MODE == GEMV_PLAIN_RESIDUAL) {
+        a.out[m * a.out_ld + u] = e.res + y0;
+    } else if (MODE == GEMV_NORM_SWIGLU) {
+        a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * y1;
+    } else {
+        const int d = a.kv.head_dim, half = d / 2;
+        const int h = u / half, i = u % half;
+        const int hq = a.n_q_heads, hkv = a.kv.n_kv_heads;
+        float r1 = y0, r2 = y1;
+        if (h < hq + hkv) {
+            r1 = y0 * e.c - y1 * e.s;
+            r2 = y0 * e.s + y1 * e.c;
+        }
+        if (h < hq) {
+            float *q = a.out + m * a.out_ld + h * d;
+            q[i] = r1;
+            q[i + half] = r2;
+            return;
+        }
+        store_kv(a.kv.pool, e.kv_e, r1, a.kv_fp32);
+        store_kv(a.kv.pool, e.kv_e + half, r2, a.kv_fp32);
     }
-    const int slot = a.meta->seq_slot[sidx];
-    const int block = a.kv.block_table[(size_t)slot * a.kv.max_blocks + pos / kBlockTokens];
-    const int kv = h < hq + hkv ? 0 : 1;
-    const int g = h - hq - kv * hkv;
-    const size_t e = (((size_t)block * 2 + kv) * hkv + g) * kBlockTokens * d +
-                     (size_t)(pos % kBlockTokens) * d + i;
-    store_kv(a.kv.pool, e, r1, a.kv_fp32);
-    store_kv(a.kv.pool, e + half, r2, a.kv_fp32);
 }
 
 // One workgroup: units blockIdx.x * R .. + R - 1 for the launch's a.rows (<= M) activation rows.
@@ -173,6 +208,12 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 #pragma unroll
             for (int r = 0; r < R; ++r) acc[w][r][m] = 0.f;
     }
+
+    // epilogue inputs of lane r * M + m of wavefront 0 (unit unit0 + r, row m), ahead of the weights
+    const int er = lane / M, em = lane % M, eu = unit0 + er;
+    const bool epi_lane = wave == 0 && lane < R * M && eu < units && em < rows;
+    EpiIn epi;
+    if (epi_lane) epi = epi_load<MODE>(a, eu, em);
 
     for (int s0 = wave; s0 < steps; s0 += kWaves * U) {
         uint4 wv[U][NW][R];
@@ -237,21 +278,13 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     __syncthreads();
 
     // epilogue: lane r * M + m of wavefront 0 finishes unit unit0 + r of activation row m
-    if (wave != 0 || lane >= R * M) return;
-    const int r = lane / M, m = lane % M, u = unit0 + r;
-    if (u >= units || m >= rows) return;
+    if (!epi_lane) return;
     auto total = [&](int i) { return ((part[0][i] + part[1][i]) + part[2][i]) + part[3][i]; };
     float scale = 1.f;
-    if (kNorm) scale = 1.f / sqrtf(total(NW * R * M + m) / (float)K + a.eps);
-    const float y0 = total(r * M + m) * scale;
-    if (MODE == GEMV_NORM_ROPE_KV) {
-        rope_kv_epilogue(a, u, m, y0, total((R + r) * M + m) * scale);
-    } else if (MODE == GEMV_PLAIN_RESIDUAL) {
-        a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
-    } else {
-        const float up = total((R + r) * M + m) * scale;
-        a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
-    }
+    if (kNorm) scale = 1.f / sqrtf(total(NW * R * M + em) / (float)K + a.eps);
+    const float y0 = total(er * M + em) * scale;
+    const float y1 = NW == 2 ? total((R + er) * M + em) * scale : 0.f;
+    epi_store<MODE>(a, epi, eu, em, y0, y1);
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -393,15 +426,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
             continue;
         }
         const float scale = kNorm ? 1.f / sqrtf(row_ss(m) / (float)K + a.eps) : 1.f;
-        const float y0 = d[0][i] * scale;
-        if (MODE == GEMV_NORM_ROPE_KV) {
-            rope_kv_epilogue(a, u, m, y0, d[NW - 1][i] * scale);
-        } else if (MODE == GEMV_PLAIN_RESIDUAL) {
-            a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
-        } else {
-            const float up = d[NW - 1][i] * scale;
-            a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
-        }
+        epi_store<MODE>(a, epi_load<MODE>(a, u, m), u, m, d[0][i] * scale, d[NW - 1][i] * scale);
     }
 }
 
@@ -428,15 +453,7 @@ __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int split
         for (int sp = 1; sp < splits; ++sp) sq += a.split_ss[sp * kMfmaRows + m];
         scale = 1.f / sqrtf(sq / (float)a.K + a.eps);
     }
-    const float y0 = t[0] * scale;
-    if (MODE == GEMV_NORM_ROPE_KV) {
-        rope_kv_epilogue(a, u, m, y0, t[NW - 1] * scale);
-    } else if (MODE == GEMV_PLAIN_RESIDUAL) {
-        a.out[m * a.out_ld + u] = a.res[m * a.out_ld + u] + y0;
-    } else {
-        const float up = t[NW - 1] * scale;
-        a.out[m * a.out_ld + u] = y0 / (1.f + expf(-y0)) * up;
-    }
+    epi_store<MODE>(a, epi_load<MODE>(a, u, m), u, m, t[0] * scale, t[NW - 1] * scale);
 }
 
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
