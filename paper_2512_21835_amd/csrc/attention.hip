@@ -9,9 +9,12 @@
 //
 // Prefill (split_keys == 0): with a bf16 cache, attn_prefill_mfma runs the products on the matrix
 // cores (flash-attention tiling, below); with an fp32 cache (the parity mode), attn_kernel: one
-// workgroup per (row, KV head) walks all of the row's keys.  Decode (split_keys > 0, attn_decode_kernel): the context is cut into splits of
-// split_keys keys so that one token's attention still fills the GPU, and a second launch
-// (attn_merge_kernel) merges each row's splits in ascending order.
+// workgroup per (row, KV head) walks all of the row's keys.  Decode (split_keys > 0): the context is
+// cut into splits of split_keys keys so that one token's attention still fills the GPU, and a
+// second launch (attn_merge_kernel) merges each row's splits in ascending order.  With a bf16
+// cache and 128-wide heads the splits run on the matrix cores (attn_decode_mfma: the G query
+// heads of a KV head are the N dimension of S^T = K Q^T, then O = P V; with G = 8 the vector form
+// spends 16 multiply-adds per cached element and is bound by them); otherwise attn_decode_kernel.
 #include <hip/hip_runtime.h>
 
 #include "lanes.h"
@@ -399,6 +402,143 @@ __device__ __forceinline__ void split8(const float *x, bf16x8_t &hi, bf16x8_t &l
     }
 }
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+// Decode attention of one (64-key split, KV head g, row) on the matrix cores (bf16 KV, D = 128,
+// G <= 16): S^T = K Q^T with the K rows of the split's cache blocks as the A operand (one 16-key
+// block per wavefront) and Q as a bf16 hi/lo pair; softmax statistics per head from the MFMA
+// layout; O = P V with P (hi/lo) from LDS and V read transposed from an LDS tile.  Partial
+// outputs as attn_decode_task writes them.
+template <int G, int D>
+__global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
+    static_assert(D == 128 && G <= 16, "one 128-wide head, up to 16 query heads per KV head");
+    constexpr int VROW = D + 8;                     // V tile row stride in bf16 (272 bytes)
+    __shared__ uint16_t vs[kChunk][VROW];
+    __shared__ uint4 pf[2][2][64];                  // P A-fragments [key step][hi, lo][lane]
+    __shared__ float wm[4][16], wl[4][16];
+    const int split = blockIdx.x, g = blockIdx.y, row = blockIdx.z;
+    const int sidx = row / a.meta->rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+    const int slot = a.meta->seq_slot[sidx];
+    const int ctx = pos + 1, kbeg = split * a.split_keys;
+    if (kbeg >= ctx) return;
+    const int n = min(a.split_keys, ctx - kbeg);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int hq_total = a.n_q_heads, hkv = a.kv.n_kv_heads;
+    const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
+    const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
+    const uint16_t *pool = static_cast<const uint16_t *>(a.kv.pool);
+    const int l16 = lane & 15, lq = lane >> 4;
+    // K fragments: key 16 wave + l16 of the split (clamped into the split), d 32 s + 8 lq
+    const int kkey = kbeg + min(16 * wave + l16, n - 1);
+    const uint16_t *kp = pool + (size_t)table[kkey / kBlockTokens] * blk_stride +
+                         ((size_t)g * kBlockTokens + kkey % kBlockTokens) * D + 8 * lq;
+    uint4 kf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kf[s] = *reinterpret_cast<const uint4 *>(kp + 32 * s);
+    // V rows: instruction i, lane l: key 16 wave + 4 i + lq, d 8 l16
+    uint4 vr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int key = kbeg + min(16 * wave + 4 * i + lq, n - 1);
+        const uint16_t *vp = pool + (size_t)table[key / kBlockTokens] * blk_stride +
+                             ((size_t)(hkv + g) * kBlockTokens + key % kBlockTokens) * D + 8 * l16;
+        vr[i] = *reinterpret_cast<const uint4 *>(vp);
+    }
+    // Q^T fragments: head l16 (zero past G), d 32 s + 8 lq, scaled by 1/sqrt(d), hi/lo
+    const float scale = 1.f / sqrtf((float)D);
+    bf16x8_t qh[4], ql[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        float x[8];
+        if (l16 < G) {
+            const float *qp = a.q + (size_t)row * hq_total * D + (size_t)(g * G + l16) * D + 32 * s + 8 * lq;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = qp[j] * scale;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = 0.f;
+        }
+        split8(x, qh[s], ql[s]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<uint4 *>(&vs[16 * wave + 4 * i + lq][8 * l16]) = vr[i];
+    f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(kf[s]), qh[s], sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(kf[s]), ql[s], sc, 0, 0, 0);
+    }
+    // sc[i]: score of key 16 wave + 4 lq + i for head l16
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (16 * wave + 4 * lq + i >= n) sc[i] = -INFINITY;
+        mx = fmaxf(mx, sc[i]);
+    }
+    mx = fmaxf(mx, lane_xor(mx, 16));
+    mx = fmaxf(mx, lane_xor(mx, 32));
+    if (lane < 16) wm[wave][lane] = mx;
+    __syncthreads();
+    const float mh = fmaxf(fmaxf(wm[0][l16], wm[1][l16]), fmaxf(wm[2][l16], wm[3][l16]));
+    float p[4], ls = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        p[i] = sc[i] == -INFINITY ? 0.f : expf(sc[i] - mh);
+        ls += p[i];
+    }
+    ls += lane_xor(ls, 16);
+    ls += lane_xor(ls, 32);
+    if (lane < 16) wl[wave][lane] = ls;
+    // P fragment slot of key 16 wave + 4 lq + i: key step wave / 2, lane l16 + 16 (2 (wave % 2) + lq / 2),
+    // elements 4 (lq % 2) + i
+    {
+        uint16_t hb[4], lb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const __bf16 h = (__bf16)p[i];
+            const __bf16 l = (__bf16)(p[i] - (float)h);
+            hb[i] = __builtin_bit_cast(uint16_t, h);
+            lb[i] = __builtin_bit_cast(uint16_t, l);
+        }
+        const int L = l16 + 16 * (2 * (wave & 1) + (lq >> 1));
+        uint2 h2 = make_uint2(hb[0] | ((uint32_t)hb[1] << 16), hb[2] | ((uint32_t)hb[3] << 16));
+        uint2 l2 = make_uint2(lb[0] | ((uint32_t)lb[1] << 16), lb[2] | ((uint32_t)lb[3] << 16));
+        reinterpret_cast<uint2 *>(&pf[wave >> 1][0][L])[lq & 1] = h2;
+        reinterpret_cast<uint2 *>(&pf[wave >> 1][1][L])[lq & 1] = l2;
+    }
+    __syncthreads();
+    // O block (heads 0..15) x (d 32 wave + 16 nb .. + 15), K = the split's 64 keys in two steps
+    f32x4_t o[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8_t ph = as_bf(pf[ks][0][lane]), pl = as_bf(pf[ks][1][lane]);
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const int d = 32 * wave + 16 * nb + l16;
+            bf16x8_t vb;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) vb[j] = __builtin_bit_cast(__bf16, vs[32 * ks + 8 * lq + j][d]);
+            o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vb, o[nb], 0, 0, 0);
+            o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vb, o[nb], 0, 0, 0);
+        }
+    }
+    // o[nb][i]: head 4 lq + i, d 32 wave + 16 nb + l16
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = 4 * lq + i;
+        if (h >= G) continue;
+        const size_t pi = ((size_t)row * hq_total + g * G + h) * a.max_splits + split;
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) a.part_o[pi * D + 32 * wave + 16 * nb + l16] = o[nb][i];
+    }
+    if (wave == 0 && lane < G) {
+        const size_t pi = ((size_t)row * hq_total + g * G + lane) * a.max_splits + split;
+        a.part_ml[pi * 2 + 0] = fmaxf(fmaxf(wm[0][lane], wm[1][lane]), fmaxf(wm[2][lane], wm[3][lane]));
+        a.part_ml[pi * 2 + 1] = ((wl[0][lane] + wl[1][lane]) + wl[2][lane]) + wl[3][lane];
+    }
+}
+
 constexpr int KT = 32;                 // keys per tile of the prefill kernel
 constexpr int VROW = KT + 8;           // transposed V tile row stride in bf16 (padding)
 
@@ -585,6 +725,8 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
     dim3 grid(a.grid_splits, hkv, a.rows);
     if (a.kv_fp32)
         hipLaunchKernelGGL((attn_decode_kernel<G, D, true>), grid, dim3(256), 0, st, a);
+    else if constexpr (D == 128)
+        hipLaunchKernelGGL((attn_decode_mfma<G, D>), grid, dim3(256), 0, st, a);
     else
         hipLaunchKernelGGL((attn_decode_kernel<G, D, false>), grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
