@@ -1,6 +1,7 @@
 """GPU parity at the edges of the call sequence: a one-token prefill, prefills that continue a
-sequence (chunked prefill, prefill after K/V appended through stage_kv_append), and decode at the
-largest context the library supports (16384 positions, 256 attention splits)."""
+sequence (chunked prefill, prefill after K/V appended through stage_kv_append), decode at the
+largest context the library supports (16384 positions, 256 attention splits), and sequences of
+very different lengths decoded in one call."""
 import numpy as np
 import pytest
 
@@ -98,3 +99,56 @@ def test_decode_at_the_largest_context(kv_fp32):
     _gpu()
     plan = [("append", 16383), ("decode", 1)]
     _check(f"tiny max-context kv_fp32={kv_fp32}", _run(synth.TINY, plan, kv_fp32, 3, 16384))
+
+
+@pytest.mark.parametrize("kv_fp32", [False, True])
+def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32):
+    """8B-shaped stage: three sequences with 37, 200 and 1100 positions appended, decoded together
+    for two steps (3 rows per call: the matrix-core GEMVs; with the bf16 cache the matrix-core
+    attention).  The rows span 1, 4 and 18 attention splits, so workgroups of the shorter rows
+    exit early and every row's last split is ragged; each row is checked against the oracle."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from oracle.stage_oracle import OracleStage
+
+    shape = synth.LLAMA8B_STAGE
+    w = weights_of(shape)
+    L, hkv, d, H = shape.n_layers, shape.n_kv_heads, shape.head_dim, shape.hidden
+    hist = (37, 200, 1100)
+    orc = OracleStage(shape, w, kv_dtype="f32" if kv_fp32 else "bf16")
+    with compute_stream() as cs:
+        cfg = P.config_for(shape, max_microbatches=3, max_batch=1, max_context=1200, n_resident_max=L,
+                           kv_fp32=kv_fp32, compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        try:
+            for l in range(L):
+                P.stage_load_layer(h, l, w(l), 1)
+            for m, n in enumerate(hist):
+                seed = synth.seed_of(0xE3, m, n)
+                k = synth.normal_bf16(seed, (L, n, hkv, d))
+                v = synth.normal_bf16(seed + 1, (L, n, hkv, d))
+                if kv_fp32:
+                    kd = torch.from_numpy(synth.bf16_to_f32(k)).cuda()
+                    vd = torch.from_numpy(synth.bf16_to_f32(v)).cuda()
+                else:
+                    kd = torch.from_numpy(k.view(np.int16)).cuda()
+                    vd = torch.from_numpy(v.view(np.int16)).cuda()
+                P.stage_kv_append(h, m, 0, n, kd, vd)
+                orc.append_kv(f"s{m}", synth.bf16_to_f32(k).astype(np.float64), synth.bf16_to_f32(v).astype(np.float64))
+            for step in range(2):
+                x = synth.normal_f32(synth.seed_of(0xE4, step, 3), (3, H))
+                xd = torch.from_numpy(x).cuda().reshape(3, 1, H)
+                yd = torch.empty_like(xd)
+                P.stage_decode(h, [0, 1, 2], 1, xd, yd)
+                P.stage_sync(h)
+                got = yd.cpu().numpy().reshape(3, H)
+                want = orc.forward([(f"s{m}", x[m:m + 1]) for m in range(3)])
+                for m in range(3):
+                    cmp = compare(got[m:m + 1], want[m], x[m:m + 1], x[m:m + 1])
+                    print(f"\n[ragged kv_fp32={kv_fp32} step {step} row {m} ctx {hist[m] + step + 1}] {cmp}", flush=True)
+                    assert cmp["max_abs"] <= TOL_ABS and cmp["cos"] >= TOL_COS and cmp["cos_delta"] >= TOL_COS, (m, cmp)
+            for m, n in enumerate(hist):
+                assert P.stage_get_length(h, m, 0) == n + 2 == orc.length(f"s{m}")
+        finally:
+            P.stage_destroy(h)
