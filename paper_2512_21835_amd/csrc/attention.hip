@@ -602,10 +602,13 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
         }
     }
 
-    // tile loads: thread tid handles key (tid >> 3) ... 32 keys x (D / 8) chunks = 512 (D = 128)
+    // tile loads: 32 keys x (D / 8) 16-byte chunks (512 for D = 128), PER_T per thread; chunk
+    // c = tid + 256 i.  K: key c / (D / 8), d chunk c % (D / 8) (a wavefront reads 4 whole key
+    // rows).  V: key c % 32, d chunk c / 32, so that one transposed store instruction writes 32
+    // consecutive keys of one V^T row (the K mapping would put a wavefront's 16 rows 8 apart: on
+    // two LDS bank offsets)
     constexpr int CHUNKS = KT * D / 8;          // 16-byte chunks per K (or V) tile
     constexpr int PER_T = CHUNKS / 256;         // per thread (2 for D = 128, 1 for D = 64)
-    // chunk c = tid + 256 i (i < PER_T): key c / (D / 8), d chunk c % (D / 8)
     uint4 kr0, kr1, vr0, vr1;
 #define STG_GLOAD(TILE, I, KR, VR)                                                                        \
     do {                                                                                                  \
@@ -614,17 +617,21 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
         const size_t b_ = (size_t)table[kp_ / kBlockTokens] * blk_stride +                                \
                           (size_t)(kp_ % kBlockTokens) * D + (c_ % (D / 8)) * 8;                          \
         KR = *reinterpret_cast<const uint4 *>(pool + b_ + (size_t)g * kBlockTokens * D);                 \
-        VR = *reinterpret_cast<const uint4 *>(pool + b_ + (size_t)(hkv + g) * kBlockTokens * D);         \
+        const int vp_ = min((TILE) * KT + c_ % KT, n_keys - 1);                                           \
+        const size_t v_ = (size_t)table[vp_ / kBlockTokens] * blk_stride +                                \
+                          (size_t)(vp_ % kBlockTokens) * D + (c_ / KT) * 8;                               \
+        VR = *reinterpret_cast<const uint4 *>(pool + v_ + (size_t)(hkv + g) * kBlockTokens * D);         \
     } while (0)
 #define STG_LSTORE(I, KR, VR)                                                                             \
     do {                                                                                                  \
         const int c_ = tid + 256 * (I);                                                                   \
         const int key_ = c_ / (D / 8), d_ = (c_ % (D / 8)) * 8;                                           \
         *reinterpret_cast<uint4 *>(sk + key_ * KROW + d_) = KR;                                           \
+        const int vkey_ = c_ % KT, vd_ = (c_ / KT) * 8;                                                   \
         const uint32_t w_[4] = {VR.x, VR.y, VR.z, VR.w};                                                  \
         _Pragma("unroll") for (int j_ = 0; j_ < 4; ++j_) {                                                \
-            sv[(d_ + 2 * j_) * VROW + key_] = (uint16_t)(w_[j_] & 0xFFFFu);                               \
-            sv[(d_ + 2 * j_ + 1) * VROW + key_] = (uint16_t)(w_[j_] >> 16);                               \
+            sv[(vd_ + 2 * j_) * VROW + vkey_] = (uint16_t)(w_[j_] & 0xFFFFu);                             \
+            sv[(vd_ + 2 * j_ + 1) * VROW + vkey_] = (uint16_t)(w_[j_] >> 16);                             \
         }                                                                                                 \
     } while (0)
     auto gload = [&](int tile) {
