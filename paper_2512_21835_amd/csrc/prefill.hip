@@ -192,14 +192,20 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     // instruction q = wave * WB + i of an operand: lane l copies row 16 q + l / 4, k segment
     // (l % 4) ^ ((row >> 2) & 3) into slot 64 q + l; rows past M or N are clamped (in bounds),
     // their results are never stored
+    // SWIGLU: the tile's 32-row blocks alternate between Wg and Wu rows n0 / 2 + 32 (b / 2) ..
     const uint16_t *src_hi[WB], *src_lo[WB], *src_w[WB];
 #pragma unroll
     for (int i = 0; i < WB; ++i) {
         const int q = wave * WB + i, r = 16 * q + (lane >> 2), seg = (lane & 3) ^ ((r >> 2) & 3);
-        const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
+        const int m = min(m0 + r, M - 1);
         src_hi[i] = a.a_hi + (size_t)m * a.lda + 8 * seg;
         src_lo[i] = a.a_lo + (size_t)m * a.lda + 8 * seg;
-        src_w[i] = W + (size_t)n * K + 8 * seg;
+        if (MODE == GEMM_SWIGLU) {
+            const int b = r >> 5, n = min(n0 / 2 + 32 * (b >> 1) + (r & 31), N - 1);
+            src_w[i] = a.w[b & 1] + (size_t)n * K + 8 * seg;
+        } else {
+            src_w[i] = W + (size_t)min(n0 + r, N - 1) * K + 8 * seg;
+        }
     }
     auto issue = [&](int t) {
         const int st = t % S, k0 = t * BK;
@@ -253,6 +259,24 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
         }
     }
 
+    if (MODE == GEMM_SWIGLU) {   // blocks j (gate) and j + 1 (up) hold the same rows of h
+#pragma unroll
+        for (int i = 0; i < WB; ++i)
+#pragma unroll
+            for (int j = 0; j < WB; j += 2) {
+                const int n = n0 / 2 + 32 * ((wn * WB + j) >> 1) + (lane & 31);
+                if (n >= N) continue;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int m = m0 + wm * 32 * WB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    if (m >= M) continue;
+                    const float gt = acc[i][j][r], up = acc[i][j + 1][r];
+                    const size_t o = (size_t)m * a.ldo + n;
+                    split(gt / (1.f + expf(-gt)) * up, a.out_hi[o], a.out_lo[o]);
+                }
+            }
+        return;
+    }
     const int col_off = a.out_col[blockIdx.z];
 #pragma unroll
     for (int i = 0; i < WB; ++i)
@@ -317,11 +341,17 @@ int grid_for(size_t count) {
 
 template <int MODE>
 void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
-    dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, n_mats);
-    dim3 wide((a.M + 255) / 256, (a.N + 255) / 256, n_mats);
-    if (a.K % BK != 0)
-        hipLaunchKernelGGL(gemm_kernel<MODE>, grid, dim3(256), 0, st, a);
-    else if ((long)wide.x * wide.y * wide.z >= 256)   // the wide tiles still fill every compute unit
+    // SWIGLU tiles span the rows of both matrices: 2N virtual rows, one grid layer
+    const int nv = MODE == GEMM_SWIGLU ? 2 * a.N : a.N;
+    dim3 grid((a.M + BM - 1) / BM, (nv + BN - 1) / BN, n_mats);
+    dim3 wide((a.M + 255) / 256, (nv + 255) / 256, n_mats);
+    if constexpr (MODE != GEMM_SWIGLU) {
+        if (a.K % BK != 0) {
+            hipLaunchKernelGGL(gemm_kernel<MODE>, grid, dim3(256), 0, st, a);
+            return;
+        }
+    }
+    if ((long)wide.x * wide.y * wide.z >= 256)   // the wide tiles still fill every compute unit
         hipLaunchKernelGGL((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
     else
         hipLaunchKernelGGL((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);
@@ -332,8 +362,14 @@ void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) {
     if (a.M <= 0) return hipSuccess;
     // every variant runs the same MFMAs in the same order: the choice never changes a bit
-    if (mode == GEMM_RESIDUAL) launch_gemm_mode<GEMM_RESIDUAL>(a, n_mats, st);
-    else launch_gemm_mode<GEMM_STORE>(a, n_mats, st);
+    if (mode == GEMM_SWIGLU) {
+        if (a.K % BK != 0 || n_mats != 1 || !a.out_hi || !a.out_lo) return hipErrorInvalidValue;
+        launch_gemm_mode<GEMM_SWIGLU>(a, 1, st);
+    } else if (mode == GEMM_RESIDUAL) {
+        launch_gemm_mode<GEMM_RESIDUAL>(a, n_mats, st);
+    } else {
+        launch_gemm_mode<GEMM_STORE>(a, n_mats, st);
+    }
     return hipGetLastError();
 }
 

@@ -66,9 +66,11 @@ constexpr int kGemvMaxSplits = 8;
 hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start = nullptr,
                        hipEvent_t ev_stop = nullptr);
 
-enum GemmMode { GEMM_STORE = 0, GEMM_RESIDUAL = 1 };
+enum GemmMode { GEMM_STORE = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2 };
 
 // Prefill projection on the matrix cores: out[m, out_col + n] (+)= sum_k (a_hi + a_lo)[m, k] W[n, k].
+// SWIGLU (K a multiple of 32, n_mats = 1): w[0] = Wg, w[1] = Wu, both [N, K]; writes
+// h = silu(Wg a) * (Wu a) as a bf16 hi/lo pair out_hi/out_lo [M, N] with row stride ldo.
 struct GemmArgs {
     const uint16_t *a_hi, *a_lo;  // [M, K] bf16 pair of the fp32 activation, row stride lda
     long lda;
@@ -78,6 +80,7 @@ struct GemmArgs {
     long ldo;
     int out_col[2];               // output column offset of each matrix
     int M, N, K;
+    uint16_t *out_hi, *out_lo;    // SWIGLU output pair
 };
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st);
 // y = rmsnorm(x) * g as a bf16 hi/lo pair [rows, H].

@@ -697,14 +697,26 @@ int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int 
     gu.a_hi = s->ws_hi; gu.a_lo = s->ws_lo; gu.lda = H;
     gu.w[0] = base + s->off_wg / 2;
     gu.w[1] = base + s->off_wu / 2;
-    gu.out = s->ws_qkv; gu.ldo = 2 * (long)F;
-    gu.out_col[0] = 0; gu.out_col[1] = F;
     gu.M = rows; gu.N = F; gu.K = H;
-    HIP_TRY(launch_gemm(GEMM_STORE, gu, 2, s->cs));
-    HIP_TRY(launch_swiglu_split(s->ws_qkv, F, rows, s->ws_hi, s->ws_lo, s->cs));
+    const uint16_t *h_hi = s->ws_hi, *h_lo = s->ws_lo;   // h = silu(Wg y) * (Wu y) as a bf16 pair
+    if (H % 32 == 0) {
+        // SwiGLU and the hi/lo split in the GEMM's epilogue; the GEMM still reads the pair of y
+        // from ws_hi / ws_lo, so h goes to the (fp32-sized) QKV workspace
+        gu.out_hi = reinterpret_cast<uint16_t *>(s->ws_qkv);
+        gu.out_lo = gu.out_hi + (size_t)rows * F;
+        gu.ldo = F;
+        HIP_TRY(launch_gemm(GEMM_SWIGLU, gu, 1, s->cs));
+        h_hi = gu.out_hi;
+        h_lo = gu.out_lo;
+    } else {
+        gu.out = s->ws_qkv; gu.ldo = 2 * (long)F;
+        gu.out_col[0] = 0; gu.out_col[1] = F;
+        HIP_TRY(launch_gemm(GEMM_STORE, gu, 2, s->cs));
+        HIP_TRY(launch_swiglu_split(s->ws_qkv, F, rows, s->ws_hi, s->ws_lo, s->cs));
+    }
 
     GemmArgs dn{};
-    dn.a_hi = s->ws_hi; dn.a_lo = s->ws_lo; dn.lda = F;
+    dn.a_hi = h_hi; dn.a_lo = h_lo; dn.lda = F;
     dn.w[0] = base + s->off_wd / 2;
     dn.out = x_dst; dn.res = x_dst; dn.ldo = H;
     dn.M = rows; dn.N = H; dn.K = F;
