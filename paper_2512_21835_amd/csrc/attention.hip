@@ -11,7 +11,7 @@
 // cores (flash-attention tiling, below); with an fp32 cache (the parity mode), attn_kernel: one
 // workgroup per (row, KV head) walks all of the row's keys.  Decode (split_keys > 0): the context is
 // cut into splits of split_keys keys so that one token's attention still fills the GPU, and a
-// second launch (attn_merge_kernel) merges each row's splits in ascending order.  With a bf16
+// second launch (attn_merge_flat) merges each row's splits in ascending order.  With a bf16
 // cache and 128-wide heads the splits run on the matrix cores (attn_decode_mfma: the G query
 // heads of a KV head are the N dimension of S^T = K Q^T, then O = P V; with G = 8 the vector form
 // spends 16 multiply-adds per cached element and is bound by them); otherwise attn_decode_kernel.
@@ -51,56 +51,10 @@ struct DecodeSmem {
     float o[4][G][D];
 };
 
-template <int G>
-struct MergeSmem {
-    float cm[G][kMaxDecodeSplits], cl[G][kMaxDecodeSplits], den[G];
-};
-
-// Merges the nsp splits of (row, KV head g) in ascending order: the weight of split s for head h
-// is exp(m_s - max_s m_s) / sum_s(...) of its max m_s and sum l_s.
-template <int G, int D>
-__device__ __forceinline__ void attn_merge_group(const AttnArgs &a, int g, int row, int nsp, MergeSmem<G> &sm) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int hq_total = a.n_q_heads;
-    const size_t q_ld = (size_t)hq_total * D;
-    for (int i = tid; i < G * nsp; i += 256) {
-        const int h = i / nsp, sp = i % nsp;
-        const size_t pi = ((size_t)row * hq_total + g * G + h) * a.max_splits + sp;
-        sm.cm[h][sp] = a.part_ml[pi * 2 + 0];
-        sm.cl[h][sp] = a.part_ml[pi * 2 + 1];
-    }
-    __syncthreads();
-    for (int h = wave; h < G; h += 4) {
-        float mx = -INFINITY;
-        for (int sp = lane; sp < nsp; sp += 64) mx = fmaxf(mx, sm.cm[h][sp]);
-#pragma unroll
-        for (int o2 = 32; o2 >= 1; o2 >>= 1) mx = fmaxf(mx, lane_xor(mx, o2));
-        float den = 0.f;
-        for (int sp = lane; sp < nsp; sp += 64) {
-            const float w = expf(sm.cm[h][sp] - mx);
-            sm.cm[h][sp] = w;
-            den = fmaf(w, sm.cl[h][sp], den);
-        }
-#pragma unroll
-        for (int o2 = 32; o2 >= 1; o2 >>= 1) den += lane_xor(den, o2);
-        if (lane == 0) sm.den[h] = den;
-    }
-    __syncthreads();
-    for (int i = tid; i < G * D; i += 256) {
-        const int h = i / D, c = i % D;
-        const int hq = g * G + h;
-        const float *po = a.part_o + ((size_t)row * hq_total + hq) * a.max_splits * D + c;
-        float num = 0.f;
-#pragma unroll 8
-        for (int sp = 0; sp < nsp; ++sp) num = fmaf(sm.cm[h][sp], po[(size_t)sp * D], num);
-        a.out[row * q_ld + (size_t)hq * D + c] = num / sm.den[h];
-    }
-}
-
 // Decode: one workgroup per (key split, KV head, row); a split holds at most kChunk keys.  K and V
 // of the lane's keys are fetched together up front, scores are reduced across the D/8 lanes of a
 // key, the split's maximum and sum across the workgroup through LDS once, and the partial output
-// (unnormalised, with its max and sum) goes to global memory for attn_merge_group.
+// (unnormalised, with its max and sum) goes to global memory for attn_merge_flat.
 template <int G, int D, bool F32KV>
 __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, int g, int row,
                                                  DecodeSmem<G, D> &sm) {
@@ -375,14 +329,60 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnArgs a) {
     attn_decode_task<G, D, F32KV>(a, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
-// Merge of the decode splits as its own launch: one workgroup per (KV head, row).
-template <int G, int D>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-    __shared__ MergeSmem<G> sm;
-    const int g = blockIdx.x, row = blockIdx.y;
-    const int sidx = row / a.meta->rows_per_seq;
-    const int ctx = a.meta->pos0[sidx] + row % a.meta->rows_per_seq + 1;
-    attn_merge_group<G, D>(a, g, row, (ctx + a.split_keys - 1) / a.split_keys, sm);
+// Merge of the decode splits, one thread per output element (row, query head, column).  The
+// splits' (max, sum) pairs and partial outputs are loaded kMergeChunk at a time, all in flight
+// together and before the row's split count is known (addresses clamped to the call's longest
+// row, a.grid_splits): one round trip for contexts up to kMergeChunk splits.  Across chunks the
+// running sums are rescaled to the new maximum; within one chunk the weight of split s is
+// exp(m_s - max), and the numerator and denominator add the splits in ascending order.
+constexpr int kMergeChunk = 32;
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_flat(AttnArgs a) {
+    const int hq_total = a.n_q_heads;
+    const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= (size_t)a.rows * hq_total * D) return;
+    const int c = (int)(e % D);
+    const size_t rh = e / D;
+    const int hq = (int)(rh % hq_total), row = (int)(rh / hq_total);
+    const size_t pi0 = ((size_t)row * hq_total + hq) * a.max_splits;
+    const float2 *ml = reinterpret_cast<const float2 *>(a.part_ml) + pi0;
+    const float *po = a.part_o + pi0 * D + c;
+    const int lim = a.grid_splits;
+    float mx = -INFINITY, den = 0.f, num = 0.f;
+    int nsp = -1;
+    for (int s0 = 0; s0 < lim; s0 += kMergeChunk) {
+        float2 v[kMergeChunk];
+        float o[kMergeChunk];
+#pragma unroll
+        for (int j = 0; j < kMergeChunk; ++j) {
+            const int sp = min(s0 + j, lim - 1);
+            v[j] = ml[sp];
+            o[j] = po[(size_t)sp * D];
+        }
+        if (nsp < 0) {
+            const int sidx = row / a.meta->rows_per_seq;
+            const int ctx = a.meta->pos0[sidx] + row % a.meta->rows_per_seq + 1;
+            nsp = (ctx + a.split_keys - 1) / a.split_keys;
+        }
+        if (s0 >= nsp) break;
+        const int n = min(kMergeChunk, nsp - s0);
+        float m = mx;
+#pragma unroll
+        for (int j = 0; j < kMergeChunk; ++j)
+            if (j < n) m = fmaxf(m, v[j].x);
+        const float r = expf(mx - m);  // 0 on the first chunk (mx = -inf, m finite)
+        den *= r;
+        num *= r;
+#pragma unroll
+        for (int j = 0; j < kMergeChunk; ++j)
+            if (j < n) {
+                const float w = expf(v[j].x - m);
+                den = fmaf(w, v[j].y, den);
+                num = fmaf(w, o[j], num);
+            }
+        mx = m;
+    }
+    a.out[(size_t)row * hq_total * D + (size_t)hq * D + c] = num / den;
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -738,7 +738,8 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
         hipLaunchKernelGGL((attn_decode_kernel<G, D, false>), grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_merge_kernel<G, D>), dim3(hkv, a.rows), dim3(256), 0, st, a);
+    const size_t n_out = (size_t)a.rows * a.n_q_heads * D;
+    hipLaunchKernelGGL((attn_merge_flat<D>), dim3((unsigned)((n_out + 255) / 256)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
