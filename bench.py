@@ -32,8 +32,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, published
 # script (FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by what the counter reads for a
 # plain 1 GiB device copy in the same run).  Valid for the GEMV source it was taken on: with any
 # other source the field is reported as null.
-GATEUP_TRAFFIC = {"bytes": 235259143,
-                  "source_sha256": "d83c9e50a14affb6ec5c50003921a802f200e70aecaf56615f03a07b5a036f55"}
+GATEUP_TRAFFIC = {"bytes": 235259002,
+                  "source_sha256": "5c2175d0c0df5f063ed53b3c7620bb289003dcec94bc39241873b26e9a318f13"}
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
 
