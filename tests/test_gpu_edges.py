@@ -101,12 +101,15 @@ def test_decode_at_the_largest_context(kv_fp32):
     _check(f"tiny max-context kv_fp32={kv_fp32}", _run(synth.TINY, plan, kv_fp32, 3, 16384))
 
 
-@pytest.mark.parametrize("kv_fp32", [False, True])
-def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32):
-    """8B-shaped stage: three sequences with 37, 200 and 1100 positions appended, decoded together
-    for two steps (3 rows per call: the matrix-core GEMVs; with the bf16 cache the matrix-core
-    attention).  The rows span 1, 4 and 18 attention splits, so workgroups of the shorter rows
-    exit early and every row's last split is ragged; each row is checked against the oracle."""
+@pytest.mark.parametrize("kv_fp32,hist", [(False, (37, 200, 1100)), (True, (37, 200, 1100)),
+                                          (False, (2047, 2049, 4161))])
+def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32, hist):
+    """8B-shaped stage: three sequences with `hist` positions appended, decoded together for two
+    steps (3 rows per call: the matrix-core GEMVs; with the bf16 cache the matrix-core attention).
+    (37, 200, 1100): the rows span 1, 4 and 18 attention splits, so workgroups of the shorter rows
+    exit early and every row's last split is ragged.  (2047, 2049, 4161): 32 to 66 splits, so the
+    merge's 32-split load batches end exactly at, just past and well past a batch boundary.  Each
+    row is checked against the oracle."""
     _gpu()
     import torch
     import paper_2512_21835_amd as P
@@ -115,10 +118,9 @@ def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32):
     shape = synth.LLAMA8B_STAGE
     w = weights_of(shape)
     L, hkv, d, H = shape.n_layers, shape.n_kv_heads, shape.head_dim, shape.hidden
-    hist = (37, 200, 1100)
     orc = OracleStage(shape, w, kv_dtype="f32" if kv_fp32 else "bf16")
     with compute_stream() as cs:
-        cfg = P.config_for(shape, max_microbatches=3, max_batch=1, max_context=1200, n_resident_max=L,
+        cfg = P.config_for(shape, max_microbatches=3, max_batch=1, max_context=max(hist) + 64, n_resident_max=L,
                            kv_fp32=kv_fp32, compute_stream=cs.handle)
         h = P.stage_init(cfg)
         try:
