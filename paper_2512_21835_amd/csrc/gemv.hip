@@ -466,8 +466,18 @@ template <int MODE>
 void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int units = host_units(MODE, c), chunks = c.K / kChunkK;
     const int blocks = (units + 63) / 64;
-    int splits = (640 + blocks / 2) / blocks;
-    splits = max(1, min(splits, min(kGemvMaxSplits, chunks / 2)));
+    // about 640 workgroups, preferring a whole number per compute unit (256 of them) between 512
+    // and 768, larger on a tie (measured on the 8B- and 70B-shaped layers; 70B down projection at
+    // 16 rows: 5 splits 92.8 us, 6 splits 84.5 us)
+    const int max_splits = max(1, min(kGemvMaxSplits, chunks / 2));
+    int splits = max(1, min((640 + blocks / 2) / blocks, max_splits));
+    for (int sp = 1, best = 1 << 30; sp <= max_splits; ++sp) {
+        const int g = blocks * sp, d = abs(g - 640);
+        if (g % 256 == 0 && g >= 512 && g <= 768 && d <= best) {
+            best = d;
+            splits = sp;
+        }
+    }
     if (!c.split_part || !c.split_ss) splits = 1;
     if (splits == 1) {
         if (e0 || e1)
