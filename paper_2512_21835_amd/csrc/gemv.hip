@@ -510,14 +510,16 @@ void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 }
 
 // Units per workgroup and steps in flight, by mode and rows (swept on the 8B- and 70B-shaped
-// layers): one row: gate/up 4 units x 1 step, O and down 4 x 2, QKV 2 x 1 (2 x 2 on the larger
-// shape); two rows: O and down 4 x 1 (8 x 1 for the 70B down projection), QKV 4 x 1 (2 x 1 on the
-// larger shape); fewer as the rows multiply the registers.
+// layers): one row: gate/up 4 units x 1 step, O 4 x 2, down (K >= 2N) 8 x 1 (70B: 70.4 us against
+// 75.4 us for 4 x 2), QKV 2 x 1 (2 x 2 on the larger shape); two rows: O and down 4 x 1 (8 x 1 for
+// the 70B down projection), QKV 4 x 1 (2 x 1 on the larger shape); fewer as the rows multiply the
+// registers.
 template <int M, int MODE>
 void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const long work = (long)host_units(MODE, c) * c.K;
     if (MODE == GEMV_PLAIN_RESIDUAL) {
-        if (M == 1) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
+        if (M == 1 && c.K >= 2 * c.N) launch_one<M, 8, 1, MODE>(c, st, e0, e1);
+        else if (M == 1) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
         else if (M == 2 && work >= 200L * 1000 * 1000) launch_one<M, 8, 1, MODE>(c, st, e0, e1);
         else launch_one<M, 4, 1, MODE>(c, st, e0, e1);
     } else if (MODE == GEMV_NORM_SWIGLU) {
