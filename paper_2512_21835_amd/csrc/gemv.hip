@@ -478,6 +478,9 @@ void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
             splits = sp;
         }
     }
+    // QKV (two weight rows per unit, RoPE epilogue): at most 6 ranges (70B shape at 16 rows: 39.6 us
+    // against 42.4 us for 8; 8B: 19.4 against 20.7)
+    if (MODE == GEMV_NORM_ROPE_KV) splits = min(splits, 6);
     if (!c.split_part || !c.split_ss) splits = 1;
     if (splits == 1) {
         if (e0 || e1)
@@ -510,15 +513,15 @@ void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 }
 
 // Units per workgroup and steps in flight, by mode and rows (swept on the 8B- and 70B-shaped
-// layers): one row: gate/up 4 units x 1 step, O 4 x 2, down (K >= 2N) 8 x 1 (70B: 70.4 us against
-// 75.4 us for 4 x 2), QKV 2 x 1 (2 x 2 on the larger shape); two rows: O and down 4 x 1 (8 x 1 for
-// the 70B down projection), QKV 4 x 1 (2 x 1 on the larger shape); fewer as the rows multiply the
-// registers.
+// layers): one row: gate/up 4 units x 1 step, O 4 x 2, down (K >= 2N) and the 70B O projection
+// 8 x 1 (70B down: 70.4 us against 75.4 us for 4 x 2; O: 23.9 against 24.6), QKV 2 x 1 (2 x 2 on
+// the larger shape); two rows: O and down 4 x 1 (8 x 1 for the 70B down projection), QKV 4 x 1
+// (2 x 1 on the larger shape); fewer as the rows multiply the registers.
 template <int M, int MODE>
 void launch_rows(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const long work = (long)host_units(MODE, c) * c.K;
     if (MODE == GEMV_PLAIN_RESIDUAL) {
-        if (M == 1 && c.K >= 2 * c.N) launch_one<M, 8, 1, MODE>(c, st, e0, e1);
+        if (M == 1 && (c.K >= 2 * c.N || work >= 60L * 1000 * 1000)) launch_one<M, 8, 1, MODE>(c, st, e0, e1);
         else if (M == 1) launch_one<M, 4, 2, MODE>(c, st, e0, e1);
         else if (M == 2 && work >= 200L * 1000 * 1000) launch_one<M, 8, 1, MODE>(c, st, e0, e1);
         else launch_one<M, 4, 1, MODE>(c, st, e0, e1);
