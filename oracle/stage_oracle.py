@@ -193,6 +193,37 @@ def decoder_layer(x: torch.Tensor, w: LayerWeights, cache: LayerCache, shape, kv
     return x + h @ w.wd.T
 
 
+def layer_kv(x: torch.Tensor, w: LayerWeights, shape, kv_round) -> Tuple[torch.Tensor, torch.Tensor]:
+    """The K and V that one decoder layer stores for the rows x [T, H] of a new sequence
+    (positions 0..T-1), as the cache holds them: [T, Hkv, d] each (the first steps of
+    decoder_layer)."""
+    t = x.shape[0]
+    hkv, d = shape.n_kv_heads, shape.head_dim
+    positions = torch.arange(t)
+    y = rms_norm(x, w.g1, shape.rms_eps)
+    k = rope((y @ w.wk.T).reshape(t, hkv, d), positions, shape.rope_theta)
+    v = (y @ w.wv.T).reshape(t, hkv, d)
+    return kv_round(k), kv_round(v)
+
+
+def decoder_layer_rows(x: torch.Tensor, w: LayerWeights, shape, rows: Sequence[int],
+                       k_all: torch.Tensor, v_all: torch.Tensor) -> torch.Tensor:
+    """Outputs of the listed rows of one decoder layer over x [T, H] of a new sequence (positions
+    0..T-1), attending over the stored K, V [T, Hkv, d] given: decoder_layer restricted to those
+    rows.  Every step but attention acts on each row alone, and attention reads only its own
+    query row and the stored K and V, so the restriction changes nothing for the rows kept."""
+    hq, d = shape.n_q_heads, shape.head_dim
+    idx = torch.as_tensor(list(rows), dtype=torch.long)
+    xr = x[idx]
+    y = rms_norm(xr, w.g1, shape.rms_eps)
+    q = rope((y @ w.wq.T).reshape(len(idx), hq, d), idx, shape.rope_theta)
+    o = gqa_attention(q, k_all, v_all, idx)
+    xr = xr + o @ w.wo.T
+    y2 = rms_norm(xr, w.g2, shape.rms_eps)
+    h = silu(y2 @ w.wg.T) * (y2 @ w.wu.T)
+    return xr + h @ w.wd.T
+
+
 # ---------------------------------------------------------------------------
 # the stage
 # ---------------------------------------------------------------------------

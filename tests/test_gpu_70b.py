@@ -205,3 +205,64 @@ def test_70b_offloaded_decode_at_context_2048_equals_resident():
     off = _full_context_round(4, 1, 2048, 4, False, 7, sampled)
     assert np.array_equal(res[0], off[0])
     _check_sampled("70b ctx2048 offloaded", off[0], off[3], _oracle_full_context(off[2], off[3], False))
+
+
+def test_70b_prefill_2048_one_layer_sampled_rows():
+    """Full-size prefill of one 70B-shaped layer (T = 2048 tokens of one sequence, the production
+    bf16 cache, 256 x 256 GEMM tiles, matrix-core prefill attention with 8 query heads per KV
+    head): at least 99% of the stored K/V elements equal the oracle's bf16 K/V bit for bit, and every
+    one is within a bf16 step of it or within 2^-8 of the tensor's rms (a value that comes out of
+    cancellation carries the fp32 rounding of its larger terms), and sampled output rows -- at
+    the 16-token block, 16-row query block and 32-key tile edges and at the ends -- computed by the
+    oracle over the GPU's own stored K/V are within max|d| <= 2e-2, cosine >= 0.9995."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from oracle import stage_oracle as O
+
+    one = dataclasses.replace(SHAPE, n_layers=1)
+    T, H, hkv, d = 2048, SHAPE.hidden, SHAPE.n_kv_heads, SHAPE.head_dim
+    bits = weights_of(SHAPE)(0)
+    x = synth.normal_f32(synth.seed_of(0xC7, 2048), (T, H))
+    with compute_stream() as cs:
+        cfg = P.config_for(one, max_microbatches=1, max_batch=1, max_context=T, n_resident_max=1,
+                           compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        try:
+            P.stage_load_layer(h, 0, bits, 1)
+            x_in = torch.from_numpy(x).cuda().reshape(1, 1, T, H)
+            x_out = torch.empty_like(x_in)
+            P.stage_prefill(h, [0], 1, T, x_in, x_out)
+            k_dev = torch.empty(1, T, hkv, d, dtype=torch.int16, device="cuda")
+            v_dev = torch.empty_like(k_dev)
+            P.stage_kv_export_tail(h, 0, 0, T, k_dev, v_dev, False)
+            P.stage_sync(h)
+            got = x_out.cpu().numpy().reshape(T, H)
+            k_gpu = k_dev.cpu().numpy().view(np.uint16)[0]
+            v_gpu = v_dev.cpu().numpy().view(np.uint16)[0]
+        finally:
+            P.stage_destroy(h)
+
+    w = O.LayerWeights(bits)
+    x64 = torch.as_tensor(x, dtype=torch.float64)
+    k_orc, v_orc = O.layer_kv(x64, w, one, O.round_to_bf16)
+    for name, g_bits, o in (("K", k_gpu, k_orc), ("V", v_gpu, v_orc)):
+        g = synth.bf16_to_f32(g_bits).astype(np.float64)
+        o = o.numpy()
+        rms = float(np.sqrt(np.mean(o * o)))
+        bound = np.abs(o) * 2.0 ** -7 + rms * 2.0 ** -8      # one bf16 step at |o|, plus cancellation
+        diff = np.abs(g - o)
+        equal = float(np.mean(diff == 0))
+        worst = int(np.argmax(diff / bound))
+        print(f"\n[70b prefill 2048 stored {name}] bit-equal {equal:.6f}, rms {rms:.4g}, max |d| {float(diff.max()):.3g}, "
+              f"worst |d| / bound {float(diff.flat[worst] / bound.flat[worst]):.3g} at |o| {abs(float(o.flat[worst])):.3g}",
+              flush=True)
+        assert np.all(diff <= bound), name
+        assert equal >= 0.99, (name, equal)
+    rows = [0, 1, 15, 16, 17, 31, 32, 127, 128, 1000, 1023, 1024, 1535, 2032, 2046, 2047]
+    k_t = torch.as_tensor(synth.bf16_to_f32(k_gpu), dtype=torch.float64)
+    v_t = torch.as_tensor(synth.bf16_to_f32(v_gpu), dtype=torch.float64)
+    want = O.decoder_layer_rows(x64, w, one, rows, k_t, v_t).numpy()
+    m = compare(got[rows], want, x[rows], x[rows])
+    _report("70b prefill 2048 one layer, sampled rows over the GPU's K/V", m)
+    assert m["max_abs"] <= TOL_ABS and m["cos"] >= TOL_COS and m["cos_delta"] >= TOL_COS, m

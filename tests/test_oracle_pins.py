@@ -256,6 +256,23 @@ def test_layer_matches_loop_brute_force_f32_kv():
     assert st.shape is TINY3
 
 
+def test_layer_rows_match_loop_brute_force():
+    """layer_kv (the K/V a layer stores) and decoder_layer_rows (the layer restricted to some rows,
+    attending over given stored K/V) against the pure-Python loop brute force of the whole layer."""
+    bits = tiny_bits(24)
+    x = rand(9, 8, seed=25).numpy()
+    kc, vc = [], []
+    ref = brute_layer(x, bits, 0, kc, vc, TINY3, f32_round_scalar)
+    w = O.LayerWeights(bits)
+    xt = torch.as_tensor(x)
+    k, v = O.layer_kv(xt, w, TINY3, O.round_to_f32)
+    np.testing.assert_allclose(k.reshape(9, 4).numpy(), np.array(kc), rtol=0, atol=0)
+    np.testing.assert_allclose(v.reshape(9, 4).numpy(), np.array(vc), rtol=0, atol=0)
+    rows = [0, 3, 8]
+    got = O.decoder_layer_rows(xt, w, TINY3, rows, k, v).numpy()
+    np.testing.assert_allclose(got, ref[rows], rtol=1e-12, atol=1e-13)
+
+
 def test_layer_with_zero_output_projections_is_identity():
     bits = tiny_bits(22)
     bits["wo"] = np.zeros_like(bits["wo"])
