@@ -36,7 +36,8 @@ Pins (tests/test_oracle_pins.py): RMSNorm unit RMS before the gain; RoPE closed
 form on unit vectors, pair-norm preservation and relative-position invariance;
 softmax rows sum to 1; one key returns V; zero queries give the causal mean of
 V; GQA with Hkv = Hq equals per-head brute force; decode step t equals row t of
-one prefill; a pure-Python loop brute force of the tiny layer.
+one prefill; a pure-Python loop brute force of the tiny layer, which also pins
+layer_kv and decoder_layer_rows.
 """
 from __future__ import annotations
 
