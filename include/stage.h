@@ -57,6 +57,7 @@ typedef enum {
 #define STAGE_MAX_THRESHOLDS 32
 #define STAGE_MAX_SEQS_PER_CALL 64
 #define STAGE_MAX_CONTEXT 16384
+#define STAGE_MAX_LANES 4
 
 /* Residency of a layer (stage_load_layer, stage_get_residency).  "MHA-only offloading" in the
    sense of Section III-D: the MHA block streams, the MLP block stays resident. */
@@ -125,6 +126,13 @@ typedef struct {
        buffer per parked sequence, 2 * n_layers * kv_park_tokens * n_kv_heads * head_dim KV
        elements, which the parking kernels read and write directly over the host link. */
     int32_t kv_park_tokens;
+    /* Decode lanes (0 or 1: one).  Lane l (1 <= l < n_lanes) has its own stream and workspaces, so
+       decode calls on different lanes (stage_decode_lane) run concurrently: the interleaved
+       schedule's independent micro-batches, whose weight streams then fill each other's
+       latency-bound phases.  lane_streams[l]: lane l's hipStream_t (NULL = the library creates
+       one); lane 0 is compute_stream. */
+    int32_t n_lanes;
+    void *lane_streams[STAGE_MAX_LANES];
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
@@ -173,6 +181,19 @@ int stage_prefill(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, int3
    must already hold at least one token (ESTATE otherwise). */
 int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
                  float *x_out);
+
+/* stage_decode on decode lane `lane` (0 <= lane < n_lanes; lane 0 is stage_decode itself): the
+   call runs on the lane's stream with its workspaces, so calls on different lanes may overlap on
+   the GPU.  A call waits (on the GPU) for the last call on another lane that touched any of its
+   sequences, so a sequence's steps stay in order whichever lanes they use (stage_prefill and
+   stage_decode order themselves the same way); the caller orders the call's inputs and outputs
+   with the lane's stream.  The KV entry points (append, export, park, unpark, reset) and
+   stage_load_layer synchronize all lanes first.  ESTATE for lanes >= 1 when a layer would be staged through the
+   slots (lanes need resident or zero-copy layers), a residency schedule is pending, or a
+   sequence of the call has a parked KV tail; EINVAL for a lane out of range; otherwise as
+   stage_decode.  Outputs are identical to stage_decode's. */
+int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                      float *x_out);
 
 /* Appends n_tokens positions of already-rotated K and V to sequence (mb, b) without compute:
    the concatenation of a received KV-cache tail in the KV transfer protocol (Section III-E,

@@ -93,6 +93,20 @@ struct ParkEvent {
 
 }  // namespace
 
+// What a decode lane owns: its stream and the workspaces and row metadata of its calls.  The call
+// in flight swaps its lane's state into the stage's own fields (lane 0's live there), so the
+// kernels of a call on lane l use lane l's buffers and stream.
+struct LaneState {
+    hipStream_t cs = nullptr;
+    bool own_cs = false;
+    CallMeta *d_meta = nullptr;
+    size_t ws_rows = 0, part_rows = 0;
+    float *ws_qkv = nullptr, *ws_q = nullptr, *ws_attn = nullptr, *ws_h = nullptr;
+    uint16_t *ws_hi = nullptr, *ws_lo = nullptr;
+    float *ws_part_o = nullptr, *ws_part_ml = nullptr;
+    float *ws_split = nullptr, *ws_split_ss = nullptr;
+};
+
 struct stage {
     stage_config cfg{};
     int H = 0, Hq = 0, Hkv = 0, D = 0, F = 0, L = 0;
@@ -147,6 +161,12 @@ struct stage {
     // per KV block: the event of the park whose copies may still read it, until it is taken again
     std::vector<std::shared_ptr<ParkEvent>> block_park;
     long long bytes_parked = 0, bytes_unparked = 0;
+
+    // decode lanes 1 .. n_lanes-1 (index 0 unused: lane 0's state is the stage's own); per sequence,
+    // the stream of the last call that touched it and an event recorded at that call's end
+    std::vector<LaneState> lanes;
+    std::vector<hipStream_t> seq_stream;
+    std::vector<hipEvent_t> seq_ev;
 
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
     long long bytes_direct = 0;   // offloaded-block bytes read in place by zero-copy kernels
@@ -211,6 +231,46 @@ hipEvent_t pooled_event(stage *s) {
 int sync_all(stage *s) {
     HIP_TRY(hipStreamSynchronize(s->cs));
     HIP_TRY(hipStreamSynchronize(s->xs));
+    for (size_t l = 1; l < s->lanes.size(); ++l) HIP_TRY(hipStreamSynchronize(s->lanes[l].cs));
+    return STAGE_OK;
+}
+
+// Exchanges the stage's call state (lane 0's, or the lane swapped in) with lanes[l]'s.
+void swap_lane(stage *s, int l) {
+    LaneState &o = s->lanes[l];
+    std::swap(s->cs, o.cs);
+    std::swap(s->d_meta, o.d_meta);
+    std::swap(s->ws_rows, o.ws_rows);
+    std::swap(s->part_rows, o.part_rows);
+    std::swap(s->ws_qkv, o.ws_qkv);
+    std::swap(s->ws_q, o.ws_q);
+    std::swap(s->ws_attn, o.ws_attn);
+    std::swap(s->ws_h, o.ws_h);
+    std::swap(s->ws_hi, o.ws_hi);
+    std::swap(s->ws_lo, o.ws_lo);
+    std::swap(s->ws_part_o, o.ws_part_o);
+    std::swap(s->ws_part_ml, o.ws_part_ml);
+    std::swap(s->ws_split, o.ws_split);
+    std::swap(s->ws_split_ss, o.ws_split_ss);
+}
+
+// With several lanes: the call about to run on s->cs waits for the last call on another stream
+// that touched any of its sequences (KV cache order); after it, its sequences remember s->cs.
+int order_sequences(stage *s, const std::vector<int> &slots) {
+    if (s->lanes.size() < 2) return STAGE_OK;
+    for (int sl : slots)
+        if (s->seq_stream[sl] && s->seq_stream[sl] != s->cs) HIP_TRY(hipStreamWaitEvent(s->cs, s->seq_ev[sl], 0));
+    return STAGE_OK;
+}
+// Entry points that change state outside the call sequence wait for every lane's work first.
+int join_lanes(stage *s) { return s->lanes.size() > 1 ? sync_all(s) : STAGE_OK; }
+
+int mark_sequences(stage *s, const std::vector<int> &slots) {
+    if (s->lanes.size() < 2) return STAGE_OK;
+    for (int sl : slots) {
+        HIP_TRY(hipEventRecord(s->seq_ev[sl], s->cs));
+        s->seq_stream[sl] = s->cs;
+    }
     return STAGE_OK;
 }
 
@@ -909,6 +969,8 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         }
     }
 
+    rc = order_sequences(s, slots);
+    if (rc) return rc;
     rc = prepare_sequences(s, slots);
     if (rc) return rc;
 
@@ -1015,7 +1077,7 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         if (rc) return rc;
         s->recs.push_back(call_rec);
     }
-    return STAGE_OK;
+    return mark_sequences(s, slots);
 }
 
 }  // namespace
@@ -1062,7 +1124,8 @@ int stage_init(const stage_config *cfg, stage **out) {
                         c.n_resident_max <= c.n_layers && c.n_stream_slots >= 0 && c.n_stream_slots <= 64 &&
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
                         (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1) &&
-                        c.kv_park_tokens >= 0 && c.kv_park_tokens <= c.max_context;
+                        c.kv_park_tokens >= 0 && c.kv_park_tokens <= c.max_context && c.n_lanes >= 0 &&
+                        c.n_lanes <= STAGE_MAX_LANES;
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     if (c.plan_mode != 0 && c.plan_mode != 1) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i) {
@@ -1138,6 +1201,26 @@ int stage_init(const stage_config *cfg, stage **out) {
     s->block_park.assign(s->n_blocks, nullptr);
     if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
         return cleanup(STAGE_EHIP);
+    if (c.n_lanes > 1) {
+        s->lanes.resize(c.n_lanes);
+        for (int l = 1; l < c.n_lanes; ++l) {
+            LaneState &ln = s->lanes[l];
+            if (c.lane_streams[l]) ln.cs = static_cast<hipStream_t>(c.lane_streams[l]);
+            else if (hipStreamCreateWithFlags(&ln.cs, hipStreamNonBlocking) == hipSuccess) ln.own_cs = true;
+            else return cleanup(STAGE_EHIP);
+            if (hipMalloc(&ln.d_meta, sizeof(CallMeta)) != hipSuccess ||
+                hipMalloc(&ln.ws_split, sizeof(float) * kGemvMaxSplits * 2 * 16 *
+                                            std::max<size_t>(std::max<size_t>(s->qkv_rows / 2, s->H), s->F)) != hipSuccess ||
+                hipMalloc(&ln.ws_split_ss, sizeof(float) * kGemvMaxSplits * 16) != hipSuccess) {
+                (void)hipGetLastError();
+                return cleanup(STAGE_ENOMEM);
+            }
+        }
+        s->seq_stream.assign(s->n_seq_slots, nullptr);
+        s->seq_ev.assign(s->n_seq_slots, nullptr);
+        for (hipEvent_t &e : s->seq_ev)
+            if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return cleanup(STAGE_EHIP);
+    }
     // RoPE tables: angle = p * theta^(-2i/d), evaluated in double, cos/sin rounded to fp32.
     const int half = s->D / 2;
     std::vector<float> ct((size_t)c.max_context * half), st((size_t)c.max_context * half);
@@ -1159,6 +1242,8 @@ int stage_destroy(stage *s) {
     DeviceGuard dg(s->cfg.device);
     if (s->cs) (void)hipStreamSynchronize(s->cs);
     if (s->xs) (void)hipStreamSynchronize(s->xs);
+    for (LaneState &ln : s->lanes)
+        if (ln.cs) (void)hipStreamSynchronize(ln.cs);
     for (Layer &l : s->layers)
         for (Block &k : l.blk) free_block(k);
     for (void *p : s->slots) (void)hipFree(p);
@@ -1183,6 +1268,15 @@ int stage_destroy(stage *s) {
         if (p) (void)hipFree(p);
     if (s->own_cs && s->cs) (void)hipStreamDestroy(s->cs);
     if (s->own_xs && s->xs) (void)hipStreamDestroy(s->xs);
+    for (LaneState &ln : s->lanes) {
+        for (void *p : {(void *)ln.d_meta, (void *)ln.ws_qkv, (void *)ln.ws_q, (void *)ln.ws_attn, (void *)ln.ws_h,
+                        (void *)ln.ws_hi, (void *)ln.ws_lo, (void *)ln.ws_part_o, (void *)ln.ws_part_ml,
+                        (void *)ln.ws_split, (void *)ln.ws_split_ss})
+            if (p) (void)hipFree(p);
+        if (ln.own_cs && ln.cs) (void)hipStreamDestroy(ln.cs);
+    }
+    for (hipEvent_t e : s->seq_ev)
+        if (e) (void)hipEventDestroy(e);
     delete s;
     return STAGE_OK;
 }
@@ -1251,6 +1345,39 @@ int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const
     return run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
 }
 
+int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                      float *x_out) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (lane == 0) return stage_decode(s, n_mb, mb_ids, B, x_in, x_out);
+    if (lane < 0 || lane >= (int)s->lanes.size())
+        return s->fail(STAGE_EINVAL, "lane %d out of range (%d lanes)", lane, std::max<int>(1, (int)s->lanes.size()));
+    // a lane call stages no layer through the slots and moves no parked tail: both use the copy
+    // stream and slot events that order the stage's calls one after another
+    const bool direct = s->cfg.zero_copy;
+    for (int l = 0; l < s->L; ++l)
+        if (s->layers[l].streams() && !direct)
+            return s->fail(STAGE_ESTATE, "layer %d streams through the slots: lanes need resident (or zero-copy) layers", l);
+    if (s->cfg.plan_mode || s->thresholds_applied < s->cfg.n_thresholds)
+        return s->fail(STAGE_ESTATE, "a residency schedule is pending: lanes need a fixed residency");
+    if (n_mb >= 1 && n_mb <= s->cfg.max_microbatches && mb_ids && B >= 1 && B <= s->cfg.max_batch)
+        for (int k = 0; k < n_mb; ++k)
+            for (int b = 0; b < B; ++b) {
+                const int mb = mb_ids[k];
+                if (mb < 0 || mb >= s->cfg.max_microbatches) continue;  // run_call reports it
+                const int sl = seq_slot(s, mb, b);
+                if (s->parked[sl] || s->ready_pending[sl])
+                    return s->fail(STAGE_ESTATE, "micro-batch %d has a parked KV tail: decode it on lane 0", mb);
+            }
+    swap_lane(s, lane);
+    const int32_t timing = s->cfg.timing;
+    s->cfg.timing = 0;  // events of lane calls are not recorded
+    const int rc = run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
+    s->cfg.timing = timing;
+    swap_lane(s, lane);
+    return rc;
+}
+
 int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k, const void *v) {
     if (!s) return STAGE_EINVAL;
     s->err.clear();
@@ -1262,6 +1389,7 @@ int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const voi
     if (blocks_needed(s, slot, s->parked[slot] + n_tokens) > (int)s->free_blocks.size())
         return s->fail(STAGE_ENOMEM, "KV pool exhausted");
     DeviceGuard dg(s->cfg.device);
+    if (int rc_ = join_lanes(s)) return rc_;
     const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
     const size_t bytes = (size_t)s->L * n_tokens * s->Hkv * s->D * elem;
     const bool dev = is_device_ptr(k) && is_device_ptr(v);
@@ -1298,6 +1426,7 @@ int stage_kv_export_tail(stage *s, int32_t mb, int32_t b, int32_t n_tokens, void
     if (blocks_needed(s, slot, s->parked[slot]) > (int)s->free_blocks.size())
         return s->fail(STAGE_ENOMEM, "KV pool exhausted");
     DeviceGuard dg(s->cfg.device);
+    if (int rc_ = join_lanes(s)) return rc_;
     const size_t elem = s->cfg.kv_fp32 ? 4 : 2;
     const size_t bytes = (size_t)s->L * n_tokens * s->Hkv * s->D * elem;
     const bool dev = is_device_ptr(k) && is_device_ptr(v);
@@ -1362,6 +1491,7 @@ int stage_kv_park(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t n_token
         }
     }
     DeviceGuard dg(c.device);
+    if (int rc_ = join_lanes(s)) return rc_;
     for (int sl : slots) {
         if (s->park_host[sl]) continue;
         void *hbuf = nullptr, *dbuf = nullptr;
@@ -1427,6 +1557,7 @@ int stage_kv_unpark(stage *s, int32_t n_mb, const int32_t *mb_ids) {
     if (need > (int)s->free_blocks.size())
         return s->fail(STAGE_ENOMEM, "KV pool exhausted (%d blocks needed, %d free)", need, (int)s->free_blocks.size());
     DeviceGuard dg(c.device);
+    if (int rc_ = join_lanes(s)) return rc_;
     for (int sl : slots) {
         int rc = enqueue_unpark(s, sl);
         if (rc) return rc;

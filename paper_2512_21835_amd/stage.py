@@ -25,6 +25,7 @@ STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE = 0
 STAGE_MAX_THRESHOLDS = 32
 STAGE_MAX_SEQS_PER_CALL = 64
 STAGE_MAX_CONTEXT = 16384
+STAGE_MAX_LANES = 4
 STAGE_TIME_CALLS = 1
 STAGE_TIME_GATEUP = 2
 STAGE_TIME_LAYERS = 4
@@ -32,7 +33,7 @@ STAGE_RES_OFFLOADED, STAGE_RES_RESIDENT, STAGE_RES_MHA_OFFLOADED, STAGE_RES_MLP_
 
 EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",
-    "stage_decode", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
+    "stage_decode", "stage_decode_lane", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
     "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
     "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate", "stage_kv_park", "stage_kv_unpark",
@@ -54,6 +55,7 @@ class StageConfig(ctypes.Structure):
         ("timing", c_int32), ("zero_copy", c_int32),
         ("plan_mode", c_int32), ("plan_alpha", c_int32 * STAGE_MAX_THRESHOLDS),
         ("plan_beta", c_int32 * STAGE_MAX_THRESHOLDS), ("kv_park_tokens", c_int32),
+        ("n_lanes", c_int32), ("lane_streams", c_void_p * STAGE_MAX_LANES),
     ]
 
 
@@ -115,6 +117,7 @@ def lib():
         "stage_load_layer": (c_int32, [c_void_p, c_int32, POINTER(StageLayerWeights), c_int32]),
         "stage_prefill": (c_int32, [c_void_p, c_int32, ip, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_decode": (c_int32, [c_void_p, c_int32, ip, c_int32, c_void_p, c_void_p]),
+        "stage_decode_lane": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, c_void_p, c_void_p]),
         "stage_kv_append": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_export_tail": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_int32]),
         "stage_reset_sequence": (c_int32, [c_void_p, c_int32, c_int32]),
@@ -204,6 +207,10 @@ def stage_prefill(h, mb_ids: Sequence[int], B: int, T: int, x_in: torch.Tensor, 
 
 def stage_decode(h, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
     _check(lib().stage_decode(h, len(mb_ids), _ids(mb_ids), B, _ptr(x_in), _ptr(x_out)), h)
+
+
+def stage_decode_lane(h, lane: int, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
+    _check(lib().stage_decode_lane(h, lane, len(mb_ids), _ids(mb_ids), B, _ptr(x_in), _ptr(x_out)), h)
 
 
 def stage_kv_append(h, mb: int, b: int, n_tokens: int, k, v) -> None:
@@ -322,9 +329,11 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
                n_stream_slots: int = 2, kv_fp32: bool = False, thresholds: Sequence[int] = (),
                kv_pool_blocks: int = 0, device: int = 0, compute_stream=None, copy_stream=None,
                timing: int = 0, zero_copy: bool = False,
-               plan: Optional[Sequence[Tuple[int, int, int]]] = None, kv_park_tokens: int = 0) -> StageConfig:
+               plan: Optional[Sequence[Tuple[int, int, int]]] = None, kv_park_tokens: int = 0,
+               n_lanes: int = 1, lane_streams: Optional[Sequence] = None) -> StageConfig:
     """A StageConfig for a stage shape (any object with the StageShape fields).  ``plan``:
-    planner steps [(tokens, alpha, beta)] (plan_mode 1), instead of ``thresholds``."""
+    planner steps [(tokens, alpha, beta)] (plan_mode 1), instead of ``thresholds``.
+    ``n_lanes`` decode lanes; ``lane_streams[l]``: lane l's stream handle (None: the library's)."""
     cfg = stage_config_default()
     cfg.n_layers, cfg.hidden = shape.n_layers, shape.hidden
     cfg.n_q_heads, cfg.n_kv_heads = shape.n_q_heads, shape.n_kv_heads
@@ -352,4 +361,7 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
     cfg.timing = timing
     cfg.zero_copy = int(bool(zero_copy))
     cfg.kv_park_tokens = kv_park_tokens
+    cfg.n_lanes = n_lanes
+    for l, st in enumerate(lane_streams or ()):
+        cfg.lane_streams[l] = st
     return cfg

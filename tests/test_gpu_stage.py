@@ -318,6 +318,89 @@ def test_vector_and_matrix_engines_agree(wl, prefill, steps):
         assert m["max_abs"] <= TOL_ABS and m["cos"] >= 0.99999, m
 
 
+LLAMA8B_4x1 = synth.Workload("llama8b_4x1", 106, synth.LLAMA8B_STAGE, n_mb=4, batch=1, prefill=70,
+                             decode_steps=3)
+
+
+@pytest.mark.parametrize("alternate", [False, True])
+def test_decode_lanes_equal_one_lane_bitwise(alternate):
+    """Round-robin decode of four micro-batches on two decode lanes (each call on its lane's stream,
+    inputs ordered on that stream) gives the rows of the one-lane run bit for bit.  alternate: a
+    micro-batch's steps switch lanes every step, so each step must wait for the previous one on
+    the other lane."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from tests.harness import _inputs, compute_stream
+
+    wl = LLAMA8B_4x1
+    sc = Scenario(wl, prefill=70, decode_steps=3)
+    ref = run_gpu(sc)
+    shape, H = wl.shape, wl.shape.hidden
+    weights = weights_of(shape)
+    with compute_stream() as cs:
+        lane1 = torch.cuda.Stream()
+        streams = [cs.stream, lane1]
+        cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=1, max_context=sc.ctx(),
+                           n_resident_max=shape.n_layers, compute_stream=cs.handle, n_lanes=2,
+                           lane_streams=[None, lane1.cuda_stream])
+        h = P.stage_init(cfg)
+        outs, keep = [], []
+        try:
+            for l in range(shape.n_layers):
+                P.stage_load_layer(h, l, weights(l), 1)
+            for kind, mbs, step in sc.call_plan():
+                x = _inputs(sc, kind, mbs, step, {})
+                m = mbs[0]
+                lane = 0 if kind == "prefill" else ((m + step) % 2 if alternate else m % 2)
+                with torch.cuda.stream(streams[lane]):
+                    x_in = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+                    x_out = torch.empty_like(x_in)
+                if kind == "prefill":
+                    P.stage_prefill(h, mbs, 1, x.shape[2], x_in, x_out)
+                else:
+                    P.stage_decode_lane(h, lane, mbs, 1, x_in, x_out)
+                outs.append(x_out)
+                keep.append(x_in)
+            P.stage_sync(h)
+            got = [o.cpu().numpy() for o in outs]
+            with pytest.raises(P.StageError):
+                P.stage_decode_lane(h, 2, [0], 1, keep[-1], outs[-1])   # only lanes 0 and 1
+        finally:
+            P.stage_destroy(h)
+    assert len(got) == len(ref.outputs)
+    for c, (a, b) in enumerate(zip(got, ref.outputs)):
+        assert np.array_equal(a, b), f"call {c} differs"
+
+
+def test_decode_lanes_refuse_streamed_layers():
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from tests.harness import compute_stream
+
+    shape = synth.TINY
+    weights = weights_of(shape)
+    with compute_stream() as cs:
+        cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=32, n_resident_max=1,
+                           compute_stream=cs.handle, n_lanes=2)
+        h = P.stage_init(cfg)
+        try:
+            P.stage_load_layer(h, 0, weights(0), 1)
+            P.stage_load_layer(h, 1, weights(1), 0)                     # streamed through the slots
+            x = torch.zeros(1, 1, 4, shape.hidden, device="cuda")
+            y = torch.empty_like(x)
+            P.stage_prefill(h, [0], 1, 4, x, y)
+            xd, yd = x[:, :, 0].contiguous(), torch.empty_like(x[:, :, 0]).contiguous()
+            with pytest.raises(P.StageError) as e:
+                P.stage_decode_lane(h, 1, [0], 1, xd, yd)
+            assert e.value.code == P.STAGE_ESTATE
+            P.stage_decode_lane(h, 0, [0], 1, xd, yd)                   # lane 0 streams as before
+            P.stage_sync(h)
+        finally:
+            P.stage_destroy(h)
+
+
 def test_threshold_demotions_follow_schedule_and_stay_lossless():
     _gpu()
     ths = (39, 40, 41)   # prefill 37: decode rounds 2, 3, 4 each demote one layer (2 layers: 2 demotions)
