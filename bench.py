@@ -236,10 +236,11 @@ def prefill_report(shape, T: int, seconds: float):
 
 def resident70b_leg(rounds: int, ctx: int = 2048):
     """The 70B-shaped stage with all 16 layers resident and sequences at context `ctx` (filled
-    through stage_kv_append with random K/V), decoded three ways: 4 micro-batches of batch 1
+    through stage_kv_append with random K/V), decoded four ways: 4 micro-batches of batch 1
     round-robin, one micro-batch per call (every call streams all weights for one token); the same
-    4 in one call (weights read once for 4 tokens, vector kernels); 8 micro-batches of batch 2 in
-    one call (16 rows, matrix cores).  Weights are random bf16 generated on the device (timing only;
+    round robin on two decode lanes (micro-batch m on lane m mod 2, so two calls overlap); the same
+    4 in one call (weights read once for 4 tokens); 8 micro-batches of batch 2 in one call (16 rows,
+    matrix cores).  Weights are random bf16 generated on the device (timing only;
     parity of these configurations is covered by the tests)."""
     import torch
 
@@ -250,8 +251,10 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
     dev = torch.device("cuda", 0)
     cstream = torch.cuda.current_stream(dev)
     L = shape.n_layers
-    cfg = P.config_for(shape, max_microbatches=8, max_batch=2, max_context=ctx + 3 * (rounds + 1) + 8,
-                       n_resident_max=L, compute_stream=cstream.cuda_stream)
+    lane1 = torch.cuda.Stream(dev)
+    cfg = P.config_for(shape, max_microbatches=8, max_batch=2, max_context=ctx + 4 * (rounds + 1) + 8,
+                       n_resident_max=L, compute_stream=cstream.cuda_stream, n_lanes=2,
+                       lane_streams=[None, lane1.cuda_stream])
     h = P.stage_init(cfg)
     gen = torch.Generator(device=dev).manual_seed(2513)
     res = {}
@@ -271,30 +274,33 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
         x = torch.randn(8, 2, shape.hidden, generator=gen, device=dev)
         y = torch.empty_like(x)
         layer = shape.layer_bytes()
-        modes = {"round_robin": ([[m] for m in range(4)], 1), "4_in_one_call": ([list(range(4))], 1),
-                 "16_rows_in_one_call": ([list(range(8))], 2)}
-        for mode, (groups, B) in modes.items():
+        modes = {"round_robin": ([[m] for m in range(4)], 1, 1), "round_robin_2_lanes": ([[m] for m in range(4)], 1, 2),
+                 "4_in_one_call": ([list(range(4))], 1, 1), "16_rows_in_one_call": ([list(range(8))], 2, 1)}
+        for mode, (groups, B, lanes) in modes.items():
             xs = [x[g[0]: g[0] + len(g), :B].contiguous() for g in groups]
             ys = [torch.empty_like(xi) for xi in xs]
-            for g, xi, yi in zip(groups, xs, ys):   # warm-up round
-                P.stage_decode(h, g, B, xi, yi)
+            torch.cuda.synchronize()
+
+            def one_round():
+                for i, (g, xi, yi) in enumerate(zip(groups, xs, ys)):
+                    P.stage_decode_lane(h, i % lanes, g, B, xi, yi)
+            one_round()                              # warm-up round
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             for _ in range(rounds):
-                for g, xi, yi in zip(groups, xs, ys):
-                    P.stage_decode(h, g, B, xi, yi)
+                one_round()
             torch.cuda.synchronize()
             dt = time.perf_counter() - t0
             calls = rounds * len(groups)
             tokens = rounds * sum(len(g) for g in groups) * B
-            hbm = calls * L * layer + tokens * L * (ctx + 3 * rounds) * 2 * shape.kv_dim * 2
+            hbm = calls * L * layer + tokens * L * (ctx + 4 * rounds) * 2 * shape.kv_dim * 2
             res[mode] = {"tokens_per_s": tokens / dt, "ms_per_call": dt * 1e3 / calls,
                          "hbm_GBs": hbm / dt / 1e9, "hbm_frac": hbm / dt / 1e9 / HBM_PEAK_GBS}
     finally:
         P.stage_destroy(h)
     res["workload"] = (f"llama70b_resident decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672) resident, "
-                       f"context {ctx}; 4 micro-batches of batch 1 (round robin or one call), or 8 of batch 2 "
-                       f"in one call")
+                       f"context {ctx}; 4 micro-batches of batch 1 (round robin on one or two decode lanes, or "
+                       f"one call), or 8 of batch 2 in one call")
     return res
 
 
