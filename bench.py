@@ -492,7 +492,8 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
     through stage_kv_append with random K/V), decoded round robin, one micro-batch per call.
     Without parking, then with it: before micro-batch m's call the next micro-batch's tail is
     requested back (stage_kv_unpark, copy stream), and after the call m's last n_park tokens
-    move out (stage_kv_park), for each n_park in `n_parks`.  Reports the call time each way, the
+    move out (stage_kv_park), for each n_park in `n_parks`.  Also without parking on two decode
+    lanes (micro-batch m on lane m mod 2: two calls overlap).  Reports the call time each way, the
     bytes each call moves over the host link, and the KV blocks held in HBM after the last call."""
     import torch
 
@@ -516,11 +517,12 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
            .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)] for _ in range(n_mb)]
     x = torch.randn(n_mb, 1, 1, shape.hidden, generator=gen, device=dev)
     res = {}
-    for n_park in (0,) + tuple(n_parks):
+    lane1 = torch.cuda.Stream(dev)
+    for n_park, lanes in [(0, 1), (0, 2)] + [(n, 1) for n in n_parks]:
         park = n_park > 0
         cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + rounds + 8, n_resident_max=L,
                            compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream,
-                           kv_park_tokens=n_park)
+                           kv_park_tokens=n_park, n_lanes=lanes, lane_streams=[None, lane1.cuda_stream])
         h = P.stage_init(cfg)
         try:
             for l in range(L):
@@ -532,7 +534,7 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
             def step(m):
                 if park:
                     P.stage_kv_unpark(h, [(m + 1) % n_mb])
-                P.stage_decode(h, [m], 1, x[m], ys[m])
+                P.stage_decode_lane(h, m % lanes, [m], 1, x[m], ys[m])
                 if park:
                     P.stage_kv_park(h, [m], n_park)
 
@@ -547,15 +549,16 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
             st = P.stage_get_stats(h)
         finally:
             P.stage_destroy(h)
-        key = f"park_{n_park}" if park else "plain"
+        key = f"park_{n_park}" if park else ("plain" if lanes == 1 else f"plain_{lanes}_lanes")
         res[key] = {
             "ms_per_call": dt * 1e3 / (rounds * n_mb), "kv_blocks_in_hbm": st["kv_blocks"] - st["kv_blocks_free"],
             "host_link_MB_per_call": (st["bytes_parked"] + st["bytes_unparked"]) / 1e6 / ((rounds + 1) * n_mb)}
         if park:
             res[key]["overhead"] = res[key]["ms_per_call"] / res["plain"]["ms_per_call"] - 1
     res["workload"] = (f"llama8b_stage decode: 8 layers resident, 4 micro-batches of batch 1 at context {ctx}, round "
-                       f"robin one per call; parking moves the last n tokens of each micro-batch between its calls "
-                       f"and fetches the next one's back ahead of its call")
+                       f"robin one per call (plain_2_lanes: micro-batch m on decode lane m mod 2); parking moves the "
+                       f"last n tokens of each micro-batch between its calls and fetches the next one's back ahead "
+                       f"of its call")
     return res
 
 
