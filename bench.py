@@ -238,7 +238,7 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
     """The 70B-shaped stage with all 16 layers resident and sequences at context `ctx` (filled
     through stage_kv_append with random K/V), decoded four ways: 4 micro-batches of batch 1
     round-robin, one micro-batch per call (every call streams all weights for one token); the same
-    round robin on two decode lanes (micro-batch m on lane m mod 2, so two calls overlap); the same
+    round robin on two and on four decode lanes (micro-batch m on lane m mod n: calls overlap); the same
     4 in one call (weights read once for 4 tokens); 8 micro-batches of batch 2 in one call (16 rows,
     matrix cores).  Weights are random bf16 generated on the device (timing only;
     parity of these configurations is covered by the tests)."""
@@ -251,10 +251,9 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
     dev = torch.device("cuda", 0)
     cstream = torch.cuda.current_stream(dev)
     L = shape.n_layers
-    lane1 = torch.cuda.Stream(dev)
-    cfg = P.config_for(shape, max_microbatches=8, max_batch=2, max_context=ctx + 4 * (rounds + 1) + 8,
-                       n_resident_max=L, compute_stream=cstream.cuda_stream, n_lanes=2,
-                       lane_streams=[None, lane1.cuda_stream])
+    lane_streams = [None] + [torch.cuda.Stream(dev).cuda_stream for _ in range(3)]
+    cfg = P.config_for(shape, max_microbatches=8, max_batch=2, max_context=ctx + 5 * (rounds + 1) + 8,
+                       n_resident_max=L, compute_stream=cstream.cuda_stream, n_lanes=4, lane_streams=lane_streams)
     h = P.stage_init(cfg)
     gen = torch.Generator(device=dev).manual_seed(2513)
     res = {}
@@ -275,6 +274,7 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
         y = torch.empty_like(x)
         layer = shape.layer_bytes()
         modes = {"round_robin": ([[m] for m in range(4)], 1, 1), "round_robin_2_lanes": ([[m] for m in range(4)], 1, 2),
+                 "round_robin_4_lanes": ([[m] for m in range(4)], 1, 4),
                  "4_in_one_call": ([list(range(4))], 1, 1), "16_rows_in_one_call": ([list(range(8))], 2, 1)}
         for mode, (groups, B, lanes) in modes.items():
             xs = [x[g[0]: g[0] + len(g), :B].contiguous() for g in groups]
@@ -293,13 +293,13 @@ def resident70b_leg(rounds: int, ctx: int = 2048):
             dt = time.perf_counter() - t0
             calls = rounds * len(groups)
             tokens = rounds * sum(len(g) for g in groups) * B
-            hbm = calls * L * layer + tokens * L * (ctx + 4 * rounds) * 2 * shape.kv_dim * 2
+            hbm = calls * L * layer + tokens * L * (ctx + 5 * rounds) * 2 * shape.kv_dim * 2
             res[mode] = {"tokens_per_s": tokens / dt, "ms_per_call": dt * 1e3 / calls,
                          "hbm_GBs": hbm / dt / 1e9, "hbm_frac": hbm / dt / 1e9 / HBM_PEAK_GBS}
     finally:
         P.stage_destroy(h)
     res["workload"] = (f"llama70b_resident decode: 16 layers (hidden 8192, 64/8 heads, ffn 28672) resident, "
-                       f"context {ctx}; 4 micro-batches of batch 1 (round robin on one or two decode lanes, or "
+                       f"context {ctx}; 4 micro-batches of batch 1 (round robin on one, two or four decode lanes, or "
                        f"one call), or 8 of batch 2 in one call")
     return res
 
@@ -493,7 +493,7 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
     Without parking, then with it: before micro-batch m's call the next micro-batch's tail is
     requested back (stage_kv_unpark, copy stream), and after the call m's last n_park tokens
     move out (stage_kv_park), for each n_park in `n_parks`.  Also without parking on two decode
-    lanes (micro-batch m on lane m mod 2: two calls overlap).  Reports the call time each way, the
+    lanes and on four (micro-batch m on lane m mod n: calls overlap).  Reports the call time each way, the
     bytes each call moves over the host link, and the KV blocks held in HBM after the last call."""
     import torch
 
@@ -517,12 +517,12 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
            .to(torch.bfloat16).view(torch.int16).contiguous() for _ in range(2)] for _ in range(n_mb)]
     x = torch.randn(n_mb, 1, 1, shape.hidden, generator=gen, device=dev)
     res = {}
-    lane1 = torch.cuda.Stream(dev)
-    for n_park, lanes in [(0, 1), (0, 2)] + [(n, 1) for n in n_parks]:
+    lane_streams = [None] + [torch.cuda.Stream(dev).cuda_stream for _ in range(3)]
+    for n_park, lanes in [(0, 1), (0, 2), (0, 4)] + [(n, 1) for n in n_parks]:
         park = n_park > 0
         cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + rounds + 8, n_resident_max=L,
                            compute_stream=cstream.cuda_stream, copy_stream=xstream.cuda_stream,
-                           kv_park_tokens=n_park, n_lanes=lanes, lane_streams=[None, lane1.cuda_stream])
+                           kv_park_tokens=n_park, n_lanes=lanes, lane_streams=lane_streams)
         h = P.stage_init(cfg)
         try:
             for l in range(L):
@@ -556,7 +556,7 @@ def parking_leg(rounds: int = 32, ctx: int = 1024, n_parks=(128, 512)):
         if park:
             res[key]["overhead"] = res[key]["ms_per_call"] / res["plain"]["ms_per_call"] - 1
     res["workload"] = (f"llama8b_stage decode: 8 layers resident, 4 micro-batches of batch 1 at context {ctx}, round "
-                       f"robin one per call (plain_2_lanes: micro-batch m on decode lane m mod 2); parking moves the "
+                       f"robin one per call (plain_n_lanes: micro-batch m on decode lane m mod n); parking moves the "
                        f"last n tokens of each micro-batch between its calls and fetches the next one's back ahead "
                        f"of its call")
     return res
