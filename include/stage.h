@@ -195,6 +195,12 @@ int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const
 int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
                       float *x_out);
 
+/* stage_prefill on lane `lane`, with the same rules as stage_decode_lane: a new request's prefill
+   can overlap other micro-batches' decode calls (its matrix-core GEMMs against their weight
+   streams).  Outputs are identical to stage_prefill's. */
+int stage_prefill_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, int32_t T,
+                       const float *x_in, float *x_out);
+
 /* Appends n_tokens positions of already-rotated K and V to sequence (mb, b) without compute:
    the concatenation of a received KV-cache tail in the KV transfer protocol (Section III-E,
    Alg. 2).  k, v: [n_layers][n_tokens][n_kv_heads][head_dim] in the KV element type (bf16 bits

@@ -1345,16 +1345,15 @@ int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const
     return run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
 }
 
-int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
-                      float *x_out) {
-    if (!s) return STAGE_EINVAL;
-    s->err.clear();
-    if (lane == 0) return stage_decode(s, n_mb, mb_ids, B, x_in, x_out);
+namespace {
+// A call on decode lane `lane` >= 1 (stage_decode_lane, stage_prefill_lane).
+int run_lane_call(stage *s, int lane, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
+                  bool decode) {
     if (lane < 0 || lane >= (int)s->lanes.size())
         return s->fail(STAGE_EINVAL, "lane %d out of range (%d lanes)", lane, std::max<int>(1, (int)s->lanes.size()));
     // a lane call stages no layer through the slots and moves no parked tail: both use the copy
     // stream and slot events that order the stage's calls one after another
-    const bool direct = s->cfg.zero_copy;
+    const bool direct = s->cfg.zero_copy && T == 1;
     for (int l = 0; l < s->L; ++l)
         if (s->layers[l].streams() && !direct)
             return s->fail(STAGE_ESTATE, "layer %d streams through the slots: lanes need resident (or zero-copy) layers", l);
@@ -1367,15 +1366,32 @@ int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_id
                 if (mb < 0 || mb >= s->cfg.max_microbatches) continue;  // run_call reports it
                 const int sl = seq_slot(s, mb, b);
                 if (s->parked[sl] || s->ready_pending[sl])
-                    return s->fail(STAGE_ESTATE, "micro-batch %d has a parked KV tail: decode it on lane 0", mb);
+                    return s->fail(STAGE_ESTATE, "micro-batch %d has a parked KV tail: run it on lane 0", mb);
             }
     swap_lane(s, lane);
     const int32_t timing = s->cfg.timing;
     s->cfg.timing = 0;  // events of lane calls are not recorded
-    const int rc = run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
+    const int rc = run_call(s, n_mb, mb_ids, B, T, x_in, x_out, decode);
     s->cfg.timing = timing;
     swap_lane(s, lane);
     return rc;
+}
+}  // namespace
+
+int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                      float *x_out) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (lane == 0) return stage_decode(s, n_mb, mb_ids, B, x_in, x_out);
+    return run_lane_call(s, lane, n_mb, mb_ids, B, 1, x_in, x_out, true);
+}
+
+int stage_prefill_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, int32_t T,
+                       const float *x_in, float *x_out) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    if (lane == 0) return stage_prefill(s, n_mb, mb_ids, B, T, x_in, x_out);
+    return run_lane_call(s, lane, n_mb, mb_ids, B, T, x_in, x_out, false);
 }
 
 int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k, const void *v) {

@@ -33,7 +33,7 @@ STAGE_RES_OFFLOADED, STAGE_RES_RESIDENT, STAGE_RES_MHA_OFFLOADED, STAGE_RES_MLP_
 
 EXPORTED = (
     "stage_config_default", "stage_init", "stage_destroy", "stage_load_layer", "stage_prefill",
-    "stage_decode", "stage_decode_lane", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
+    "stage_decode", "stage_decode_lane", "stage_prefill_lane", "stage_kv_append", "stage_kv_export_tail", "stage_reset_sequence", "stage_sync",
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
     "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
     "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate", "stage_kv_park", "stage_kv_unpark",
@@ -118,6 +118,7 @@ def lib():
         "stage_prefill": (c_int32, [c_void_p, c_int32, ip, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_decode": (c_int32, [c_void_p, c_int32, ip, c_int32, c_void_p, c_void_p]),
         "stage_decode_lane": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, c_void_p, c_void_p]),
+        "stage_prefill_lane": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_append": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_export_tail": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_int32]),
         "stage_reset_sequence": (c_int32, [c_void_p, c_int32, c_int32]),
@@ -211,6 +212,11 @@ def stage_decode(h, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: to
 
 def stage_decode_lane(h, lane: int, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
     _check(lib().stage_decode_lane(h, lane, len(mb_ids), _ids(mb_ids), B, _ptr(x_in), _ptr(x_out)), h)
+
+
+def stage_prefill_lane(h, lane: int, mb_ids: Sequence[int], B: int, T: int, x_in: torch.Tensor,
+                       x_out: torch.Tensor) -> None:
+    _check(lib().stage_prefill_lane(h, lane, len(mb_ids), _ids(mb_ids), B, T, _ptr(x_in), _ptr(x_out)), h)
 
 
 def stage_kv_append(h, mb: int, b: int, n_tokens: int, k, v) -> None:

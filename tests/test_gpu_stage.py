@@ -323,11 +323,11 @@ LLAMA8B_4x1 = synth.Workload("llama8b_4x1", 106, synth.LLAMA8B_STAGE, n_mb=4, ba
 
 
 @pytest.mark.parametrize("alternate", [False, True])
-def test_decode_lanes_equal_one_lane_bitwise(alternate):
-    """Round-robin decode of four micro-batches on two decode lanes (each call on its lane's stream,
-    inputs ordered on that stream) gives the rows of the one-lane run bit for bit.  alternate: a
-    micro-batch's steps switch lanes every step, so each step must wait for the previous one on
-    the other lane."""
+def test_lanes_equal_one_lane_bitwise(alternate):
+    """Prefills and round-robin decode of four micro-batches on two lanes (micro-batch m's prefill
+    on lane m mod 2; each call on its lane's stream, inputs ordered on that stream) give the rows
+    of the one-lane run bit for bit.  alternate: a micro-batch's decode steps switch lanes every
+    step, so each step must wait for the previous one on the other lane."""
     _gpu()
     import torch
     import paper_2512_21835_amd as P
@@ -352,12 +352,12 @@ def test_decode_lanes_equal_one_lane_bitwise(alternate):
             for kind, mbs, step in sc.call_plan():
                 x = _inputs(sc, kind, mbs, step, {})
                 m = mbs[0]
-                lane = 0 if kind == "prefill" else ((m + step) % 2 if alternate else m % 2)
+                lane = m % 2 if kind == "prefill" else ((m + step) % 2 if alternate else m % 2)
                 with torch.cuda.stream(streams[lane]):
                     x_in = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
                     x_out = torch.empty_like(x_in)
                 if kind == "prefill":
-                    P.stage_prefill(h, mbs, 1, x.shape[2], x_in, x_out)
+                    P.stage_prefill_lane(h, lane, mbs, 1, x.shape[2], x_in, x_out)
                 else:
                     P.stage_decode_lane(h, lane, mbs, 1, x_in, x_out)
                 outs.append(x_out)
