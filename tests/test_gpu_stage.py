@@ -282,14 +282,18 @@ def test_planner_reloads_blocks_when_the_cache_shrinks():
 
 
 def _one_vs_all(wl, prefill, steps):
+    """(rows of the round robin, rows of the one-call run, their common inputs) per call group."""
     a = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="one"))
     b = run_gpu(Scenario(wl, prefill=prefill, decode_steps=steps, calls="all"))
     H, n = wl.shape.hidden, wl.n_mb
-    pairs = [(np.concatenate([o.reshape(-1, H) for o in a.outputs[:n]]), b.outputs[0].reshape(-1, H))]
+    rows = lambda outs: np.concatenate([o.reshape(-1, H) for o in outs])
+    out = [(rows(a.outputs[:n]), b.outputs[0].reshape(-1, H), rows(a.inputs[:n]))]
     for s in range(steps):
-        pairs.append((np.concatenate([o.reshape(-1, H) for o in a.outputs[n + n * s: 2 * n + n * s]]),
-                      b.outputs[1 + s].reshape(-1, H)))
-    return pairs
+        grp = slice(n + n * s, 2 * n + n * s)
+        out.append((rows(a.outputs[grp]), b.outputs[1 + s].reshape(-1, H), rows(a.inputs[grp])))
+    for one, all_, x in out:
+        assert x.shape == one.shape == all_.shape
+    return out
 
 
 @pytest.mark.parametrize("wl,prefill,steps", [(TINY_2x1, 37, 4), (LLAMA8B_2x8, 24, 3)])
@@ -298,7 +302,7 @@ def test_round_robin_equals_all_in_one_call_bitwise(wl, prefill, steps):
     decode projections run on the same engine: 1 vs 2 rows per call on the vector kernels (tiny
     shape), 8 vs 16 rows per call on the matrix cores (8B shape)."""
     _gpu()
-    for one, all_ in _one_vs_all(wl, prefill, steps):
+    for one, all_, _ in _one_vs_all(wl, prefill, steps):
         assert np.array_equal(one, all_)
 
 
@@ -309,13 +313,14 @@ def test_vector_and_matrix_engines_agree(wl, prefill, steps):
     parity bound (the engines round differently, and a decode row's K/V can round to a neighbouring
     bf16 value, which the later steps carry)."""
     _gpu()
-    for i, (one, all_) in enumerate(_one_vs_all(wl, prefill, steps)):
+    for i, (one, all_, x) in enumerate(_one_vs_all(wl, prefill, steps)):
         if i == 0:
             assert np.array_equal(one, all_)
             continue
-        m = compare(one, all_, one, one)
-        print(f"\n[engines {wl.name} decode step {i - 1}] max|d| {m['max_abs']:.3g} cos {m['cos']:.10f}")
-        assert m["max_abs"] <= TOL_ABS and m["cos"] >= 0.99999, m
+        m = compare(one, all_, x, x)
+        print(f"\n[engines {wl.name} decode step {i - 1}] max|d| {m['max_abs']:.3g} cos {m['cos']:.10f} "
+              f"cos(out - in) {m['cos_delta']:.10f}")
+        assert m["max_abs"] <= TOL_ABS and m["cos"] >= 0.99999 and m["cos_delta"] >= TOL_COS, m
 
 
 LLAMA8B_4x1 = synth.Workload("llama8b_4x1", 106, synth.LLAMA8B_STAGE, n_mb=4, batch=1, prefill=70,

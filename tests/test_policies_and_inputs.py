@@ -90,6 +90,36 @@ def test_residency_codes_block_granular():
     assert s.log == [(0, 1, 0), (0, 2, 1), (0, 3, 0), (0, 4, 1)]
 
 
+def test_planned_residency_hand_table():
+    """Planner steps (Section III-E, Eq. (7)) over an allocation that mixes whole-layer, MHA-only and
+    MLP-only offloading: the alpha MHA blocks and beta MLP blocks come from the highest-id layers
+    whose block the allocation keeps resident (a layer whose MHA block is already offloaded is not
+    counted again), plans are not nested (a later step brings MHA blocks back), and the plan
+    follows the token count down to the allocation.  Expected codes written out by hand."""
+    alloc = [1, 3, 1, 2, 1, 1]          # layer 1: MLP offloaded; layer 3: MHA offloaded
+    plan = [(100, 1, 0), (200, 3, 0), (300, 0, 1), (400, 2, 2), (900, 9, 0)]
+    r = ResidencySchedule(6, codes=alloc, plan=plan)
+    expect = [
+        # (held tokens, codes after the call's step, changes logged by that call)
+        (50, [1, 3, 1, 2, 1, 1], []),                                # below the first threshold
+        (100, [1, 3, 1, 2, 1, 2], [(5, 2)]),                         # MHA of layer 5
+        (150, [1, 3, 1, 2, 1, 2], []),                               # same step: nothing moves
+        (250, [1, 3, 2, 2, 2, 2], [(2, 2), (4, 2)]),                 # MHA of 5, 4, 2 (3 has none)
+        (350, [1, 3, 1, 2, 1, 3], [(2, 1), (4, 1), (5, 3)]),         # MHA back; MLP of layer 5
+        (450, [1, 3, 1, 2, 0, 0], [(4, 0), (5, 0)]),                 # MHA of 5, 4 and MLP of 5, 4
+        (120, [1, 3, 1, 2, 1, 2], [(4, 1), (5, 2)]),                 # cache shrank: step (1, 0)
+        (10, [1, 3, 1, 2, 1, 1], [(5, 1)]),                          # back to the allocation
+        (1000, [2, 0, 2, 2, 2, 2], [(0, 2), (1, 0), (2, 2), (4, 2), (5, 2)]),   # alpha > 5 blocks
+    ]
+    for call, (held, codes, changes) in enumerate(expect):
+        before = len(r.changes)
+        r.before_call_planned(call, held)
+        assert r.codes == codes, (call, r.codes)
+        assert r.changes[before:] == [(call, l, c) for l, c in changes], (call, r.changes[before:])
+    assert r.allocation == alloc
+    assert r.streamed() == [0, 1, 2, 3, 4, 5]
+
+
 # ----------------------------------------------------------------- generator
 def test_splitmix64_matches_published_reference():
     ref = [int(l) for l in open(os.path.join(GOLDEN, "splitmix64_seed1234567.txt")) if l.strip() and l[0] != "#"]
