@@ -99,8 +99,14 @@ typedef struct {
     int32_t n_thresholds;
     int32_t thresholds[STAGE_MAX_THRESHOLDS];
     int32_t device;       /* HIP device ordinal */
-    void *compute_stream; /* hipStream_t for kernels; NULL = the library creates one */
-    void *copy_stream;    /* hipStream_t for slot copies; NULL = the library creates one */
+    /* Streams.  NULL: the library creates the stream on a hardware queue of its own (a stream
+       with a compute-unit mask that enables every compute unit; it waits for work on the null
+       stream like any blocking stream).  HIP otherwise maps streams onto a few shared hardware
+       queues in creation order, and a copy stream sharing the compute stream's queue serialises
+       the slot copies with the kernels (Section III-A's loading under computation is lost), so a
+       caller that passes copy_stream must give it a queue of its own; NULL is recommended. */
+    void *compute_stream; /* hipStream_t for kernels */
+    void *copy_stream;    /* hipStream_t for slot copies and KV parking */
     int32_t timing;       /* STAGE_TIME_* flags; 0 = no events */
     /* 0 (default): offloaded layers are copied into a stream slot before their kernels run.
        1: calls with one token per sequence (every decode call, and a prefill with T = 1) run the
@@ -130,7 +136,7 @@ typedef struct {
        decode calls on different lanes (stage_decode_lane) run concurrently: the interleaved
        schedule's independent micro-batches, whose weight streams then fill each other's
        latency-bound phases.  lane_streams[l]: lane l's hipStream_t (NULL = the library creates
-       one); lane 0 is compute_stream. */
+       one, as for the streams above); lane 0 is compute_stream. */
     int32_t n_lanes;
     void *lane_streams[STAGE_MAX_LANES];
 } stage_config;
@@ -286,7 +292,7 @@ int stage_set_timing(stage *s, int32_t flags);
 
 /* JSON object with counters: calls, tokens, layer loads, bytes streamed through slots and read in
    place (zero copy), block sizes, residency counts, HBM bytes in use, parked tokens and bytes
-   moved by parking. */
+   moved by parking, kernels enqueued by prefill/decode calls in all and by the last one. */
 int stage_get_stats(stage *s, char *buf, int32_t cap);
 
 /* Message of the last error on this handle ("" if none); valid until the next call. */

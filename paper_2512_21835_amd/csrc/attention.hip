@@ -719,27 +719,27 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
     const int hkv = a.kv.n_kv_heads;
     if (a.split_keys == 0) {
         if (a.kv_fp32) {
-            hipLaunchKernelGGL((attn_kernel<G, D, true>), dim3(1, hkv, a.rows), dim3(256), 0, st, a);
+            STG_LAUNCH((attn_kernel<G, D, true>), dim3(1, hkv, a.rows), dim3(256), 0, st, a);
         } else {
             if (a.n_seqs * a.rows_per_seq != a.rows) return hipErrorInvalidValue;
             constexpr int BQ = 128 / G;
             dim3 grid((a.rows_per_seq + BQ - 1) / BQ, hkv, a.n_seqs);
-            hipLaunchKernelGGL((attn_prefill_mfma<G, D>), grid, dim3(256), 0, st, a);
+            STG_LAUNCH((attn_prefill_mfma<G, D>), grid, dim3(256), 0, st, a);
         }
         return hipGetLastError();
     }
     if (a.split_keys > kChunk || a.max_splits > kMaxDecodeSplits) return hipErrorInvalidValue;
     dim3 grid(a.grid_splits, hkv, a.rows);
     if (a.kv_fp32)
-        hipLaunchKernelGGL((attn_decode_kernel<G, D, true>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_kernel<G, D, true>), grid, dim3(256), 0, st, a);
     else if constexpr (D == 128)
-        hipLaunchKernelGGL((attn_decode_mfma<G, D>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_mfma<G, D>), grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL((attn_decode_kernel<G, D, false>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_kernel<G, D, false>), grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t n_out = (size_t)a.rows * a.n_q_heads * D;
-    hipLaunchKernelGGL((attn_merge_flat<D>), dim3((unsigned)((n_out + 255) / 256)), dim3(256), 0, st, a);
+    STG_LAUNCH((attn_merge_flat<D>), dim3((unsigned)((n_out + 255) / 256)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

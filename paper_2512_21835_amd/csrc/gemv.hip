@@ -484,32 +484,32 @@ void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
     if (!c.split_part || !c.split_ss) splits = 1;
     if (splits == 1) {
         if (e0 || e1)
-            hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, c, 0);
+            STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, c, 0);
         else
-            hipLaunchKernelGGL((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, c, 0);
+            STG_LAUNCH((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, c, 0);
         return;
     }
     const int cps = (chunks + splits - 1) / splits;
     splits = (chunks + cps - 1) / cps;  // no empty range
     if (e0)
-        hipExtLaunchKernelGGL((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
+        STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
                               c, cps);
     else
-        hipLaunchKernelGGL((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
+        STG_LAUNCH((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
     const int eg = (c.rows * units + 255) / 256;
     if (e1)
-        hipExtLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, nullptr, e1, 0, c, splits);
+        STG_EXT_LAUNCH((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, nullptr, e1, 0, c, splits);
     else
-        hipLaunchKernelGGL((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, c, splits);
+        STG_LAUNCH((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, c, splits);
 }
 
 template <int M, int R, int U, int MODE>
 void launch_one(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int grid = (host_units(MODE, c) + R - 1) / R;
     if (e0 || e1)
-        hipExtLaunchKernelGGL((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
+        STG_EXT_LAUNCH((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, e0, e1, 0, c);
     else
-        hipLaunchKernelGGL((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, c);
+        STG_LAUNCH((gemv_kernel<M, R, U, MODE>), dim3(grid), dim3(256), 0, st, c);
 }
 
 // Units per workgroup and steps in flight, by mode and rows (swept on the 8B- and 70B-shaped

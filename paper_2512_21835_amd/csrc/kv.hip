@@ -152,18 +152,18 @@ __global__ __launch_bounds__(256) void kv_park_kernel(KvParkArgs a) {
 
 hipError_t launch_kv_park(const KvParkArgs &a, hipStream_t st) {
     if (a.n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(kv_park_kernel, dim3(kParkWorkgroups), dim3(256), 0, st, a);
+    STG_LAUNCH(kv_park_kernel, dim3(kParkWorkgroups), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
 hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st) {
     if (a.rows <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rope_kv_kernel, dim3(a.rows), dim3(256), 0, st, a);
+    STG_LAUNCH(rope_kv_kernel, dim3(a.rows), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
 hipError_t launch_meta_write(const CallMeta &m, CallMeta *dst, hipStream_t st) {
-    hipLaunchKernelGGL(meta_write_kernel, dim3(1), dim3(256), 0, st, m, dst);
+    STG_LAUNCH(meta_write_kernel, dim3(1), dim3(256), 0, st, m, dst);
     return hipGetLastError();
 }
 
@@ -176,7 +176,7 @@ hipError_t launch_table_write(int *table, const int *idx, const int *val, int n,
             c.idx[i] = idx[b + i];
             c.val[i] = val[b + i];
         }
-        hipLaunchKernelGGL(table_write_kernel, dim3(1), dim3(256), 0, st, c);
+        STG_LAUNCH(table_write_kernel, dim3(1), dim3(256), 0, st, c);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -187,9 +187,9 @@ hipError_t launch_kv_copy(const KvCopyArgs &a, hipStream_t st) {
     if (a.n <= 0) return hipSuccess;
     dim3 grid(a.n, a.n_layers);
     if (a.kv_fp32)
-        hipLaunchKernelGGL(kv_copy_kernel<float>, grid, dim3(256), 0, st, a);
+        STG_LAUNCH(kv_copy_kernel<float>, grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL(kv_copy_kernel<uint16_t>, grid, dim3(256), 0, st, a);
+        STG_LAUNCH(kv_copy_kernel<uint16_t>, grid, dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

@@ -347,14 +347,14 @@ void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
     dim3 wide((a.M + 255) / 256, (nv + 255) / 256, n_mats);
     if constexpr (MODE != GEMM_SWIGLU) {
         if (a.K % BK != 0) {
-            hipLaunchKernelGGL(gemm_kernel<MODE>, grid, dim3(256), 0, st, a);
+            STG_LAUNCH(gemm_kernel<MODE>, grid, dim3(256), 0, st, a);
             return;
         }
     }
     if ((long)wide.x * wide.y * wide.z >= 256)   // the wide tiles still fill every compute unit
-        hipLaunchKernelGGL((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
+        STG_LAUNCH((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);
 }
 
 }  // namespace
@@ -376,19 +376,19 @@ hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) 
 hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *hi,
                                 uint16_t *lo, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, hi, lo);
+    STG_LAUNCH(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, hi, lo);
     return hipGetLastError();
 }
 
 hipError_t launch_split(const float *x, size_t count, uint16_t *hi, uint16_t *lo, hipStream_t st) {
     if (count == 0) return hipSuccess;
-    hipLaunchKernelGGL(split_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, count, hi, lo);
+    STG_LAUNCH(split_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, count, hi, lo);
     return hipGetLastError();
 }
 
 hipError_t launch_swiglu_split(const float *gu, int F, size_t rows, uint16_t *hi, uint16_t *lo, hipStream_t st) {
     if (rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(swiglu_split_kernel, dim3(grid_for(rows * F)), dim3(256), 0, st, gu, F, rows, hi, lo);
+    STG_LAUNCH(swiglu_split_kernel, dim3(grid_for(rows * F)), dim3(256), 0, st, gu, F, rows, hi, lo);
     return hipGetLastError();
 }
 

@@ -8,6 +8,20 @@
 
 namespace stg {
 
+// Kernel launches made by this thread through the launch helpers below (the runtime reports the
+// count per call in its statistics).
+extern thread_local long long tl_launches;
+#define STG_LAUNCH(...)                  \
+    do {                                 \
+        ++::stg::tl_launches;            \
+        hipLaunchKernelGGL(__VA_ARGS__);    \
+    } while (0)
+#define STG_EXT_LAUNCH(...)              \
+    do {                                 \
+        ++::stg::tl_launches;            \
+        hipExtLaunchKernelGGL(__VA_ARGS__); \
+    } while (0)
+
 constexpr int kMaxSeqs = 64;     // sequences in one call
 constexpr int kBlockTokens = 16; // tokens per paged-KV block
 

@@ -40,6 +40,10 @@
 
 using namespace stg;
 
+namespace stg {
+thread_local long long tl_launches = 0;
+}
+
 namespace {
 
 constexpr int kDecodeSplitKeys = 64;
@@ -168,6 +172,8 @@ struct stage {
     std::vector<hipStream_t> seq_stream;
     std::vector<hipEvent_t> seq_ev;
 
+    long long kernel_launches = 0, last_call_kernels = 0;  // kernels enqueued by prefill/decode calls
+
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
     long long bytes_direct = 0;   // offloaded-block bytes read in place by zero-copy kernels
     std::string err;
@@ -217,6 +223,22 @@ bool is_device_ptr(const void *p) {
 
 int seq_slot(const stage *s, int mb, int b) { return mb * s->cfg.max_batch + b; }
 
+// A stream on a hardware queue of its own.  HIP spreads ordinary streams over a few hardware queues
+// that they share (4 per process by default), in creation order; two streams on one queue run
+// their work in one order, so a copy stream's wait for a host-to-HBM copy there holds back every
+// compute kernel queued after it, and whether weight streaming overlaps compute would depend on
+// how many streams the process made before.  A stream created with a compute-unit mask always gets
+// a new queue; the mask here enables every compute unit.
+hipError_t create_private_stream(int device, hipStream_t *out) {
+    int n_cu = 0;
+    hipError_t e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return e;
+    if (n_cu < 1) return hipErrorInvalidDevice;
+    std::vector<uint32_t> mask((size_t)(n_cu + 31) / 32, 0xffffffffu);
+    if (n_cu % 32) mask.back() = (1u << (n_cu % 32)) - 1u;
+    return hipExtStreamCreateWithCUMask(out, (uint32_t)mask.size(), mask.data());
+}
+
 hipEvent_t pooled_event(stage *s) {
     if (!s->ev_pool.empty()) {
         hipEvent_t e = s->ev_pool.back();
@@ -235,10 +257,8 @@ int sync_all(stage *s) {
     return STAGE_OK;
 }
 
-// Exchanges the stage's call state (lane 0's, or the lane swapped in) with lanes[l]'s.
-void swap_lane(stage *s, int l) {
-    LaneState &o = s->lanes[l];
-    std::swap(s->cs, o.cs);
+// Exchanges the stage's call workspaces (lane 0's, or those swapped in) with o's.
+void swap_workspaces(stage *s, LaneState &o) {
     std::swap(s->d_meta, o.d_meta);
     std::swap(s->ws_rows, o.ws_rows);
     std::swap(s->part_rows, o.part_rows);
@@ -252,6 +272,12 @@ void swap_lane(stage *s, int l) {
     std::swap(s->ws_part_ml, o.ws_part_ml);
     std::swap(s->ws_split, o.ws_split);
     std::swap(s->ws_split_ss, o.ws_split_ss);
+}
+
+// Exchanges the stage's call state (lane 0's, or the lane swapped in) with lanes[l]'s.
+void swap_lane(stage *s, int l) {
+    std::swap(s->cs, s->lanes[l].cs);
+    swap_workspaces(s, s->lanes[l]);
 }
 
 // With several lanes: the call about to run on s->cs waits for the last call on another stream
@@ -890,7 +916,7 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
 // blocks beyond the allocation, the highest-id layers first (Section III-E, Eq. (7)); layers whose
 // residency differs from that target move, ascending.  The target keeps a subset of the
 // allocation's resident blocks, so it always fits the budget the allocation fits.
-int apply_plan(stage *s, long long call_no, long long held) {
+std::vector<int> plan_codes(const stage *s, long long held) {
     const stage_config &c = s->cfg;
     int step = -1;
     for (int j = 0; j < c.n_thresholds; ++j)
@@ -905,9 +931,17 @@ int apply_plan(stage *s, long long call_no, long long held) {
         if (keep_a[l]) { keep_a[l] = false; --alpha; }
     for (int l = s->L - 1; l >= 0 && beta > 0; --l)
         if (keep_m[l]) { keep_m[l] = false; --beta; }
+    std::vector<int> codes(s->L);
+    for (int l = 0; l < s->L; ++l)
+        codes[l] = keep_a[l] ? (keep_m[l] ? STAGE_RES_RESIDENT : STAGE_RES_MLP_OFFLOADED)
+                             : (keep_m[l] ? STAGE_RES_MHA_OFFLOADED : STAGE_RES_OFFLOADED);
+    return codes;
+}
+
+int apply_plan(stage *s, long long call_no, long long held) {
+    const std::vector<int> codes = plan_codes(s, held);
     for (int l = 0; l < s->L; ++l) {
-        const int code = keep_a[l] ? (keep_m[l] ? STAGE_RES_RESIDENT : STAGE_RES_MLP_OFFLOADED)
-                                   : (keep_m[l] ? STAGE_RES_MHA_OFFLOADED : STAGE_RES_OFFLOADED);
+        const int code = codes[l];
         if (code == code_of(s->layers[l])) continue;
         int rc = set_residency(s, l, code);
         if (rc) return rc;
@@ -916,9 +950,23 @@ int apply_plan(stage *s, long long call_no, long long held) {
     return STAGE_OK;
 }
 
-// Shared body of prefill and decode.
+int run_call_body(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
+                  bool decode);
+
+// Shared body of prefill and decode; counts the kernels the call enqueues.
 int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
              bool decode) {
+    const long long before = tl_launches;
+    const int rc = run_call_body(s, n_mb, mb_ids, B, T, x_in, x_out, decode);
+    if (s) {
+        s->last_call_kernels = tl_launches - before;
+        s->kernel_launches += s->last_call_kernels;
+    }
+    return rc;
+}
+
+int run_call_body(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
+                  bool decode) {
     if (!s) return STAGE_EINVAL;
     s->err.clear();
     const stage_config &c = s->cfg;
@@ -1009,6 +1057,8 @@ int run_call(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const floa
         max_ctx = std::max(max_ctx, s->lengths[slots[i]]);
     }
     const int grid_splits = (max_ctx + kDecodeSplitKeys - 1) / kDecodeSplitKeys;
+    if (T == 1 && grid_splits > s->max_splits)
+        return s->fail(STAGE_ESTATE, "attention partials hold %d splits, the call needs %d", s->max_splits, grid_splits);
     HIP_TRY(launch_meta_write(meta, s->d_meta, s->cs));
     s->calls++;
     if (decode) s->tok_decode += (long long)rows; else s->tok_prefill += (long long)rows;
@@ -1181,10 +1231,10 @@ int stage_init(const stage_config *cfg, stage **out) {
         return code;
     };
     if (c.compute_stream) s->cs = static_cast<hipStream_t>(c.compute_stream);
-    else if (hipStreamCreateWithFlags(&s->cs, hipStreamNonBlocking) == hipSuccess) s->own_cs = true;
+    else if (create_private_stream(c.device, &s->cs) == hipSuccess) s->own_cs = true;
     else return cleanup(STAGE_EHIP);
     if (c.copy_stream) s->xs = static_cast<hipStream_t>(c.copy_stream);
-    else if (hipStreamCreateWithFlags(&s->xs, hipStreamNonBlocking) == hipSuccess) s->own_xs = true;
+    else if (create_private_stream(c.device, &s->xs) == hipSuccess) s->own_xs = true;
     else return cleanup(STAGE_EHIP);
 
     if (hipMalloc(&s->kv_pool, s->kv_layer_stride * s->L) != hipSuccess ||
@@ -1206,7 +1256,7 @@ int stage_init(const stage_config *cfg, stage **out) {
         for (int l = 1; l < c.n_lanes; ++l) {
             LaneState &ln = s->lanes[l];
             if (c.lane_streams[l]) ln.cs = static_cast<hipStream_t>(c.lane_streams[l]);
-            else if (hipStreamCreateWithFlags(&ln.cs, hipStreamNonBlocking) == hipSuccess) ln.own_cs = true;
+            else if (create_private_stream(c.device, &ln.cs) == hipSuccess) ln.own_cs = true;
             else return cleanup(STAGE_EHIP);
             if (hipMalloc(&ln.d_meta, sizeof(CallMeta)) != hipSuccess ||
                 hipMalloc(&ln.ws_split, sizeof(float) * kGemvMaxSplits * 2 * 16 *
@@ -1347,7 +1397,7 @@ int stage_decode(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const
 
 namespace {
 // A call on decode lane `lane` >= 1 (stage_decode_lane, stage_prefill_lane).
-int run_lane_call(stage *s, int lane, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
+static int run_lane_call(stage *s, int lane, int n_mb, const int32_t *mb_ids, int B, int T, const float *x_in, float *x_out,
                   bool decode) {
     if (lane < 0 || lane >= (int)s->lanes.size())
         return s->fail(STAGE_EINVAL, "lane %d out of range (%d lanes)", lane, std::max<int>(1, (int)s->lanes.size()));
@@ -1393,6 +1443,7 @@ int stage_prefill_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_i
     if (lane == 0) return stage_prefill(s, n_mb, mb_ids, B, T, x_in, x_out);
     return run_lane_call(s, lane, n_mb, mb_ids, B, T, x_in, x_out, false);
 }
+
 
 int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k, const void *v) {
     if (!s) return STAGE_EINVAL;
@@ -1694,11 +1745,11 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
         "\"offloaded_mha_blocks\": %d, \"offloaded_mlp_blocks\": %d, "
         "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"host_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, "
         "\"kv_blocks\": %d, \"kv_blocks_free\": %d, \"parked_tokens\": %lld, \"bytes_parked\": %lld, "
-        "\"bytes_unparked\": %lld}",
+        "\"bytes_unparked\": %lld, \"kernel_launches\": %lld, \"last_call_kernels\": %lld}",
         s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes,
         s->blk_bytes[kMha], s->blk_bytes[kMlp], res, streamed, off_mha, off_mlp,
         s->slots.size(), hbm_w, host_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size(),
-        parked, s->bytes_parked, s->bytes_unparked);
+        parked, s->bytes_parked, s->bytes_unparked, s->kernel_launches, s->last_call_kernels);
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }
 

@@ -164,11 +164,11 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
     shape, wl = sc.shape, sc.wl
     weights = weights or weights_of(shape)
     dev = torch.device("cuda", device)
-    copy_stream = torch.cuda.Stream(dev)
+    # copy_stream None: the library's own copy stream, on a hardware queue of its own
     cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=sc.ctx(),
                        n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
                        thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
-                       copy_stream=copy_stream.cuda_stream, timing=sc.timing, zero_copy=sc.zero_copy,
+                       copy_stream=None, timing=sc.timing, zero_copy=sc.zero_copy,
                        plan=sc.plan)
     h = P.stage_init(cfg)
     res = RunResult()
@@ -368,3 +368,39 @@ def compare(got: np.ndarray, ref: np.ndarray, x_got: np.ndarray, x_ref: np.ndarr
         return float((a * b).sum() / math.sqrt((a * a).sum() * (b * b).sum()))
     return {"max_abs": float(np.abs(g - r).max()), "cos": cos(g, r), "cos_delta": cos(dg, dr),
             "rms_ref": float(np.sqrt((r * r).mean())), "n": int(g.size)}
+
+
+def overlap_of_last_call(timeline) -> dict:
+    """Copy/compute overlap of the last call in a stage timeline (records kind, layer, start, end):
+    the union of slot copies (kinds 1, 4) and of layer kernels (kinds 3, 5) of that call, their
+    intersection, hidden-copy = |copy & compute| / |copy| and hidden-shorter = |copy & compute| /
+    min(|copy|, |compute|)."""
+    def union(iv):
+        out = []
+        for s, e in sorted(iv):
+            if out and s <= out[-1][1]:
+                out[-1][1] = max(out[-1][1], e)
+            else:
+                out.append([s, e])
+        return out
+
+    def inter(a, b):
+        i = j = 0
+        tot = 0.0
+        while i < len(a) and j < len(b):
+            tot += max(0.0, min(a[i][1], b[j][1]) - max(a[i][0], b[j][0]))
+            if a[i][1] < b[j][1]:
+                i += 1
+            else:
+                j += 1
+        return tot
+
+    ends = [i for i, r in enumerate(timeline) if r[0] == 0]
+    seg = timeline[ends[-2] + 1: ends[-1] + 1] if len(ends) > 1 else timeline[: ends[-1] + 1]
+    copies = union([(a, b) for k, _, a, b in seg if k in (1, 4)])
+    comp = union([(a, b) for k, _, a, b in seg if k in (3, 5)])
+    t_copy = sum(e - s for s, e in copies)
+    t_comp = sum(e - s for s, e in comp)
+    both = inter(copies, comp)
+    return {"copy_ms": t_copy, "compute_ms": t_comp, "hidden_copy": both / t_copy,
+            "hidden_shorter": both / min(t_copy, t_comp)}

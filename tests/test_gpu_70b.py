@@ -123,8 +123,7 @@ def _full_context_round(n_mb, B, ctx, n_resident, kv_fp32, seed_tag, sampled):
     kvs, xs = {}, {}
     with compute_stream() as cs:
         cfg = P.config_for(SHAPE, max_microbatches=n_mb, max_batch=B, max_context=ctx, n_resident_max=n_resident,
-                           kv_fp32=kv_fp32, compute_stream=cs.handle,
-                           copy_stream=torch.cuda.Stream().cuda_stream)
+                           kv_fp32=kv_fp32, compute_stream=cs.handle)
         h = P.stage_init(cfg)
         try:
             for l in range(L):

@@ -224,6 +224,55 @@ def test_attention_starts_before_the_mlp_block_arrives():
         assert mlp_comp[l][0] >= mha_comp[l][1] - 1e-3
 
 
+def test_streaming_overlaps_compute_whatever_streams_the_process_made():
+    """Loading under computation (Section III-A; the reusable buffer refilled on the GPU's signal,
+    Section III-C) must not depend on the caller's other streams.  HIP shares a few hardware queues
+    among a process's streams in creation order, so the process first creates 8 more streams and
+    then, for four consecutive positions of the compute stream in that order, builds an 8B-shaped
+    stage whose 8 layers all stream through 2 slots on the library's own copy stream, and times a
+    decode call (3 micro-batches of batch 3): the layer kernels must run under the slot copies
+    (hidden-shorter >= 0.8), and the call must take about the copy time alone."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from tests.harness import overlap_of_last_call
+
+    wl = LLAMA8B_MULTI
+    shape = wl.shape
+    weights = weights_of(shape)
+    others = [torch.cuda.Stream() for _ in range(8)]
+    x = torch.from_numpy(np.stack([np.stack([synth.prefill_inputs(wl, m, b, 8) for b in range(wl.batch)])
+                                   for m in range(wl.n_mb)])).cuda()
+    xd = x[:, :, 0].contiguous()
+    for shift in range(4):
+        others += [torch.cuda.Stream() for _ in range(shift)]
+        cs = torch.cuda.Stream()
+        with torch.cuda.stream(cs):
+            cfg = P.config_for(shape, max_microbatches=wl.n_mb, max_batch=wl.batch, max_context=16, n_resident_max=0,
+                               compute_stream=cs.cuda_stream)
+            h = P.stage_init(cfg)
+            try:
+                for l in range(shape.n_layers):
+                    P.stage_load_layer(h, l, weights(l), 0)
+                y = torch.empty_like(x)
+                P.stage_prefill(h, list(range(wl.n_mb)), wl.batch, 8, x, y)
+                yd = torch.empty_like(xd)
+                P.stage_decode(h, list(range(wl.n_mb)), wl.batch, xd, yd)
+                P.stage_sync(h)
+                P.stage_get_timeline(h)
+                P.stage_set_timing(h, P.STAGE_TIME_CALLS | P.STAGE_TIME_LAYERS)
+                for _ in range(2):
+                    P.stage_decode(h, list(range(wl.n_mb)), wl.batch, xd, yd)
+                tl = P.stage_get_timeline(h)
+            finally:
+                P.stage_destroy(h)
+        ov = overlap_of_last_call(tl)
+        call = [b - a for k, _, a, b in tl if k == 0][-1]
+        print(f"\n[overlap, compute stream shifted by {shift}] {ov}, call {call:.3f} ms", flush=True)
+        assert ov["hidden_shorter"] >= 0.8, (shift, ov)
+        assert call <= 1.1 * ov["copy_ms"] + 0.5, (shift, call, ov)
+
+
 @pytest.mark.parametrize("zero_copy", [False, True])
 def test_planner_steps_drive_block_residency(zero_copy):
     """Steps of the online planner (Eq. (7), computed by stage_plan_offload for a device whose
