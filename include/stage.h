@@ -163,8 +163,9 @@ int stage_destroy(stage *s);
 /* Loads layer `layer` (0 <= layer < n_layers) and sets its residency `resident`, a STAGE_RES_*
    code (Section III-A: retained vs offloaded layers; Section III-D: MHA or MLP block only).
    w != NULL: copy the weights into library storage -- HBM for a resident block, pinned host
-   memory (hipHostMalloc) for an offloaded one; the caller may free w on return (the call
-   synchronises its copies).  w == NULL: change the residency of an already loaded layer (each
+   memory (hipHostMalloc) for an offloaded one; device sources must hold their values when the
+   call is made (e.g. written on the compute stream); the copies run on the compute stream and the
+   call waits for them, so the caller may free w on return.  w == NULL: change the residency of an already loaded layer (each
    block that changes side is copied across), which is the planner's offload action (Section
    III-E).  EINVAL: bad layer or code; ENOMEM: the resident blocks would exceed the weight budget,
    or allocation failed (the layer is unchanged); ESTATE: w == NULL for a layer never loaded. */

@@ -151,9 +151,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
 // of the wavefront writes LDS bytes [lds_addr + 16 l, lds_addr + 16 l + 16).  Issued as inline
 // assembly so that the compiler does not wait for every such load before each LDS read (it cannot
 // tell which LDS bytes a DMA load writes); the kernel waits for them itself (wait_vm).  m0 holds
-// the wavefront-uniform LDS address; nothing else in the kernel uses m0.
+// the wavefront-uniform LDS address; nothing else in the kernel uses m0.  An LDS DMA must not
+// directly follow a scalar write of m0 (gfx9 asks for one wait state there; the compiler inserts it
+// in code it generates, not inside inline assembly), hence the s_nop.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory");
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory");
 }
 
 // s_waitcnt vmcnt(N), other counters untouched.

@@ -433,7 +433,10 @@ int set_residency(stage *s, int layer, int code) {
         Block &k = ly.blk[b];
         if (k.resident) {
             if (fresh[b].host) {
-                hipError_t e = hipMemcpy(fresh[b].host, k.dev, s->blk_bytes[b], hipMemcpyDeviceToHost);
+                // on the compute stream, waited for here: the copies of this file never go through the
+                // null stream, which a caller's non-blocking compute stream does not wait for
+                hipError_t e = hipMemcpyAsync(fresh[b].host, k.dev, s->blk_bytes[b], hipMemcpyDeviceToHost, s->cs);
+                if (e == hipSuccess) e = hipStreamSynchronize(s->cs);
                 if (e != hipSuccess) {
                     release();
                     return s->fail_hip(e, "copying a weight block to host memory");
@@ -446,7 +449,8 @@ int set_residency(stage *s, int layer, int code) {
             k.dev = nullptr;
             k.resident = false;
         } else {
-            hipError_t e = hipMemcpy(fresh[b].dev, k.host, s->blk_bytes[b], hipMemcpyHostToDevice);
+            hipError_t e = hipMemcpyAsync(fresh[b].dev, k.host, s->blk_bytes[b], hipMemcpyHostToDevice, s->cs);
+            if (e == hipSuccess) e = hipStreamSynchronize(s->cs);
             if (e != hipSuccess) {
                 release();
                 return s->fail_hip(e, "copying a weight block to HBM");
@@ -1249,7 +1253,7 @@ int stage_init(const stage_config *cfg, stage **out) {
         return cleanup(STAGE_ENOMEM);
     }
     s->block_park.assign(s->n_blocks, nullptr);
-    if (hipMemset(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess)
+    if (hipMemsetAsync(s->d_table, 0, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks, s->cs) != hipSuccess)
         return cleanup(STAGE_EHIP);
     if (c.n_lanes > 1) {
         s->lanes.resize(c.n_lanes);
@@ -1280,8 +1284,11 @@ int stage_init(const stage_config *cfg, stage **out) {
             ct[(size_t)p * half + i] = (float)std::cos(ang);
             st[(size_t)p * half + i] = (float)std::sin(ang);
         }
-    if (hipMemcpy(s->d_cos, ct.data(), ct.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(s->d_sin, st.data(), st.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess)
+    // on the compute stream and waited for: the stage's kernels run on non-blocking streams, which do
+    // not wait for work on the null stream
+    if (hipMemcpyAsync(s->d_cos, ct.data(), ct.size() * sizeof(float), hipMemcpyHostToDevice, s->cs) != hipSuccess ||
+        hipMemcpyAsync(s->d_sin, st.data(), st.size() * sizeof(float), hipMemcpyHostToDevice, s->cs) != hipSuccess ||
+        hipStreamSynchronize(s->cs) != hipSuccess)
         return cleanup(STAGE_EHIP);
     *out = s;
     return STAGE_OK;
@@ -1368,14 +1375,19 @@ int stage_load_layer(stage *s, int32_t layer, const stage_layer_weights *w, int3
                             s->off_wo, s->off_wg, s->off_wu, s->off_wd, s->off_g1, s->off_g2};
     const size_t bytes[9] = {qd * H * 2, kvd * H * 2, kvd * H * 2, H * qd * 2, F * H * 2,
                              F * H * 2, H * F * 2, H * 2, H * 2};
-    for (int i = 0; i < 9; ++i) {
+    // Copies on the compute stream, then waited for: a device-to-device hipMemcpy on the null stream
+    // returns before it completes, and kernels on a non-blocking compute stream would not wait for it
+    // (they could read a half-copied layer).
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < 9 && e == hipSuccess; ++i) {
         const Block &k = fresh[blk_of[i]];
         char *dst = static_cast<char *>(k.resident ? k.dev : k.host);
-        hipError_t e = hipMemcpy(dst + offs[i], src[i], bytes[i], hipMemcpyDefault);
-        if (e != hipSuccess) {
-            for (Block &f : fresh) free_block(f);
-            return s->fail_hip(e, "copying layer weights");
-        }
+        e = hipMemcpyAsync(dst + offs[i], src[i], bytes[i], hipMemcpyDefault, s->cs);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(s->cs);
+    if (e != hipSuccess) {
+        for (Block &f : fresh) free_block(f);
+        return s->fail_hip(e, "copying layer weights");
     }
     for (int b = 0; b < 2; ++b) {
         free_block(ly.blk[b]);
