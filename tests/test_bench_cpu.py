@@ -46,3 +46,14 @@ def test_roofline_bytes_and_flops():
     gemm, attn = bench.prefill_flops(s8, 1024)
     assert gemm == 2 * (6144 * 4096 + 4096 * 4096 + 3 * 14336 * 4096) * 1024 * 8 == 3_573_412_790_272
     assert attn == 4 * (1024 * 1025 // 2) * 32 * 128 * 8 == 68_786_585_600
+
+
+def test_eq1_total_of_a_given_spread_by_hand():
+    """Eq. (1) for the hand-worked two-device instance (whole-layer offloading): compute 1*3 + 2*3,
+    hops 2 stages x 2 devices x 1, uncovered max(0, 1*10 - (1*2 + 2*3 + 2), 2*6 - (2*1 + 1*3 + 2))
+    = 5; total 18."""
+    import bench
+    devices = [(25, 1, 3, 7), (15, 2, 2, 4)]
+    assert bench.eq1_total(2, devices, [3, 3], [2, 1], [1, 2], 1) == 9 + 4 + 5 == 18
+    # nothing offloaded: compute and hops only
+    assert bench.eq1_total(1, devices, [2, 1], [2, 1], [0, 0], 3) == 2 + 2 + 1 * 2 * 3
