@@ -366,8 +366,30 @@ def compare(got: np.ndarray, ref: np.ndarray, x_got: np.ndarray, x_ref: np.ndarr
 
     def cos(a, b):
         return float((a * b).sum() / math.sqrt((a * a).sum() * (b * b).sum()))
-    return {"max_abs": float(np.abs(g - r).max()), "cos": cos(g, r), "cos_delta": cos(dg, dr),
-            "rms_ref": float(np.sqrt((r * r).mean())), "n": int(g.size)}
+    d = np.abs(g - r)
+    worst = int(np.argmax(d))
+    row, col = divmod(worst, g.shape[-1]) if g.ndim > 1 else (0, worst)
+    return {"max_abs": float(d.flat[worst]), "cos": cos(g, r), "cos_delta": cos(dg, dr),
+            "rms_ref": float(np.sqrt((r * r).mean())), "n": int(g.size), "worst_row": row, "worst_col": col,
+            "worst_ref": float(r.flat[worst])}
+
+
+def row_origin(sc: Scenario, row: int) -> Tuple[int, str, int, int, int]:
+    """Where flat output row `row` of a run of the scenario comes from: (call index, kind, mb, b,
+    position in the sequence); rows are in call order, each call's rows [mb][b][t]."""
+    pos: Dict[Tuple[int, int], int] = {}
+    for call, (kind, mbs, _) in enumerate(sc.call_plan()):
+        T = sc.prefill if kind == "prefill" else 1
+        n = len(mbs) * sc.wl.batch * T
+        if row < n:
+            i, rest = divmod(row, sc.wl.batch * T)
+            b, t = divmod(rest, T)
+            return call, kind, mbs[i], b, pos.get((mbs[i], b), 0) + t
+        row -= n
+        for m in mbs:
+            for b in range(sc.wl.batch):
+                pos[(m, b)] = pos.get((m, b), 0) + T
+    raise IndexError("row beyond the scenario's calls")
 
 
 def overlap_of_last_call(timeline) -> dict:
