@@ -41,9 +41,8 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": None, "source_sha256": None},
-    "llama3-8b-shaped-8L": {"bytes": 235259002,
-                            "source_sha256": "e777833278ae2ff5d75ff4ad83970d5e41d1c0b523fbca1a4a771d884799cd66"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940189838,
+                                "source_sha256": "662ff977647f7a9c6b4cd3fd3f1d6f3f4a491b2d7ddb59344bb3c1d41cbe338b"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
