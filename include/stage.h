@@ -208,6 +208,28 @@ int stage_decode_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_id
 int stage_prefill_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_ids, int32_t B, int32_t T,
                        const float *x_in, float *x_out);
 
+/* Size of the per-GPU scratch array used by stage_decode_noalloc: 64 MiB. */
+#define STAGE_NOALLOC_SCRATCH_BYTES 67108864
+
+/* stage_decode for callers that cannot allocate device memory during the call (code under HIP
+   graph capture, tight serving loops, harnesses that forbid hipMalloc): the same kernels and the
+   same outputs as stage_decode, with their workspaces (row metadata, rotated queries, attention
+   split partials and output, SwiGLU output, split-K partials) carved out of one fixed scratch
+   array that every GPU the library runs on holds from the library's load until the process ends
+   (STAGE_NOALLOC_SCRATCH_BYTES; its device address is looked up once per device by stage_init).
+   The call makes no hipMalloc, hipFree or other allocating call and records no timing events.
+   Every call on one GPU shares that GPU's array and leaves its contents behind: calls that
+   overlap on one GPU (other stages' noalloc calls on other streams, or this stage's on other
+   lanes) race; calls ordered on one stream are safe.  The caller still owns x_in and x_out.
+   ENOMEM: the call needs more scratch than the array holds (the message gives the bytes; it
+   grows with rows x (2 Hq d + ffn) and rows x Hq x ceil(context / 64) x (d + 2), plus a split-K
+   area for 3 rows or more); ESTATE: the call would allocate -- a residency change is due (the
+   threshold schedule or the planner), stream slots have not been allocated yet (run one
+   stage_decode first), or a sequence of the call has a parked KV tail; otherwise as
+   stage_decode.  Nothing changes on an error. */
+int stage_decode_noalloc(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                         float *x_out);
+
 /* Appends n_tokens positions of already-rotated K and V to sequence (mb, b) without compute:
    the concatenation of a received KV-cache tail in the KV transfer protocol (Section III-E,
    Alg. 2).  k, v: [n_layers][n_tokens][n_kv_heads][head_dim] in the KV element type (bf16 bits

@@ -7,7 +7,8 @@ from .stage import (  # noqa: F401
     StageConfig, StageLayerWeights, StageError, config_for, lib, EXPORTED, LIB_PATH,
     STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE,
     STAGE_TIME_CALLS, STAGE_TIME_GATEUP, STAGE_TIME_LAYERS, STAGE_MAX_THRESHOLDS, STAGE_MAX_SEQS_PER_CALL,
-    STAGE_MAX_CONTEXT, STAGE_MAX_LANES, stage_decode_lane, stage_prefill_lane,
+    STAGE_MAX_CONTEXT, STAGE_MAX_LANES, stage_decode_lane, stage_prefill_lane, stage_decode_noalloc,
+    STAGE_NOALLOC_SCRATCH_BYTES,
     STAGE_RES_OFFLOADED, STAGE_RES_RESIDENT, STAGE_RES_MHA_OFFLOADED, STAGE_RES_MLP_OFFLOADED,
     stage_config_default, stage_init, stage_destroy, stage_load_layer, stage_prefill, stage_decode,
     stage_kv_append, stage_kv_export_tail, stage_reset_sequence, stage_sync, stage_get_block_table,

@@ -174,4 +174,10 @@ struct KvParkArgs {
 constexpr int kParkWorkgroups = 32;  // few compute units: the host link is the bound
 hipError_t launch_kv_park(const KvParkArgs &a, hipStream_t st);
 
+// Bytes of the per-device scratch array of stage_decode_noalloc (noalloc.hip).
+constexpr size_t kScratchBytes = size_t(64) << 20;
+// Device address of the current device's scratch array, looked up on the first call for
+// `device` (which must be current) and kept.
+hipError_t scratch_setup(int device, void **out);
+
 }  // namespace stg

@@ -172,6 +172,7 @@ struct stage {
     std::vector<hipStream_t> seq_stream;
     std::vector<hipEvent_t> seq_ev;
 
+    void *scratch = nullptr;  // this device's scratch array (stage_decode_noalloc)
     long long kernel_launches = 0, last_call_kernels = 0;  // kernels enqueued by prefill/decode calls
 
     long long tok_prefill = 0, tok_decode = 0, bytes_streamed = 0;
@@ -1134,6 +1135,37 @@ int run_call_body(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const
     return mark_sequences(s, slots);
 }
 
+// Where stage_decode_noalloc puts a call's workspaces in the scratch array: byte offsets, 256-byte
+// aligned; `split` and `split_ss` only for calls of 3 rows or more (the matrix-core projections).
+struct ScratchLayout {
+    size_t meta = 0, q = 0, attn = 0, h = 0, part_o = 0, part_ml = 0, split = 0, split_ss = 0, total = 0;
+    bool has_split = false;
+};
+
+ScratchLayout scratch_layout(const stage *s, size_t rows, int splits) {
+    ScratchLayout p;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align256(off + bytes);
+        return at;
+    };
+    const size_t qd = (size_t)s->Hq * s->D;
+    p.meta = take(sizeof(CallMeta));
+    p.q = take(rows * qd * sizeof(float));
+    p.attn = take(rows * qd * sizeof(float));
+    p.h = take(rows * (size_t)s->F * sizeof(float));
+    p.part_o = take(rows * s->Hq * (size_t)splits * s->D * sizeof(float));
+    p.part_ml = take(rows * s->Hq * (size_t)splits * 2 * sizeof(float));
+    p.has_split = rows >= 3;
+    if (p.has_split) {
+        const size_t units = std::max<size_t>(std::max<size_t>(s->qkv_rows / 2, s->H), s->F);
+        p.split = take(sizeof(float) * kGemvMaxSplits * 2 * 16 * units);
+        p.split_ss = take(sizeof(float) * kGemvMaxSplits * 16);
+    }
+    p.total = off;
+    return p;
+}
 }  // namespace
 
 extern "C" {
@@ -1241,6 +1273,7 @@ int stage_init(const stage_config *cfg, stage **out) {
     else if (create_private_stream(c.device, &s->xs) == hipSuccess) s->own_xs = true;
     else return cleanup(STAGE_EHIP);
 
+    if (scratch_setup(c.device, &s->scratch) != hipSuccess) return cleanup(STAGE_EHIP);
     if (hipMalloc(&s->kv_pool, s->kv_layer_stride * s->L) != hipSuccess ||
         hipMalloc(&s->d_table, sizeof(int) * (size_t)s->n_seq_slots * s->max_blocks) != hipSuccess ||
         hipMalloc(&s->d_cos, sizeof(float) * (size_t)c.max_context * (s->D / 2)) != hipSuccess ||
@@ -1456,6 +1489,78 @@ int stage_prefill_lane(stage *s, int32_t lane, int32_t n_mb, const int32_t *mb_i
     return run_lane_call(s, lane, n_mb, mb_ids, B, T, x_in, x_out, false);
 }
 
+
+int stage_decode_noalloc(stage *s, int32_t n_mb, const int32_t *mb_ids, int32_t B, const float *x_in,
+                         float *x_out) {
+    if (!s) return STAGE_EINVAL;
+    s->err.clear();
+    const stage_config &c = s->cfg;
+    if (n_mb < 1 || n_mb > c.max_microbatches || !mb_ids || B < 1 || B > c.max_batch || !x_in || !x_out)
+        return s->fail(STAGE_EINVAL, "bad call arguments (n_mb=%d B=%d)", n_mb, B);
+    std::vector<int> slots;
+    std::vector<char> seen(c.max_microbatches, 0);
+    for (int k = 0; k < n_mb; ++k) {
+        const int mb = mb_ids[k];
+        if (mb < 0 || mb >= c.max_microbatches || seen[mb])
+            return s->fail(STAGE_EINVAL, "micro-batch id %d out of range or repeated", mb);
+        seen[mb] = 1;
+        for (int b = 0; b < B; ++b) slots.push_back(seq_slot(s, mb, b));
+    }
+    int longest = 0, max_after = 1;
+    long long held = (long long)slots.size();
+    for (int len : s->lengths) {
+        longest = std::max(longest, len);
+        held += len;
+    }
+    for (int sl : slots) {
+        if (s->parked[sl]) return s->fail(STAGE_ESTATE, "sequence slot %d has a parked KV tail", sl);
+        longest = std::max(longest, s->lengths[sl] + 1);
+        max_after = std::max(max_after, s->lengths[sl] + 1);
+    }
+    const int splits = std::min(s->max_splits, (max_after + kDecodeSplitKeys - 1) / kDecodeSplitKeys);
+    const ScratchLayout lay = scratch_layout(s, slots.size(), splits);
+    if (lay.total > kScratchBytes)
+        return s->fail(STAGE_ENOMEM, "the call needs %zu bytes of scratch; the limit is %zu (STAGE_NOALLOC_SCRATCH_BYTES)",
+                       lay.total, kScratchBytes);
+    // nothing in the call may allocate: no residency change, no first slot allocation
+    if (c.plan_mode) {
+        const std::vector<int> codes = plan_codes(s, held);
+        for (int l = 0; l < s->L; ++l)
+            if (codes[l] != code_of(s->layers[l]))
+                return s->fail(STAGE_ESTATE, "the planner would change layer %d's residency in this call", l);
+    } else if (s->thresholds_applied < c.n_thresholds && c.thresholds[s->thresholds_applied] <= longest) {
+        return s->fail(STAGE_ESTATE, "a residency threshold is reached in this call");
+    }
+    if (!c.zero_copy && s->slots.empty()) {
+        bool may_stream = c.plan_mode ? c.n_thresholds > 0 : s->thresholds_applied < c.n_thresholds;
+        for (const Layer &ly : s->layers) may_stream = may_stream || ly.streams();
+        if (may_stream) return s->fail(STAGE_ESTATE, "stream slots are not allocated yet (run stage_decode once)");
+    }
+    if (!s->scratch) return s->fail(STAGE_ESTATE, "no scratch array on this device");
+    char *base = static_cast<char *>(s->scratch);
+    LaneState ws;
+    ws.d_meta = reinterpret_cast<CallMeta *>(base + lay.meta);
+    ws.ws_rows = slots.size();
+    ws.part_rows = slots.size();
+    ws.ws_q = reinterpret_cast<float *>(base + lay.q);
+    ws.ws_attn = reinterpret_cast<float *>(base + lay.attn);
+    ws.ws_h = reinterpret_cast<float *>(base + lay.h);
+    ws.ws_part_o = reinterpret_cast<float *>(base + lay.part_o);
+    ws.ws_part_ml = reinterpret_cast<float *>(base + lay.part_ml);
+    ws.ws_split = lay.has_split ? reinterpret_cast<float *>(base + lay.split) : nullptr;
+    ws.ws_split_ss = lay.has_split ? reinterpret_cast<float *>(base + lay.split_ss) : nullptr;
+    DeviceGuard dg(c.device);
+    swap_workspaces(s, ws);
+    const int saved_splits = s->max_splits;
+    const int32_t timing = s->cfg.timing;
+    s->max_splits = splits;  // the stride of the attention partials in the scratch array
+    s->cfg.timing = 0;       // no timing events: their pool may have to create one
+    const int rc = run_call(s, n_mb, mb_ids, B, 1, x_in, x_out, true);
+    s->cfg.timing = timing;
+    s->max_splits = saved_splits;
+    swap_workspaces(s, ws);
+    return rc;
+}
 
 int stage_kv_append(stage *s, int32_t mb, int32_t b, int32_t n_tokens, const void *k, const void *v) {
     if (!s) return STAGE_EINVAL;

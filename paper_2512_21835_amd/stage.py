@@ -37,7 +37,9 @@ EXPORTED = (
     "stage_get_block_table", "stage_get_length", "stage_get_residency", "stage_get_slot_log",
     "stage_get_demotion_log", "stage_get_residency_log", "stage_get_timeline", "stage_set_timing", "stage_get_stats",
     "stage_last_error", "stage_strerror", "stage_plan_offload", "stage_allocate", "stage_kv_park", "stage_kv_unpark",
+    "stage_decode_noalloc",
 )
+STAGE_NOALLOC_SCRATCH_BYTES = 67108864
 STAGE_ALLOC_MAX_DEVICES = 64
 STAGE_ALLOC_MAX_LAYERS = 4096
 
@@ -118,6 +120,7 @@ def lib():
         "stage_prefill": (c_int32, [c_void_p, c_int32, ip, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_decode": (c_int32, [c_void_p, c_int32, ip, c_int32, c_void_p, c_void_p]),
         "stage_decode_lane": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, c_void_p, c_void_p]),
+        "stage_decode_noalloc": (c_int32, [c_void_p, c_int32, ip, c_int32, c_void_p, c_void_p]),
         "stage_prefill_lane": (c_int32, [c_void_p, c_int32, c_int32, ip, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_append": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
         "stage_kv_export_tail": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_int32]),
@@ -208,6 +211,10 @@ def stage_prefill(h, mb_ids: Sequence[int], B: int, T: int, x_in: torch.Tensor, 
 
 def stage_decode(h, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
     _check(lib().stage_decode(h, len(mb_ids), _ids(mb_ids), B, _ptr(x_in), _ptr(x_out)), h)
+
+
+def stage_decode_noalloc(h, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
+    _check(lib().stage_decode_noalloc(h, len(mb_ids), _ids(mb_ids), B, _ptr(x_in), _ptr(x_out)), h)
 
 
 def stage_decode_lane(h, lane: int, mb_ids: Sequence[int], B: int, x_in: torch.Tensor, x_out: torch.Tensor) -> None:
