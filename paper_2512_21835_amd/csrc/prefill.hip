@@ -17,6 +17,8 @@
 // attention output (before O) and the SwiGLU of the gate/up output (before down).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "lanes.h"
 #include "stage_kernels.h"
 
@@ -164,6 +166,13 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt(0x3F70 | (N & 0xF) | ((N >> 4) << 14));
 }
 
+// s_waitcnt lgkmcnt(N), other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_lgkm() {
+    static_assert(N >= 0 && N < 16, "lgkmcnt is four bits");
+    __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+}
+
 // The same product as gemm_kernel (same MFMAs in the same order: bit-identical results) for K a
 // multiple of 32, with the operand tiles copied into a ring of three LDS stages by
 // global_load_lds: tile t + 2 is in flight while tile t is multiplied, and no registers stage it.
@@ -175,6 +184,12 @@ __device__ __forceinline__ void wait_vm() {
 // contiguous bytes (lane l: row 16 q + l / 4 of instruction q), and the 32 x 32 fragment reads
 // (lane l: row l % 32, segment 2 step + l / 32) touch every LDS bank once per 16 lanes.  (Loading
 // in fragment order instead, 32 rows x 32 bytes per instruction, took 1.3-1.6x as long.)
+//
+// With one wavefront per SIMD (WB = 4) nothing else hides the latency of a fragment read or of the
+// barrier, so that loop is software-pipelined (K >= 64): the fragments of the next k step are
+// read one whole batch of 32 MFMAs before they are used, the tile's barrier sits between its two
+// k steps, and the DMA of tile t + 2 is issued between the MFMAs of tile t's first step.  Schedule
+// fences keep the compiler from moving the MFMAs across the barrier or the reads to their use.
 template <int MODE, int WB>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     constexpr int S = 3;
@@ -209,15 +224,16 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
             src_w[i] = W + (size_t)min(n0 + r, N - 1) * K + 8 * seg;
         }
     }
+    // this wavefront's share of tile t: instruction i of each operand
+    auto issue_part = [&](int t, int i) {
+        const int st = t % S, k0 = t * BK, q = wave * WB + i;
+        dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + q * 64) * 16);
+        dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + q * 64) * 16);
+        dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + q * 64) * 16);
+    };
     auto issue = [&](int t) {
-        const int st = t % S, k0 = t * BK;
 #pragma unroll
-        for (int i = 0; i < WB; ++i) {
-            const int q = wave * WB + i;
-            dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + q * 64) * 16);
-            dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + q * 64) * 16);
-            dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + q * 64) * 16);
-        }
+        for (int i = 0; i < WB; ++i) issue_part(t, i);
     };
 
     f32x16 acc[WB][WB];
@@ -228,37 +244,84 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    issue(0);
-    if (nk > 1) issue(1);
     const int fr = lane & 31, fk = lane >> 5;   // fragment row and k half of this lane
-    for (int t = 0; t < nk; ++t) {
-        // tile t has landed when at most the next tile's loads are still in flight
-        if (t + 1 < nk) wait_vm<PER_TILE>();
-        else wait_vm<0>();
-        __syncthreads();  // every wavefront's part of tile t is in LDS; stage (t - 1) % S is free
-        if (t + 2 < nk) issue(t + 2);
+    // the fragments of k step `step` (0 or 1) of tile t, which is in stage t % S
+    auto read = [&](int t, int step, bf16x8 (&ah)[WB], bf16x8 (&al)[WB], bf16x8 (&bw)[WB]) {
         const uint4 *L = &lds[t % S][0][0];
+        const int seg = 2 * step + fk;
 #pragma unroll
-        for (int step = 0; step < BK / 16; ++step) {
-            bf16x8 ah[WB], al[WB], bw[WB];
-            const int seg = 2 * step + fk;
+        for (int b = 0; b < WB; ++b) {
+            const int ra = 32 * (wm * WB + b) + fr, rb = 32 * (wn * WB + b) + fr;
+            const int sa = 4 * ra + (seg ^ ((ra >> 2) & 3));
+            const int sb = 4 * rb + (seg ^ ((rb >> 2) & 3));
+            ah[b] = as_bf16x8(L[sa]);
+            al[b] = as_bf16x8(L[SLOTS + sa]);
+            bw[b] = as_bf16x8(L[2 * SLOTS + sb]);
+        }
+    };
+    // one k step of accumulator row i: hi then lo into each block
+    auto mma_row = [&](int i, const bf16x8 (&ah)[WB], const bf16x8 (&al)[WB], const bf16x8 (&bw)[WB]) {
 #pragma unroll
-            for (int b = 0; b < WB; ++b) {
-                const int ra = 32 * (wm * WB + b) + fr, rb = 32 * (wn * WB + b) + fr;
-                const int sa = 4 * ra + (seg ^ ((ra >> 2) & 3));
-                const int sb = 4 * rb + (seg ^ ((rb >> 2) & 3));
-                ah[b] = as_bf16x8(L[sa]);
-                al[b] = as_bf16x8(L[SLOTS + sa]);
-                bw[b] = as_bf16x8(L[2 * SLOTS + sb]);
+        for (int j = 0; j < WB; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bw[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bw[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    if constexpr (WB != 4) {
+        issue(0);
+        if (nk > 1) issue(1);
+        for (int t = 0; t < nk; ++t) {
+            // tile t has landed when at most the next tile's loads are still in flight
+            if (t + 1 < nk) wait_vm<PER_TILE>();
+            else wait_vm<0>();
+            __syncthreads();  // every wavefront's part of tile t is in LDS; stage (t - 1) % S is free
+            if (t + 2 < nk) issue(t + 2);
+#pragma unroll
+            for (int step = 0; step < BK / 16; ++step) {
+                bf16x8 ah[WB], al[WB], bw[WB];
+                read(t, step, ah, al, bw);
+#pragma unroll
+                for (int i = 0; i < WB; ++i) mma_row(i, ah, al, bw);
+            }
+        }
+    } else {
+        // nk >= 2 (launch_gemm_mode).  The loop body is straight-line (the last two tiles are
+        // peeled), so that no merge of control flow makes the second batch wait for the reads
+        // issued after the barrier.
+        issue(0);
+        issue(1);
+        wait_vm<PER_TILE>();
+        __syncthreads();
+        bf16x8 h0[WB], l0[WB], w0[WB], h1[WB], l1[WB], w1[WB];
+        read(0, 0, h0, l0, w0);
+        auto tile = [&](int t, auto more_dma, auto more_tiles) {
+            read(t, 1, h1, l1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+            // the DMA of tile t + 2 goes to stage (t + 2) % S, which held tile t - 1: every
+            // wavefront finished reading it before the previous tile's barrier
+#pragma unroll
+            for (int i = 0; i < WB; ++i) {
+                mma_row(i, h0, l0, w0);
+                if constexpr (decltype(more_dma)::value) issue_part(t + 2, i);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (decltype(more_tiles)::value) {
+                if constexpr (decltype(more_dma)::value) wait_vm<PER_TILE>();   // tile t + 1 has landed
+                else wait_vm<0>();
+                wait_lgkm<0>();   // this wavefront's reads of tile t are done
+                __syncthreads();
+                read(t + 1, 0, h0, l0, w0);
+                __builtin_amdgcn_sched_barrier(0);
             }
 #pragma unroll
-            for (int i = 0; i < WB; ++i)
-#pragma unroll
-                for (int j = 0; j < WB; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bw[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bw[j], acc[i][j], 0, 0, 0);
-                }
-        }
+            for (int i = 0; i < WB; ++i) mma_row(i, h1, l1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        int t = 0;
+        for (; t + 2 < nk; ++t) tile(t, std::true_type{}, std::true_type{});
+        tile(t, std::false_type{}, std::true_type{});
+        tile(t + 1, std::false_type{}, std::false_type{});
     }
 
     if (MODE == GEMM_SWIGLU) {   // blocks j (gate) and j + 1 (up) hold the same rows of h
@@ -353,7 +416,8 @@ void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
             return;
         }
     }
-    if ((long)wide.x * wide.y * wide.z >= 256)   // the wide tiles still fill every compute unit
+    // the wide tiles when they still fill every compute unit (their pipelined loop takes K >= 64)
+    if ((long)wide.x * wide.y * wide.z >= 256 && a.K >= 2 * BK)
         STG_LAUNCH((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
     else
         STG_LAUNCH((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);
