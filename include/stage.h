@@ -51,7 +51,8 @@ typedef enum {
     STAGE_ENOMEM = -2, /* HBM budget, device/pinned allocation or KV block pool exhausted */
     STAGE_EHIP = -3,   /* a HIP runtime call failed */
     STAGE_ESTATE = -4, /* not valid now (layer not loaded, sequence empty, ...) */
-    STAGE_ERANGE = -5  /* a sequence would exceed max_context */
+    STAGE_ERANGE = -5, /* a sequence would exceed max_context */
+    STAGE_ESLOT = -6   /* a slot tag check failed (stage_config.slot_check; reported by stage_sync) */
 } stage_status;
 
 #define STAGE_MAX_THRESHOLDS 32
@@ -139,6 +140,21 @@ typedef struct {
        one, as for the streams above); lane 0 is compute_stream. */
     int32_t n_lanes;
     void *lane_streams[STAGE_MAX_LANES];
+    /* Slot tag check (Section III-C: a reusable slot is refilled only after the kernels reading
+       its previous layer have finished, and read only after its copy completed).  0: off.
+       1: each stream slot carries a tag per block (layer, load number of the stage's life).  The
+       copy stream invalidates a block's tag before copying into it and writes the new tag after
+       the copy; on the compute stream a one-thread kernel compares the tag with the layer and load
+       the call expects before the block's first kernel and again after the layer's last kernel,
+       and counts mismatches in device memory.  A mismatch before means the block was not (or not
+       yet) loaded; after, that the copy stream started refilling the slot while the layer still
+       read it.  stage_sync returns STAGE_ESLOT once any check has failed since the previous
+       stage_sync (stage_last_error names the first mismatch) and clears the count.  Costs one
+       check kernel per streamed block before and after its layer and two tag writes per copy;
+       outputs are bit-identical to mode 0.  2: as 1, but the checks before MHA blocks expect the
+       next load number, so that they fail: a self-test of the detection path that changes no
+       weight and no output. */
+    int32_t slot_check;
 } stage_config;
 
 /* Weights of one decoder layer: bf16 bit patterns, host or device memory, read only during
@@ -315,7 +331,8 @@ int stage_set_timing(stage *s, int32_t flags);
 
 /* JSON object with counters: calls, tokens, layer loads, bytes streamed through slots and read in
    place (zero copy), block sizes, residency counts, HBM bytes in use, parked tokens and bytes
-   moved by parking, kernels enqueued by prefill/decode calls in all and by the last one. */
+   moved by parking, kernels enqueued by prefill/decode calls in all and by the last one, and the
+   slot tag checks enqueued, run and failed (the last two as of the latest stage_sync). */
 int stage_get_stats(stage *s, char *buf, int32_t cap);
 
 /* Message of the last error on this handle ("" if none); valid until the next call. */

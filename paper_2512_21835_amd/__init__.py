@@ -5,7 +5,7 @@ include/stage.h); ``stage`` is its ctypes binding with the same entry points.
 """
 from .stage import (  # noqa: F401
     StageConfig, StageLayerWeights, StageError, config_for, lib, EXPORTED, LIB_PATH,
-    STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE,
+    STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE, STAGE_ESLOT,
     STAGE_TIME_CALLS, STAGE_TIME_GATEUP, STAGE_TIME_LAYERS, STAGE_MAX_THRESHOLDS, STAGE_MAX_SEQS_PER_CALL,
     STAGE_MAX_CONTEXT, STAGE_MAX_LANES, stage_decode_lane, stage_prefill_lane, stage_decode_noalloc,
     STAGE_NOALLOC_SCRATCH_BYTES,

@@ -140,6 +140,13 @@ bool attention_supported(int group, int head_dim);
 // read it from there instead of carrying it in their arguments).
 hipError_t launch_meta_write(const CallMeta &m, CallMeta *dst, hipStream_t st);
 
+// Slot tags (stage_config.slot_check): tag = {layer, load}, two ints.  The check compares a tag
+// with the expected layer and load and counts into rec[8]: [0] checks run, [1] mismatches, [2..7]
+// the first mismatch (where, slot, expected layer, expected load, found layer, found load).
+hipError_t launch_slot_tag_write(int *tag, int layer, int load, hipStream_t st);
+hipError_t launch_slot_tag_check(const int *tag, int slot, int layer, int load, int where, int *rec,
+                                 hipStream_t st);
+
 // Writes table[idx[i]] = val[i] for i < n (any n; chunked).
 hipError_t launch_table_write(int *table, const int *idx, const int *val, int n, hipStream_t st);
 

@@ -127,6 +127,9 @@ struct stage {
     std::vector<void *> slots;
     std::vector<hipEvent_t> slot_ready[2], slot_free;
     long long loads = 0, calls = 0;
+    // slot tag check (cfg.slot_check): tags [slot][block] = {layer, load}, and the check record
+    int *d_slot_tags = nullptr, *d_slot_rec = nullptr;
+    long long slot_checks = 0, slot_checks_run = 0, slot_check_failures = 0;
     std::vector<int> slot_log, demotion_log, residency_log;
     int thresholds_applied = 0;
     std::vector<int> base_code;  // the allocation: residency last set by stage_load_layer
@@ -325,6 +328,29 @@ int ensure_slots(stage *s) {
     s->slot_ready[kMha] = ra;
     s->slot_ready[kMlp] = rm;
     s->slot_free = fr;
+    if (s->cfg.slot_check) {
+        // every tag starts invalid ({-1, -1}: no layer, no load); the record at zero
+        const size_t tag_bytes = sizeof(int) * 4 * (size_t)S;
+        if (hipMalloc(&s->d_slot_tags, tag_bytes) != hipSuccess || hipMalloc(&s->d_slot_rec, sizeof(int) * 8) != hipSuccess) {
+            (void)hipGetLastError();
+            return s->fail(STAGE_ENOMEM, "cannot allocate the slot tags");
+        }
+        HIP_TRY(hipMemsetAsync(s->d_slot_tags, 0xFF, tag_bytes, s->cs));
+        HIP_TRY(hipMemsetAsync(s->d_slot_rec, 0, sizeof(int) * 8, s->cs));
+        HIP_TRY(hipStreamSynchronize(s->cs));
+    }
+    return STAGE_OK;
+}
+
+int *slot_tag(const stage *s, int slot, int block) { return s->d_slot_tags + 4 * slot + 2 * block; }
+
+// Slot tag check on the compute stream: block `block` of `slot` should hold `layer` from load
+// `load`.  where: 0 / 1 before the MHA / MLP block's first kernel, 2 / 3 after the layer's last.
+int check_slot_tag(stage *s, int slot, int block, int layer, long long load, int where) {
+    int want = (int)(load & 0x7FFFFFFF);
+    if (s->cfg.slot_check == 2 && where == 0) want = (int)((load + 1) & 0x7FFFFFFF);  // self-test
+    HIP_TRY(launch_slot_tag_check(slot_tag(s, slot, block), slot, layer, want, where, s->d_slot_rec, s->cs));
+    s->slot_checks++;
     return STAGE_OK;
 }
 
@@ -661,9 +687,10 @@ int record_event(stage *s, hipStream_t st, hipEvent_t *out) {
     return STAGE_OK;
 }
 
-// Copies the offloaded blocks of `layer` into `slot`, MHA block first, each followed by its
-// ready event.
-int enqueue_copy(stage *s, int layer, int slot) {
+// Copies the offloaded blocks of `layer` into `slot` (load number `load` of the stage's life), MHA
+// block first, each followed by its ready event; with the slot check, each block's tag is
+// invalidated before its copy and set after it.
+int enqueue_copy(stage *s, int layer, int slot, long long load) {
     HIP_TRY(hipStreamWaitEvent(s->xs, s->slot_free[slot], 0));
     for (int b = 0; b < 2; ++b) {
         const Block &k = s->layers[layer].blk[b];
@@ -674,7 +701,10 @@ int enqueue_copy(stage *s, int layer, int slot) {
             if (rc) return rc;
         }
         char *dst = static_cast<char *>(s->slots[slot]) + (b == kMha ? 0 : s->blk_bytes[kMha]);
+        if (s->cfg.slot_check) HIP_TRY(launch_slot_tag_write(slot_tag(s, slot, b), -1, -1, s->xs));
         HIP_TRY(hipMemcpyAsync(dst, k.host, s->blk_bytes[b], hipMemcpyHostToDevice, s->xs));
+        if (s->cfg.slot_check)
+            HIP_TRY(launch_slot_tag_write(slot_tag(s, slot, b), layer, (int)(load & 0x7FFFFFFF), s->xs));
         HIP_TRY(hipEventRecord(s->slot_ready[b][slot], s->xs));
         if (s->cfg.timing & STAGE_TIME_CALLS) {
             int rc = record_event(s, s->xs, &rec.b);
@@ -691,6 +721,8 @@ int enqueue_copy(stage *s, int layer, int slot) {
 struct LayerWeights {
     const uint16_t *mha = nullptr, *mlp = nullptr;
     hipEvent_t mlp_ready = nullptr;
+    int slot = -1;          // the stream slot of a layer with an offloaded block, else -1
+    long long load = -1;    // its load number (slot tag check)
 };
 
 int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int T, const CallMeta *meta,
@@ -724,6 +756,10 @@ int mlp_boundary(stage *s, int layer, const LayerWeights &w) {
         s->recs.push_back(s->open_rec);
     }
     if (w.mlp_ready) HIP_TRY(hipStreamWaitEvent(s->cs, w.mlp_ready, 0));
+    if (w.mlp_ready && s->cfg.slot_check) {
+        int rc = check_slot_tag(s, w.slot, kMlp, layer, w.load, 1);
+        if (rc) return rc;
+    }
     if (timed) {
         s->open_rec = TimeRec{5, layer, nullptr, nullptr};
         int rc = record_event(s, s->cs, &s->open_rec.a);
@@ -1089,7 +1125,7 @@ int run_call_body(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const
     }
     s->loads += n_str;
     for (int j = 0; j < std::min(S, n_str); ++j) {
-        rc = enqueue_copy(s, streamed[j], slot_of(j));
+        rc = enqueue_copy(s, streamed[j], slot_of(j), load0 + j);
         if (rc) return rc;
     }
 
@@ -1116,13 +1152,22 @@ int run_call_body(stage *s, int n_mb, const int32_t *mb_ids, int B, int T, const
             *base[b] = reinterpret_cast<const uint16_t *>(
                 k.resident ? static_cast<const char *>(k.dev) : slot + (b == kMha ? 0 : s->blk_bytes[kMha]));
         }
-        if (!ly.blk[kMha].resident) HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[kMha][sl], 0));
+        w.slot = sl;
+        w.load = load0 + j;
+        const bool check = s->cfg.slot_check != 0;
+        if (!ly.blk[kMha].resident) {
+            HIP_TRY(hipStreamWaitEvent(s->cs, s->slot_ready[kMha][sl], 0));
+            if (check && (rc = check_slot_tag(s, sl, kMha, l, w.load, 0))) return rc;
+        }
         if (!ly.blk[kMlp].resident) w.mlp_ready = s->slot_ready[kMlp][sl];
         rc = run_layer(s, l, w, (int)rows, T, s->d_meta, grid_splits, src, x_out);
         if (rc) return rc;
+        // the layer's kernels are enqueued: its blocks must still hold it (no refill has begun)
+        for (int b = 0; b < 2 && check; ++b)
+            if (!ly.blk[b].resident && (rc = check_slot_tag(s, sl, b, l, w.load, 2 + b))) return rc;
         HIP_TRY(hipEventRecord(s->slot_free[sl], s->cs));
         if (j + S < n_str) {
-            rc = enqueue_copy(s, streamed[j + S], slot_of(j + S));
+            rc = enqueue_copy(s, streamed[j + S], slot_of(j + S), load0 + j + S);
             if (rc) return rc;
         }
         ++j;
@@ -1187,6 +1232,7 @@ const char *stage_strerror(int32_t status) {
         case STAGE_EHIP: return "HIP runtime error";
         case STAGE_ESTATE: return "invalid state for this call";
         case STAGE_ERANGE: return "sequence would exceed max_context";
+        case STAGE_ESLOT: return "slot tag check failed";
         default: return "unknown status";
     }
 }
@@ -1211,7 +1257,7 @@ int stage_init(const stage_config *cfg, stage **out) {
                         c.n_thresholds >= 0 && c.n_thresholds <= STAGE_MAX_THRESHOLDS &&
                         (c.timing & ~kTimeAll) == 0 && (c.zero_copy == 0 || c.zero_copy == 1) &&
                         c.kv_park_tokens >= 0 && c.kv_park_tokens <= c.max_context && c.n_lanes >= 0 &&
-                        c.n_lanes <= STAGE_MAX_LANES;
+                        c.n_lanes <= STAGE_MAX_LANES && c.slot_check >= 0 && c.slot_check <= 2;
     if (!shape_ok || !cap_ok) return STAGE_EINVAL;
     if (c.plan_mode != 0 && c.plan_mode != 1) return STAGE_EINVAL;
     for (int i = 0; i < c.n_thresholds; ++i) {
@@ -1354,7 +1400,7 @@ int stage_destroy(stage *s) {
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
                     (void *)s->ws_hi, (void *)s->ws_lo,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, (void *)s->ws_split, (void *)s->ws_split_ss,
-                    s->ws_dense})
+                    s->ws_dense, (void *)s->d_slot_tags, (void *)s->d_slot_rec})
         if (p) (void)hipFree(p);
     if (s->own_cs && s->cs) (void)hipStreamDestroy(s->cs);
     if (s->own_xs && s->xs) (void)hipStreamDestroy(s->xs);
@@ -1755,6 +1801,25 @@ int stage_sync(stage *s) {
     int rc = sync_all(s);
     if (rc) return rc;
     HIP_TRY(hipGetLastError());
+    if (s->d_slot_rec) {
+        int rec[8];
+        HIP_TRY(hipMemcpy(rec, s->d_slot_rec, sizeof rec, hipMemcpyDeviceToHost));
+        s->slot_checks_run += rec[0];
+        if (rec[0] || rec[1]) {
+            HIP_TRY(hipMemsetAsync(s->d_slot_rec, 0, sizeof rec, s->cs));
+            HIP_TRY(hipStreamSynchronize(s->cs));
+        }
+        if (rec[1]) {
+            static const char *const where[4] = {"before the MHA block's kernels", "before the MLP block's kernels",
+                                                 "after the layer (MHA block)", "after the layer (MLP block)"};
+            s->slot_check_failures += rec[1];
+            return s->fail(STAGE_ESLOT,
+                           "%d slot tag check(s) failed; first: slot %d %s expected layer %d load %d, found "
+                           "layer %d load %d",
+                           rec[1], rec[3], (rec[2] >= 0 && rec[2] < 4) ? where[rec[2]] : "?", rec[4], rec[5],
+                           rec[6], rec[7]);
+        }
+    }
     return STAGE_OK;
 }
 
@@ -1862,11 +1927,13 @@ int stage_get_stats(stage *s, char *buf, int32_t cap) {
         "\"offloaded_mha_blocks\": %d, \"offloaded_mlp_blocks\": %d, "
         "\"stream_slots\": %zu, \"hbm_weight_bytes\": %zu, \"host_weight_bytes\": %zu, \"kv_pool_bytes\": %zu, "
         "\"kv_blocks\": %d, \"kv_blocks_free\": %d, \"parked_tokens\": %lld, \"bytes_parked\": %lld, "
-        "\"bytes_unparked\": %lld, \"kernel_launches\": %lld, \"last_call_kernels\": %lld}",
+        "\"bytes_unparked\": %lld, \"kernel_launches\": %lld, \"last_call_kernels\": %lld, "
+        "\"slot_check\": %d, \"slot_checks\": %lld, \"slot_checks_run\": %lld, \"slot_check_failures\": %lld}",
         s->calls, s->tok_prefill, s->tok_decode, s->loads, s->bytes_streamed, s->bytes_direct, s->blob_bytes,
         s->blk_bytes[kMha], s->blk_bytes[kMlp], res, streamed, off_mha, off_mlp,
         s->slots.size(), hbm_w, host_w, s->kv_layer_stride * s->L, s->n_blocks, (int)s->free_blocks.size(),
-        parked, s->bytes_parked, s->bytes_unparked, s->kernel_launches, s->last_call_kernels);
+        parked, s->bytes_parked, s->bytes_unparked, s->kernel_launches, s->last_call_kernels, s->cfg.slot_check,
+        s->slot_checks, s->slot_checks_run, s->slot_check_failures);
     return (written >= 0 && written < cap) ? STAGE_OK : STAGE_EINVAL;
 }
 

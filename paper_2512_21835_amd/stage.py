@@ -21,7 +21,7 @@ import torch  # noqa: F401  (must precede loading libstage.so)
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstage.so")
 
-STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE = 0, -1, -2, -3, -4, -5
+STAGE_OK, STAGE_EINVAL, STAGE_ENOMEM, STAGE_EHIP, STAGE_ESTATE, STAGE_ERANGE, STAGE_ESLOT = 0, -1, -2, -3, -4, -5, -6
 STAGE_MAX_THRESHOLDS = 32
 STAGE_MAX_SEQS_PER_CALL = 64
 STAGE_MAX_CONTEXT = 16384
@@ -58,6 +58,7 @@ class StageConfig(ctypes.Structure):
         ("plan_mode", c_int32), ("plan_alpha", c_int32 * STAGE_MAX_THRESHOLDS),
         ("plan_beta", c_int32 * STAGE_MAX_THRESHOLDS), ("kv_park_tokens", c_int32),
         ("n_lanes", c_int32), ("lane_streams", c_void_p * STAGE_MAX_LANES),
+        ("slot_check", c_int32),
     ]
 
 
@@ -343,10 +344,11 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
                kv_pool_blocks: int = 0, device: int = 0, compute_stream=None, copy_stream=None,
                timing: int = 0, zero_copy: bool = False,
                plan: Optional[Sequence[Tuple[int, int, int]]] = None, kv_park_tokens: int = 0,
-               n_lanes: int = 1, lane_streams: Optional[Sequence] = None) -> StageConfig:
+               n_lanes: int = 1, lane_streams: Optional[Sequence] = None, slot_check: int = 0) -> StageConfig:
     """A StageConfig for a stage shape (any object with the StageShape fields).  ``plan``:
     planner steps [(tokens, alpha, beta)] (plan_mode 1), instead of ``thresholds``.
-    ``n_lanes`` decode lanes; ``lane_streams[l]``: lane l's stream handle (None: the library's)."""
+    ``n_lanes`` decode lanes; ``lane_streams[l]``: lane l's stream handle (None: the library's).
+    ``slot_check``: the slot tag check mode (0 off, 1 on, 2 self-test)."""
     cfg = stage_config_default()
     cfg.n_layers, cfg.hidden = shape.n_layers, shape.hidden
     cfg.n_q_heads, cfg.n_kv_heads = shape.n_q_heads, shape.n_kv_heads
@@ -377,4 +379,5 @@ def config_for(shape, *, max_microbatches: int, max_batch: int, max_context: int
     cfg.n_lanes = n_lanes
     for l, st in enumerate(lane_streams or ()):
         cfg.lane_streams[l] = st
+    cfg.slot_check = slot_check
     return cfg

@@ -65,6 +65,7 @@ class Scenario:
     zero_copy: bool = False
     residency: Optional[Tuple[int, ...]] = None   # per-layer STAGE_RES_* codes (block granularity)
     plan: Optional[Tuple[Tuple[int, int, int], ...]] = None   # planner steps (tokens, alpha, beta)
+    slot_check: int = 0   # stage_config.slot_check
 
     @property
     def shape(self):
@@ -169,7 +170,7 @@ def _run_gpu(sc: Scenario, device: int, weights, cs_handle, feed=None) -> RunRes
                        n_resident_max=sc.resident_layers(), n_stream_slots=sc.slots, kv_fp32=sc.kv_fp32,
                        thresholds=sc.thresholds, device=device, compute_stream=cs_handle,
                        copy_stream=None, timing=sc.timing, zero_copy=sc.zero_copy,
-                       plan=sc.plan)
+                       plan=sc.plan, slot_check=sc.slot_check)
     h = P.stage_init(cfg)
     res = RunResult()
     try:
