@@ -546,8 +546,11 @@ constexpr int VROW = KT + 8;           // transposed V tile row stride in bf16 (
 // KV head.  Wave w owns rows 32 w .. 32 w + 31 (row r: head r / BQ, position offset r % BQ).
 // Per 32-key tile: S^T = K Q^T (lane = one query column, 16 keys), online softmax in-lane,
 // O^T += V^T P^T with V transposed in LDS.  q and p enter the MFMAs as bf16 hi + lo pairs.
+// Bounded to two wavefronts per SIMD (205 registers): left to itself the compiler takes 276 (the
+// O^T and S^T accumulators in AGPRs), which admits one, and a tile's dependent MFMA chain and
+// softmax then run with nothing to overlap them.
 template <int G, int D>
-__global__ __launch_bounds__(256) void attn_prefill_mfma(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_prefill_mfma(AttnArgs a) {
     constexpr int KROW = D + 8;         // K tile row stride in bf16 (padding)
     constexpr int BQ = 128 / G;
     constexpr int KK = D / 16;          // k16 steps over d
