@@ -41,8 +41,8 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": 940189838,
-                                "source_sha256": "662ff977647f7a9c6b4cd3fd3f1d6f3f4a491b2d7ddb59344bb3c1d41cbe338b"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940189580,
+                                "source_sha256": "14f2cf76152e27dc59759550270a815b1b76531215981cbdb299bf84c8eb0695"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 
