@@ -54,8 +54,10 @@ struct DecodeSmem {
 // Decode: one workgroup per (key split, KV head, row); a split holds at most kChunk keys.  K and V
 // of the lane's keys are fetched together up front, scores are reduced across the D/8 lanes of a
 // key, the split's maximum and sum across the workgroup through LDS once, and the partial output
-// (unnormalised, with its max and sum) goes to global memory for attn_merge_flat.
-template <int G, int D, bool F32KV>
+// (unnormalised, with its max and sum) goes to global memory for attn_merge_flat.  FINAL (every
+// row of the call within one split): the output o / l directly, the value the merge would compute
+// from the single split (weight exp(m - m) = 1), so no merge launch follows.
+template <int G, int D, bool F32KV, bool FINAL>
 __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, int g, int row,
                                                  DecodeSmem<G, D> &sm) {
     constexpr int LPK = D / 8;
@@ -173,6 +175,12 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
     __syncthreads();
     for (int i = tid; i < G * D; i += 256) {
         const int h = i / D, c = i % D;
+        if (FINAL) {
+            const float o_sum = ((sm.o[0][h][c] + sm.o[1][h][c]) + sm.o[2][h][c]) + sm.o[3][h][c];
+            const float l_sum = ((sm.wl[0][h] + sm.wl[1][h]) + sm.wl[2][h]) + sm.wl[3][h];
+            a.out[row * q_ld + (size_t)(g * G + h) * D + c] = o_sum / l_sum;
+            continue;
+        }
         const size_t pi = ((size_t)row * hq_total + g * G + h) * a.max_splits + split;
         a.part_o[pi * D + c] = ((sm.o[0][h][c] + sm.o[1][h][c]) + sm.o[2][h][c]) + sm.o[3][h][c];
         if (c == 0) {
@@ -323,10 +331,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
 }
 
-template <int G, int D, bool F32KV>
+template <int G, int D, bool F32KV, bool FINAL>
 __global__ __launch_bounds__(256) void attn_decode_kernel(AttnArgs a) {
     __shared__ DecodeSmem<G, D> sm;
-    attn_decode_task<G, D, F32KV>(a, blockIdx.x, blockIdx.y, blockIdx.z, sm);
+    attn_decode_task<G, D, F32KV, FINAL>(a, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
 // Merge of the decode splits, one thread per output element (row, query head, column).  The
@@ -407,8 +415,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 // G <= 16): S^T = K Q^T with the K rows of the split's cache blocks as the A operand (one 16-key
 // block per wavefront) and Q as a bf16 hi/lo pair; softmax statistics per head from the MFMA
 // layout; O = P V with P (hi/lo) from LDS and V read transposed from an LDS tile.  Partial
-// outputs as attn_decode_task writes them.
-template <int G, int D>
+// outputs as attn_decode_task writes them, or with FINAL the output o / l.
+template <int G, int D, bool FINAL>
 __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
     static_assert(D == 128 && G <= 16, "one 128-wide head, up to 16 query heads per KV head");
     constexpr int VROW = D + 8;                     // V tile row stride in bf16 (272 bytes)
@@ -524,6 +532,18 @@ __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
         }
     }
     // o[nb][i]: head 4 lq + i, d 32 wave + 16 nb + l16
+    if (FINAL) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int h = 4 * lq + i;
+            if (h >= G) continue;
+            const float l_sum = ((wl[0][h] + wl[1][h]) + wl[2][h]) + wl[3][h];
+            float *op = a.out + (size_t)row * hq_total * D + (size_t)(g * G + h) * D;
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) op[32 * wave + 16 * nb + l16] = o[nb][i] / l_sum;
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int h = 4 * lq + i;
@@ -733,12 +753,21 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
     }
     if (a.split_keys > kChunk || a.max_splits > kMaxDecodeSplits) return hipErrorInvalidValue;
     dim3 grid(a.grid_splits, hkv, a.rows);
+    if (a.grid_splits == 1) {   // every row within one split: its output directly, no merge
+        if (a.kv_fp32)
+            STG_LAUNCH((attn_decode_kernel<G, D, true, true>), grid, dim3(256), 0, st, a);
+        else if constexpr (D == 128)
+            STG_LAUNCH((attn_decode_mfma<G, D, true>), grid, dim3(256), 0, st, a);
+        else
+            STG_LAUNCH((attn_decode_kernel<G, D, false, true>), grid, dim3(256), 0, st, a);
+        return hipGetLastError();
+    }
     if (a.kv_fp32)
-        STG_LAUNCH((attn_decode_kernel<G, D, true>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_kernel<G, D, true, false>), grid, dim3(256), 0, st, a);
     else if constexpr (D == 128)
-        STG_LAUNCH((attn_decode_mfma<G, D>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_mfma<G, D, false>), grid, dim3(256), 0, st, a);
     else
-        STG_LAUNCH((attn_decode_kernel<G, D, false>), grid, dim3(256), 0, st, a);
+        STG_LAUNCH((attn_decode_kernel<G, D, false, false>), grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t n_out = (size_t)a.rows * a.n_q_heads * D;

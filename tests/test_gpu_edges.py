@@ -154,3 +154,60 @@ def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32, hist):
                 assert P.stage_get_length(h, m, 0) == n + 2 == orc.length(f"s{m}")
         finally:
             P.stage_destroy(h)
+
+
+@pytest.mark.parametrize("shape_name,kv_fp32", [("tiny", False), ("tiny", True), ("llama8b", False),
+                                                ("llama8b", True)])
+def test_single_split_rows_give_the_merged_bits(shape_name, kv_fp32):
+    """Decode attention writes a row's output straight from its one split (o / l, no merge launch)
+    when every row of the call fits one 64-key split, and merges the splits otherwise; for a row
+    that fits one split the two give the same bits (the merge of a single split weighs it by
+    exp(m - m) = 1).  Row 0 (contexts 31 and 32) is decoded alone, then together with row 1
+    (contexts 301 and 302: 5 splits), both on the vector GEMV engine (1 and 2 rows).  tiny: 64-wide
+    heads (vector attention kernel); llama8b: 128-wide heads (the matrix-core kernel with a bf16
+    cache, the vector one with fp32)."""
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+
+    shape = synth.TINY if shape_name == "tiny" else synth.LLAMA8B_STAGE
+    w = weights_of(shape)
+    L, hkv, d, H = shape.n_layers, shape.n_kv_heads, shape.head_dim, shape.hidden
+    hist = (30, 300)
+    kv = []
+    for m, n in enumerate(hist):
+        seed = synth.seed_of(0xE7, m, n)
+        kv.append((synth.normal_bf16(seed, (L, n, hkv, d)), synth.normal_bf16(seed + 1, (L, n, hkv, d))))
+    xs = [synth.normal_f32(synth.seed_of(0xE8, step, 2), (2, H)) for step in range(2)]
+
+    def run(rows):
+        outs = []
+        with compute_stream() as cs:
+            cfg = P.config_for(shape, max_microbatches=2, max_batch=1, max_context=400, n_resident_max=L,
+                               kv_fp32=kv_fp32, compute_stream=cs.handle)
+            h = P.stage_init(cfg)
+            try:
+                for l in range(L):
+                    P.stage_load_layer(h, l, w(l), 1)
+                for m, (k, v) in enumerate(kv):
+                    if kv_fp32:
+                        kd = torch.from_numpy(synth.bf16_to_f32(k)).cuda()
+                        vd = torch.from_numpy(synth.bf16_to_f32(v)).cuda()
+                    else:
+                        kd = torch.from_numpy(k.view(np.int16)).cuda()
+                        vd = torch.from_numpy(v.view(np.int16)).cuda()
+                    P.stage_kv_append(h, m, 0, hist[m], kd, vd)
+                for x in xs:
+                    xd = torch.from_numpy(np.ascontiguousarray(x[:rows])).cuda().reshape(rows, 1, H)
+                    yd = torch.empty_like(xd)
+                    P.stage_decode(h, list(range(rows)), 1, xd, yd)
+                    P.stage_sync(h)
+                    outs.append(yd.cpu().numpy().reshape(rows, H))
+            finally:
+                P.stage_destroy(h)
+        return outs
+
+    alone, mixed = run(1), run(2)
+    for step in range(2):
+        assert np.isfinite(alone[step]).all()
+        assert np.array_equal(alone[step][0], mixed[step][0]), f"step {step}"
