@@ -91,3 +91,30 @@ def test_slot_check_self_test_reports_mismatches():
             finally:
                 P.stage_destroy(h)
     assert np.array_equal(outs[0], outs[2])
+
+
+@pytest.mark.parametrize("kind", ["thresholds", "planner", "zero_copy"])
+def test_slot_check_under_changing_residency(kind):
+    """The tags follow the stage's own slot use when residency changes between calls (threshold
+    demotions; planner steps that offload and reload blocks) and when only prefills stage (zero
+    copy decode): every check passes, and the outputs equal the unchecked stage's."""
+    _gpu()
+    tiny = synth.Workload("tiny_slotcheck", 105, synth.TINY, n_mb=3, batch=2, prefill=37, decode_steps=6)
+    if kind == "thresholds":
+        base = Scenario(tiny, prefill=37, decode_steps=6, calls="one", thresholds=(39, 40, 41))
+    elif kind == "planner":
+        # held tokens grow 37 per prefill and 2 per decode call: the steps offload one MHA block,
+        # then one MLP block and reload the MHA block
+        base = Scenario(tiny, prefill=37, decode_steps=6, calls="one", residency=(1, 1),
+                        plan=((100, 1, 0), (230, 0, 1)))
+    else:
+        base = Scenario(tiny, prefill=37, decode_steps=6, calls="one", n_resident=0, zero_copy=True)
+    ref = run_gpu(base)
+    got = run_gpu(dataclasses.replace(base, slot_check=1))
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    assert got.slot_log == ref.slot_log and got.residency_log == ref.residency_log
+    st = got.stats
+    assert st["slot_checks"] > 0
+    assert st["slot_checks_run"] == st["slot_checks"]
+    assert st["slot_check_failures"] == 0
