@@ -211,3 +211,17 @@ def test_single_split_rows_give_the_merged_bits(shape_name, kv_fp32):
     for step in range(2):
         assert np.isfinite(alone[step]).all()
         assert np.array_equal(alone[step][0], mixed[step][0]), f"step {step}"
+
+
+# One narrow layer whose prefill gate/up GEMM (M = 2000 rows, 2F = 8000 gate/up rows: ragged in both
+# dimensions) still fills the GPU with 256 x 256 tiles, over K = 64 or 96: the software-pipelined k
+# loop with two tiles (only its peeled tail) and with three (one pass of the loop body).
+NARROW_H64 = synth.StageShape("narrow-1L-h64", 3, 1, 64, 1, 1, 64, 4000)
+NARROW_H96 = synth.StageShape("narrow-1L-h96", 4, 1, 96, 1, 1, 64, 4000)
+
+
+@pytest.mark.parametrize("shape", [NARROW_H64, NARROW_H96], ids=["k64", "k96"])
+def test_prefill_gemm_shortest_pipelined_k_loops(shape):
+    _gpu()
+    plan = [("prefill", 2000), ("decode", 1)]
+    _check(f"{shape.name} prefill 2000", _run(shape, plan, False, 5, 2048))
