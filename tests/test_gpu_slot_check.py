@@ -118,3 +118,23 @@ def test_slot_check_under_changing_residency(kind):
     assert st["slot_checks"] > 0
     assert st["slot_checks_run"] == st["slot_checks"]
     assert st["slot_check_failures"] == 0
+
+
+def test_slot_check_on_the_70b_streamed_stage():
+    """The 70B-shaped stage with 4 resident and 12 streamed layers through 2 slots, its copies
+    overlapping compute on the library's own copy stream: 4 micro-batches, a 64-token prefill each
+    in one call, then 16 decode calls of all four.  Every tag check passes (each call refills the
+    two slots six times each while the previous layer's kernels still read the other), and the
+    outputs equal the unchecked stage's."""
+    _gpu()
+    wl = synth.WORKLOADS["llama70b_offload"]
+    base = Scenario(wl, prefill=64, decode_steps=16, calls="all", n_resident=4)
+    ref = run_gpu(base)
+    got = run_gpu(dataclasses.replace(base, slot_check=1))
+    for a, b in zip(got.outputs, ref.outputs):
+        assert np.array_equal(a, b)
+    st = got.stats
+    assert st["layer_loads"] == 12 * 17
+    assert st["slot_checks"] == 17 * 12 * 4      # 12 streamed layers x 2 blocks x (before + after)
+    assert st["slot_checks_run"] == st["slot_checks"]
+    assert st["slot_check_failures"] == 0
