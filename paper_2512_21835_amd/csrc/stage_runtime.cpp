@@ -308,6 +308,20 @@ int ensure_slots(stage *s) {
     if (!s->slots.empty()) return STAGE_OK;
     const int S = s->cfg.n_stream_slots;
     if (S < 1) return s->fail(STAGE_EINVAL, "a layer is offloaded but n_stream_slots is 0");
+    if (s->cfg.slot_check && !s->d_slot_tags) {
+        // first, so that a stage never holds slots without their tags: every tag starts invalid
+        // ({-1, -1}: no layer, no load), the record at zero
+        const size_t tag_bytes = sizeof(int) * 4 * (size_t)S;
+        if (hipMalloc(&s->d_slot_tags, tag_bytes) != hipSuccess || hipMalloc(&s->d_slot_rec, sizeof(int) * 8) != hipSuccess) {
+            (void)hipGetLastError();
+            if (s->d_slot_tags) (void)hipFree(s->d_slot_tags);
+            s->d_slot_tags = nullptr;
+            return s->fail(STAGE_ENOMEM, "cannot allocate the slot tags");
+        }
+        HIP_TRY(hipMemsetAsync(s->d_slot_tags, 0xFF, tag_bytes, s->cs));
+        HIP_TRY(hipMemsetAsync(s->d_slot_rec, 0, sizeof(int) * 8, s->cs));
+        HIP_TRY(hipStreamSynchronize(s->cs));
+    }
     std::vector<void *> sl(S, nullptr);
     std::vector<hipEvent_t> ra(S, nullptr), rm(S, nullptr), fr(S, nullptr);
     for (int i = 0; i < S; ++i) {
@@ -328,17 +342,6 @@ int ensure_slots(stage *s) {
     s->slot_ready[kMha] = ra;
     s->slot_ready[kMlp] = rm;
     s->slot_free = fr;
-    if (s->cfg.slot_check) {
-        // every tag starts invalid ({-1, -1}: no layer, no load); the record at zero
-        const size_t tag_bytes = sizeof(int) * 4 * (size_t)S;
-        if (hipMalloc(&s->d_slot_tags, tag_bytes) != hipSuccess || hipMalloc(&s->d_slot_rec, sizeof(int) * 8) != hipSuccess) {
-            (void)hipGetLastError();
-            return s->fail(STAGE_ENOMEM, "cannot allocate the slot tags");
-        }
-        HIP_TRY(hipMemsetAsync(s->d_slot_tags, 0xFF, tag_bytes, s->cs));
-        HIP_TRY(hipMemsetAsync(s->d_slot_rec, 0, sizeof(int) * 8, s->cs));
-        HIP_TRY(hipStreamSynchronize(s->cs));
-    }
     return STAGE_OK;
 }
 
