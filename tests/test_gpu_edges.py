@@ -225,3 +225,18 @@ def test_prefill_gemm_shortest_pipelined_k_loops(shape):
     _gpu()
     plan = [("prefill", 2000), ("decode", 1)]
     _check(f"{shape.name} prefill 2000", _run(shape, plan, False, 5, 2048))
+
+
+# Every attention instance the library builds (query heads per KV head G in 1, 2, 4, 8; head
+# width 64 or 128): one small layer, prefill 70 (three 32-key tiles, ragged; a 128-row query block
+# of 128 / G positions) then two decode steps at contexts 71 and 72 (two 64-key splits and their
+# merge), bf16 cache, against the oracle.
+_GD = [(g, d) for d in (64, 128) for g in (1, 2, 4, 8)]
+
+
+@pytest.mark.parametrize("g,d", _GD, ids=[f"G{g}-d{d}" for g, d in _GD])
+def test_every_attention_group_and_head_width(g, d):
+    _gpu()
+    shape = synth.StageShape(f"gqa-g{g}-d{d}", 10 + 10 * g + d // 64, 1, 256, 2 * g, 2, d, 512)
+    plan = [("prefill", 70), ("decode", 1), ("decode", 1)]
+    _check(f"{shape.name}", _run(shape, plan, False, 6, 80))
