@@ -228,15 +228,15 @@ def test_prefill_gemm_shortest_pipelined_k_loops(shape):
 
 
 # Every attention instance the library builds (query heads per KV head G in 1, 2, 4, 8; head
-# width 64 or 128): one small layer, prefill 70 (three 32-key tiles, ragged; a 128-row query block
-# of 128 / G positions) then two decode steps at contexts 71 and 72 (two 64-key splits and their
-# merge), bf16 cache, against the oracle.
-_GD = [(g, d) for d in (64, 128) for g in (1, 2, 4, 8)]
+# width 64 or 128; bf16 or fp32 cache): one small layer, prefill 70 (three 32-key tiles, ragged;
+# a 128-row query block of 128 / G positions) then two decode steps at contexts 71 and 72 (two
+# 64-key splits and their merge), against the oracle.
+_GD = [(g, d, f32) for f32 in (False, True) for d in (64, 128) for g in (1, 2, 4, 8)]
 
 
-@pytest.mark.parametrize("g,d", _GD, ids=[f"G{g}-d{d}" for g, d in _GD])
-def test_every_attention_group_and_head_width(g, d):
+@pytest.mark.parametrize("g,d,kv_fp32", _GD, ids=[f"G{g}-d{d}-{'f32' if f else 'bf16'}" for g, d, f in _GD])
+def test_every_attention_group_and_head_width(g, d, kv_fp32):
     _gpu()
     shape = synth.StageShape(f"gqa-g{g}-d{d}", 10 + 10 * g + d // 64, 1, 256, 2 * g, 2, d, 512)
     plan = [("prefill", 70), ("decode", 1), ("decode", 1)]
-    _check(f"{shape.name}", _run(shape, plan, False, 6, 80))
+    _check(f"{shape.name} kv_fp32={kv_fp32}", _run(shape, plan, kv_fp32, 6, 80))
