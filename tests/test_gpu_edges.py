@@ -240,3 +240,47 @@ def test_every_attention_group_and_head_width(g, d, kv_fp32):
     shape = synth.StageShape(f"gqa-g{g}-d{d}", 10 + 10 * g + d // 64, 1, 256, 2 * g, 2, d, 512)
     plan = [("prefill", 70), ("decode", 1), ("decode", 1)]
     _check(f"{shape.name} kv_fp32={kv_fp32}", _run(shape, plan, kv_fp32, 6, 80))
+
+
+# Decode calls of 1 to 16 rows on one small layer whose projections can run on either engine
+# (K a multiple of 128): the vector kernel's 1-, 2-, 4- and 8-row instances, the matrix-core
+# engine from 3 rows (5 for the O projection), its split and unsplit launches; every row against
+# the oracle.
+ROWS_SHAPE = synth.StageShape("rows-1L-h256", 5, 1, 256, 4, 2, 64, 512)
+
+
+@pytest.mark.parametrize("rows", [1, 2, 3, 4, 5, 7, 8, 9, 16])
+def test_decode_rows_on_both_engines(rows):
+    _gpu()
+    import torch
+    import paper_2512_21835_amd as P
+    from oracle.stage_oracle import OracleStage
+
+    shape = ROWS_SHAPE
+    w = weights_of(shape)
+    H = shape.hidden
+    orc = OracleStage(shape, w, kv_dtype="bf16")
+    with compute_stream() as cs:
+        cfg = P.config_for(shape, max_microbatches=16, max_batch=1, max_context=64, n_resident_max=1,
+                           compute_stream=cs.handle)
+        h = P.stage_init(cfg)
+        try:
+            P.stage_load_layer(h, 0, w(0), 1)
+            for m in range(rows):
+                n = 20 + m   # ragged histories
+                x = synth.normal_f32(synth.seed_of(0xE9, m, n), (n, H))
+                xd = torch.from_numpy(x).cuda().reshape(1, 1, n, H)
+                P.stage_prefill(h, [m], 1, n, xd, torch.empty_like(xd))
+                orc.forward([(f"s{m}", x)])
+            x = synth.normal_f32(synth.seed_of(0xEA, rows, 1), (rows, H))
+            xd = torch.from_numpy(x).cuda().reshape(rows, 1, H)
+            yd = torch.empty_like(xd)
+            P.stage_decode(h, list(range(rows)), 1, xd, yd)
+            P.stage_sync(h)
+            got = yd.cpu().numpy().reshape(rows, H)
+        finally:
+            P.stage_destroy(h)
+    want = orc.forward([(f"s{m}", x[m:m + 1]) for m in range(rows)])
+    for m in range(rows):
+        cmp = compare(got[m:m + 1], want[m], x[m:m + 1], x[m:m + 1])
+        assert cmp["max_abs"] <= TOL_ABS and cmp["cos"] >= TOL_COS and cmp["cos_delta"] >= TOL_COS, (rows, m, cmp)
