@@ -242,14 +242,15 @@ def test_every_attention_group_and_head_width(g, d, kv_fp32):
     _check(f"{shape.name} kv_fp32={kv_fp32}", _run(shape, plan, kv_fp32, 6, 80))
 
 
-# Decode calls of 1 to 16 rows on one small layer whose projections can run on either engine
+# Decode calls of 1 to 40 rows on one small layer whose projections can run on either engine
 # (K a multiple of 128): the vector kernel's 1-, 2-, 4- and 8-row instances, the matrix-core
-# engine from 3 rows (5 for the O projection), its split and unsplit launches; every row against
-# the oracle.
+# engine from 3 rows (5 for the O projection), its split and unsplit launches, and calls of more
+# than 16 rows cut into several launches (17: 16 + 1; 40: 16 + 16 + 8); every row against the
+# oracle.
 ROWS_SHAPE = synth.StageShape("rows-1L-h256", 5, 1, 256, 4, 2, 64, 512)
 
 
-@pytest.mark.parametrize("rows", [1, 2, 3, 4, 5, 7, 8, 9, 16])
+@pytest.mark.parametrize("rows", [1, 2, 3, 4, 5, 7, 8, 9, 16, 17, 40])
 def test_decode_rows_on_both_engines(rows):
     _gpu()
     import torch
@@ -261,13 +262,13 @@ def test_decode_rows_on_both_engines(rows):
     H = shape.hidden
     orc = OracleStage(shape, w, kv_dtype="bf16")
     with compute_stream() as cs:
-        cfg = P.config_for(shape, max_microbatches=16, max_batch=1, max_context=64, n_resident_max=1,
+        cfg = P.config_for(shape, max_microbatches=40, max_batch=1, max_context=64, n_resident_max=1,
                            compute_stream=cs.handle)
         h = P.stage_init(cfg)
         try:
             P.stage_load_layer(h, 0, w(0), 1)
             for m in range(rows):
-                n = 20 + m   # ragged histories
+                n = 20 + m % 23   # ragged histories
                 x = synth.normal_f32(synth.seed_of(0xE9, m, n), (n, H))
                 xd = torch.from_numpy(x).cuda().reshape(1, 1, n, H)
                 P.stage_prefill(h, [m], 1, n, xd, torch.empty_like(xd))
