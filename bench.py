@@ -187,7 +187,7 @@ def cpu_model() -> str:
 
 
 # ---------------------------------------------------------------------------------------------- legs
-def cpu_baseline(layers_timed: int = 2, ctx: int = 2048):
+def cpu_baseline(layers_timed: int = 8, ctx: int = 2048):
     """The float64 oracle as it stands, single-threaded, timed per unit on the headline workload
     and extrapolated: one decode step of one sequence at context `ctx` (its cache filled with seeded
     K/V) through `layers_timed` of the 16 70B-shaped layers (each layer's bf16 weights widened as the
@@ -870,8 +870,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--prefill", type=int, default=2048, help="prefill tokens per micro-batch of the headline")
     ap.add_argument("--other-rounds", type=int, default=8, help="timed rounds of the other 70B groupings (0 = skip)")
-    ap.add_argument("--cpu-layers", type=int, default=2,
-                    help="70B-shaped layers the oracle is timed on for cpu_baseline (0 = skip)")
+    ap.add_argument("--cpu-layers", type=int, default=8,
+                    help="70B-shaped layers the oracle is timed on for cpu_baseline, about 1.2 s each "
+                         "(0 = skip)")
     ap.add_argument("--c2-steps", type=int, default=128, help="timed decode steps of the 8B-shaped leg (0 = skip)")
     ap.add_argument("--c1-steps", type=int, default=256, help="timed decode steps of the tiny leg (0 = skip)")
     ap.add_argument("--offload-calls", type=int, default=3, help="timed calls of the offloaded 70B leg (0 = skip)")
