@@ -11,10 +11,10 @@
 // cores (flash-attention tiling, below); with an fp32 cache (the parity mode), attn_kernel: one
 // workgroup per (row, KV head) walks all of the row's keys.  Decode (split_keys > 0): the context is
 // cut into splits of split_keys keys so that one token's attention still fills the GPU, and a
-// second launch (attn_merge_flat) merges each row's splits in ascending order.  With a bf16
-// cache and 128-wide heads the splits run on the matrix cores (attn_decode_mfma: the G query
-// heads of a KV head are the N dimension of S^T = K Q^T, then O = P V; with G = 8 the vector form
-// spends 16 multiply-adds per cached element and is bound by them); otherwise attn_decode_kernel.
+// second launch (attn_merge) merges each row's splits.  With a bf16 cache and 128-wide heads the
+// splits run on the matrix cores (attn_decode_mfma: the G query heads of a KV head are the N
+// dimension of S^T = K Q^T, then O = P V; with G = 8 the vector form spends 16 multiply-adds per
+// cached element and is bound by them); otherwise attn_decode_kernel.
 #include <hip/hip_runtime.h>
 
 #include "lanes.h"
@@ -54,7 +54,7 @@ struct DecodeSmem {
 // Decode: one workgroup per (key split, KV head, row); a split holds at most kChunk keys.  K and V
 // of the lane's keys are fetched together up front, scores are reduced across the D/8 lanes of a
 // key, the split's maximum and sum across the workgroup through LDS once, and the partial output
-// (unnormalised, with its max and sum) goes to global memory for attn_merge_flat.  FINAL (every
+// (unnormalised, with its max and sum) goes to global memory for attn_merge.  FINAL (every
 // row of the call within one split): the output o / l directly, the value the merge would compute
 // from the single split (weight exp(m - m) = 1), so no merge launch follows.
 template <int G, int D, bool F32KV, bool FINAL>
@@ -337,60 +337,96 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnArgs a) {
     attn_decode_task<G, D, F32KV, FINAL>(a, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
-// Merge of the decode splits, one thread per output element (row, query head, column).  The
-// splits' (max, sum) pairs and partial outputs are loaded kMergeChunk at a time, all in flight
-// together and before the row's split count is known (addresses clamped to the call's longest
-// row, a.grid_splits): one round trip for contexts up to kMergeChunk splits.  Across chunks the
-// running sums are rescaled to the new maximum; within one chunk the weight of split s is
-// exp(m_s - max), and the numerator and denominator add the splits in ascending order.
-constexpr int kMergeChunk = 32;
+// Merge of the decode splits: one workgroup per (row, query head).  Thread t owns the 4 output
+// columns 4 (t % (D/4)) .. + 3 and the splits s with s % SL == t / (D/4) (SL = 1024 / D split
+// lanes: 8 for 128-wide heads, 16 for 64-wide).  Per round of kMergePer splits per lane it issues
+// the loads of all of them at once (addresses clamped to the call's longest row, a.grid_splits),
+// before the row's own split count arrives from the metadata: one round trip for contexts up to
+// kMergePer * SL splits.  A lane merges its splits in ascending order (online: rescaled to the
+// running maximum; weight exp(m_s - max)); the SL lane states then meet in LDS and are added in
+// lane order.  The order depends on the row's split count only, never on the other rows of the
+// call; for a single split the result is exactly o / l (weights exp(0) = 1, empty lanes add 0).
+constexpr int kMergePer = 8;
 template <int D>
-__global__ __launch_bounds__(256) void attn_merge_flat(AttnArgs a) {
-    const int hq_total = a.n_q_heads;
-    const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= (size_t)a.rows * hq_total * D) return;
-    const int c = (int)(e % D);
-    const size_t rh = e / D;
-    const int hq = (int)(rh % hq_total), row = (int)(rh / hq_total);
+__global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
+    constexpr int CG = D / 4, SL = 256 / CG;
+    __shared__ float s_m[SL][CG], s_l[SL][CG];
+    __shared__ float4 s_o[SL][CG];
+    const int cg = threadIdx.x % CG, sl = threadIdx.x / CG;
+    const int hq = blockIdx.x, row = blockIdx.y, hq_total = a.n_q_heads;
     const size_t pi0 = ((size_t)row * hq_total + hq) * a.max_splits;
     const float2 *ml = reinterpret_cast<const float2 *>(a.part_ml) + pi0;
-    const float *po = a.part_o + pi0 * D + c;
+    const float4 *po = reinterpret_cast<const float4 *>(a.part_o + pi0 * D) + cg;
     const int lim = a.grid_splits;
-    float mx = -INFINITY, den = 0.f, num = 0.f;
+    float mx = -INFINITY, den = 0.f;
+    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
     int nsp = -1;
-    for (int s0 = 0; s0 < lim; s0 += kMergeChunk) {
-        float2 v[kMergeChunk];
-        float o[kMergeChunk];
+    for (int s0 = 0; s0 < lim; s0 += kMergePer * SL) {
+        const int nper = min(kMergePer, (lim - s0 + SL - 1) / SL);  // same for every thread
+        float2 v[kMergePer];
+        float4 o[kMergePer];
 #pragma unroll
-        for (int j = 0; j < kMergeChunk; ++j) {
-            const int sp = min(s0 + j, lim - 1);
-            v[j] = ml[sp];
-            o[j] = po[(size_t)sp * D];
-        }
+        for (int j = 0; j < kMergePer; ++j)
+            if (j < nper) {
+                const int s = min(s0 + j * SL + sl, lim - 1);
+                v[j] = ml[s];
+                o[j] = po[(size_t)s * (D / 4)];
+            }
         if (nsp < 0) {
             const int sidx = row / a.meta->rows_per_seq;
             const int ctx = a.meta->pos0[sidx] + row % a.meta->rows_per_seq + 1;
-            nsp = (ctx + a.split_keys - 1) / a.split_keys;
+            nsp = min((ctx + a.split_keys - 1) / a.split_keys, lim);
         }
         if (s0 >= nsp) break;
-        const int n = min(kMergeChunk, nsp - s0);
         float m = mx;
 #pragma unroll
-        for (int j = 0; j < kMergeChunk; ++j)
-            if (j < n) m = fmaxf(m, v[j].x);
-        const float r = expf(mx - m);  // 0 on the first chunk (mx = -inf, m finite)
-        den *= r;
-        num *= r;
+        for (int j = 0; j < kMergePer; ++j)
+            if (j < nper && s0 + j * SL + sl < nsp) m = fmaxf(m, v[j].x);
+        if (m > -INFINITY) {  // this lane holds a split of the row
+            const float r = expf(mx - m);  // 0 on the lane's first split (mx = -inf)
+            den *= r;
+            num.x *= r;
+            num.y *= r;
+            num.z *= r;
+            num.w *= r;
 #pragma unroll
-        for (int j = 0; j < kMergeChunk; ++j)
-            if (j < n) {
-                const float w = expf(v[j].x - m);
-                den = fmaf(w, v[j].y, den);
-                num = fmaf(w, o[j], num);
-            }
-        mx = m;
+            for (int j = 0; j < kMergePer; ++j)
+                if (j < nper && s0 + j * SL + sl < nsp) {
+                    const float w = expf(v[j].x - m);
+                    den = fmaf(w, v[j].y, den);
+                    num.x = fmaf(w, o[j].x, num.x);
+                    num.y = fmaf(w, o[j].y, num.y);
+                    num.z = fmaf(w, o[j].z, num.z);
+                    num.w = fmaf(w, o[j].w, num.w);
+                }
+            mx = m;
+        }
     }
-    a.out[(size_t)row * hq_total * D + (size_t)hq * D + c] = num / den;
+    s_m[sl][cg] = mx;
+    s_l[sl][cg] = den;
+    s_o[sl][cg] = num;
+    __syncthreads();
+    if (sl != 0) return;
+    float M = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < SL; ++i) M = fmaxf(M, s_m[i][cg]);
+    float L = 0.f;
+    float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int i = 0; i < SL; ++i) {
+        const float mi = s_m[i][cg];
+        if (mi > -INFINITY) {
+            const float w = expf(mi - M);
+            const float4 oi = s_o[i][cg];
+            L = fmaf(w, s_l[i][cg], L);
+            O.x = fmaf(w, oi.x, O.x);
+            O.y = fmaf(w, oi.y, O.y);
+            O.z = fmaf(w, oi.z, O.z);
+            O.w = fmaf(w, oi.w, O.w);
+        }
+    }
+    *reinterpret_cast<float4 *>(a.out + (size_t)row * hq_total * D + (size_t)hq * D + 4 * cg) =
+        make_float4(O.x / L, O.y / L, O.z / L, O.w / L);
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -770,8 +806,7 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
         STG_LAUNCH((attn_decode_kernel<G, D, false, false>), grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t n_out = (size_t)a.rows * a.n_q_heads * D;
-    STG_LAUNCH((attn_merge_flat<D>), dim3((unsigned)((n_out + 255) / 256)), dim3(256), 0, st, a);
+    STG_LAUNCH((attn_merge<D>), dim3((unsigned)a.n_q_heads, (unsigned)a.rows), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

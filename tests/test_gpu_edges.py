@@ -102,14 +102,16 @@ def test_decode_at_the_largest_context(kv_fp32):
 
 
 @pytest.mark.parametrize("kv_fp32,hist", [(False, (37, 200, 1100)), (True, (37, 200, 1100)),
-                                          (False, (2047, 2049, 4161))])
+                                          (False, (2047, 4095, 4161))])
 def test_llama8b_ragged_contexts_in_one_decode_call(kv_fp32, hist):
     """8B-shaped stage: three sequences with `hist` positions appended, decoded together for two
     steps (3 rows per call: the matrix-core GEMVs; with the bf16 cache the matrix-core attention).
     (37, 200, 1100): the rows span 1, 4 and 18 attention splits, so workgroups of the shorter rows
-    exit early and every row's last split is ragged.  (2047, 2049, 4161): 32 to 66 splits, so the
-    merge's 32-split load batches end exactly at, just past and well past a batch boundary.  Each
-    row is checked against the oracle."""
+    exit early and every row's last split is ragged.  (2047, 4095, 4161): with 32, 64 and 66
+    splits (33, 65 and 66 on the second step) a row's last split falls well inside, exactly at the
+    end of and just past the merge's first round of loads (8 splits on each of 8 lanes, 64 in all),
+    and 33 splits leave lanes 1-7 one split short of lane 0.  Each row is checked against the
+    oracle."""
     _gpu()
     import torch
     import paper_2512_21835_amd as P
