@@ -64,18 +64,27 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
     constexpr int KPW = 64 / LPK;
     constexpr int KPS = 4 * KPW;
     constexpr int STEPS = kChunk / KPS;
-    const int sidx = row / a.meta->rows_per_seq;
-    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
-    const int slot = a.meta->seq_slot[sidx];
-    const int ctx = pos + 1;
-    const int kbeg = split * a.split_keys;
-    if (kbeg >= ctx) return;
-    const int n = min(a.split_keys, ctx - kbeg);
-
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int kl = lane / LPK, sub = lane % LPK, c0 = sub * 8;
     const int hq_total = a.n_q_heads;
     const size_t q_ld = (size_t)hq_total * D;
+    // the queries first: they depend on the row only
+    const float scale = 1.f / sqrtf((float)D);
+    float q[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const float *qp = a.q + row * q_ld + (size_t)(g * G + h) * D + c0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) q[h][j] = qp[j] * scale;
+    }
+    const int sidx = row / a.rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.rows_per_seq;
+    const int slot = a.meta->seq_slot[sidx];
+    const int ctx = pos + 1;
+    const int kbeg = split * a.split_keys;
+    if (kbeg >= ctx || slot < 0) return;  // (slot tested so that both metadata loads go out together)
+    const int n = min(a.split_keys, ctx - kbeg);
+
     const int hkv = a.kv.n_kv_heads;
     const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
     const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
@@ -97,14 +106,7 @@ __device__ __forceinline__ void attn_decode_task(const AttnArgs &a, int split, i
         load8<F32KV>(a.kv.pool, e, kf[st]);
         load8<F32KV>(a.kv.pool, e + (size_t)hkv * kBlockTokens * D, vf[st]);
     }
-    const float scale = 1.f / sqrtf((float)D);
-    float q[G][8];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        const float *qp = a.q + row * q_ld + (size_t)(g * G + h) * D + c0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) q[h][j] = qp[j] * scale;
-    }
+    __builtin_amdgcn_sched_barrier(0);  // every K and V load in flight before any is used
 
     float sc[STEPS][G];
 #pragma unroll
@@ -373,8 +375,8 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
                 o[j] = po[(size_t)s * (D / 4)];
             }
         if (nsp < 0) {
-            const int sidx = row / a.meta->rows_per_seq;
-            const int ctx = a.meta->pos0[sidx] + row % a.meta->rows_per_seq + 1;
+            const int sidx = row / a.rows_per_seq;
+            const int ctx = a.meta->pos0[sidx] + row % a.rows_per_seq + 1;
             nsp = min((ctx + a.split_keys - 1) / a.split_keys, lim);
         }
         if (s0 >= nsp) break;
@@ -460,53 +462,62 @@ __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
     __shared__ uint4 pf[2][2][64];                  // P A-fragments [key step][hi, lo][lane]
     __shared__ float wm[4][16], wl[4][16];
     const int split = blockIdx.x, g = blockIdx.y, row = blockIdx.z;
-    const int sidx = row / a.meta->rows_per_seq;
-    const int pos = a.meta->pos0[sidx] + row % a.meta->rows_per_seq;
+    const int lane = threadIdx.x & 63, l16 = lane & 15, lq = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int hq_total = a.n_q_heads, hkv = a.kv.n_kv_heads;
+    // Q^T fragments first (they depend on the row only): head l16 (heads past G load head G - 1 and
+    // are zeroed below), d 32 s + 8 lq
+    const float *qp = a.q + (size_t)row * hq_total * D + (size_t)(g * G + min(l16, G - 1)) * D + 8 * lq;
+    float4 qv[4][2];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        qv[s][0] = *reinterpret_cast<const float4 *>(qp + 32 * s);
+        qv[s][1] = *reinterpret_cast<const float4 *>(qp + 32 * s + 4);
+    }
+    const int sidx = row / a.rows_per_seq;
+    const int pos = a.meta->pos0[sidx] + row % a.rows_per_seq;
     const int slot = a.meta->seq_slot[sidx];
     const int ctx = pos + 1, kbeg = split * a.split_keys;
-    if (kbeg >= ctx) return;
+    if (kbeg >= ctx || slot < 0) return;  // (slot tested so that both metadata loads go out together)
     const int n = min(a.split_keys, ctx - kbeg);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int hq_total = a.n_q_heads, hkv = a.kv.n_kv_heads;
-    const int *table = a.kv.block_table + (size_t)slot * a.kv.max_blocks;
     const size_t blk_stride = (size_t)2 * hkv * kBlockTokens * D;
     const uint16_t *pool = static_cast<const uint16_t *>(a.kv.pool);
-    const int l16 = lane & 15, lq = lane >> 4;
+    // every key of wavefront w (16 w .. 16 w + 15 of the split, clamped into it) lies in one cache
+    // block (splits start on a block boundary): one block-table entry per wavefront
+    const int blk = a.kv.block_table[(size_t)slot * a.kv.max_blocks + (kbeg + min(16 * wave, n - 1)) / kBlockTokens];
+    const uint16_t *kb = pool + (size_t)blk * blk_stride + (size_t)g * kBlockTokens * D;
+    const uint16_t *vb = pool + (size_t)blk * blk_stride + (size_t)(hkv + g) * kBlockTokens * D;
     // K fragments: key 16 wave + l16 of the split (clamped into the split), d 32 s + 8 lq
     const int kkey = kbeg + min(16 * wave + l16, n - 1);
-    const uint16_t *kp = pool + (size_t)table[kkey / kBlockTokens] * blk_stride +
-                         ((size_t)g * kBlockTokens + kkey % kBlockTokens) * D + 8 * lq;
+    const uint16_t *kp = kb + (size_t)(kkey % kBlockTokens) * D + 8 * lq;
     uint4 kf[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) kf[s] = *reinterpret_cast<const uint4 *>(kp + 32 * s);
     // V rows: instruction i, lane l: key 16 wave + 4 i + lq, d 8 l16
-    uint4 vr[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    auto vrow = [&](int i) {
         const int key = kbeg + min(16 * wave + 4 * i + lq, n - 1);
-        const uint16_t *vp = pool + (size_t)table[key / kBlockTokens] * blk_stride +
-                             ((size_t)(hkv + g) * kBlockTokens + key % kBlockTokens) * D + 8 * l16;
-        vr[i] = *reinterpret_cast<const uint4 *>(vp);
-    }
-    // Q^T fragments: head l16 (zero past G), d 32 s + 8 lq, scaled by 1/sqrt(d), hi/lo
+        return *reinterpret_cast<const uint4 *>(vb + (size_t)(key % kBlockTokens) * D + 8 * l16);
+    };
+    const uint4 vr0 = vrow(0), vr1 = vrow(1), vr2 = vrow(2), vr3 = vrow(3);
+    // every K and V load in flight before any is used (left alone, the scheduler issues half of
+    // them after the first products, a second round trip to memory)
+    __builtin_amdgcn_sched_barrier(0);
+    // Q^T as a bf16 hi/lo pair, scaled by 1/sqrt(d)
     const float scale = 1.f / sqrtf((float)D);
     bf16x8_t qh[4], ql[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
+        const float q8[8] = {qv[s][0].x, qv[s][0].y, qv[s][0].z, qv[s][0].w,
+                             qv[s][1].x, qv[s][1].y, qv[s][1].z, qv[s][1].w};
         float x[8];
-        if (l16 < G) {
-            const float *qp = a.q + (size_t)row * hq_total * D + (size_t)(g * G + l16) * D + 32 * s + 8 * lq;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = qp[j] * scale;
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = 0.f;
-        }
+        for (int j = 0; j < 8; ++j) x[j] = l16 < G ? q8[j] * scale : 0.f;
         split8(x, qh[s], ql[s]);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<uint4 *>(&vs[16 * wave + 4 * i + lq][8 * l16]) = vr[i];
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + lq][8 * l16]) = vr0;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 4 + lq][8 * l16]) = vr1;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 8 + lq][8 * l16]) = vr2;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 12 + lq][8 * l16]) = vr3;
     f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -787,7 +798,9 @@ hipError_t launch_gd(const AttnArgs &a, hipStream_t st) {
         }
         return hipGetLastError();
     }
-    if (a.split_keys > kChunk || a.max_splits > kMaxDecodeSplits) return hipErrorInvalidValue;
+    if (a.split_keys > kChunk || a.split_keys % kBlockTokens || a.max_splits > kMaxDecodeSplits ||
+        a.rows_per_seq <= 0)
+        return hipErrorInvalidValue;
     dim3 grid(a.grid_splits, hkv, a.rows);
     if (a.grid_splits == 1) {   // every row within one split: its output directly, no merge
         if (a.kv_fp32)

@@ -129,8 +129,8 @@ struct AttnArgs {
     int split_keys;      // keys per split; 0 = one split per row (final output directly)
     int max_splits;      // stride of the partial buffers
     int grid_splits;     // splits launched: ceil(longest context in the call / split_keys)
-    int n_seqs;          // prefill: sequences in the call and rows per sequence (host copies of the
-    int rows_per_seq;    // row metadata, for the launch grid)
+    int n_seqs;          // sequences in the call and rows per sequence: host copies of the row
+    int rows_per_seq;    // metadata (the prefill launch grid; the decode kernels' row -> sequence map)
     const CallMeta *meta; // device copy of the call's row metadata
 };
 hipError_t launch_attention(const AttnArgs &a, hipStream_t st);

@@ -894,6 +894,8 @@ int run_layer_kernels(stage *s, int layer, const LayerWeights &w, int rows, int 
     at.split_keys = kDecodeSplitKeys;
     at.max_splits = s->max_splits;
     at.grid_splits = grid_splits;
+    at.n_seqs = rows;        // decode: one row per sequence
+    at.rows_per_seq = 1;
     at.meta = meta;
 
     GemvArgs o{};
