@@ -2,6 +2,8 @@
 // an fp32 activation A taken as the exact-sum pair A = hi + lo of two bf16 matrices (hi = bf16(A),
 // lo = bf16(A - hi); the pair keeps ~16 bits of A's mantissa, a single bf16 only 8).  Each 16-wide
 // k step issues v_mfma_f32_32x32x16_bf16 twice per output block, hi then lo, accumulating in fp32.
+// The pair is stored interleaved by 32-wide k blocks (hi block, then lo block, per row), so the
+// operand bytes of one k tile of a row are 128 contiguous bytes.
 //
 // Tiling: a workgroup (4 wavefronts) computes a 128 x 128 tile of C, each wavefront a 64 x 64
 // sub-tile as 2 x 2 blocks of 32 x 32; or, when the grid of 256 x 256 tiles still has a workgroup
@@ -43,6 +45,18 @@ __device__ __forceinline__ void split(float v, uint16_t &hi, uint16_t &lo) {
     lo = to_bf16(v - __uint_as_float((uint32_t)hi << 16));
 }
 
+// The hi and lo of four consecutive elements of a 32-wide block (p: the first one's hi, 8-byte
+// aligned): two 8-byte stores, the lo 32 elements further.
+__device__ __forceinline__ void store_pair4(uint16_t *p, float4 v) {
+    uint16_t h[4], l[4];
+    split(v.x, h[0], l[0]);
+    split(v.y, h[1], l[1]);
+    split(v.z, h[2], l[2]);
+    split(v.w, h[3], l[3]);
+    *reinterpret_cast<uint2 *>(p) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+    *reinterpret_cast<uint2 *>(p + 32) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
     bf16x8 r;
     __builtin_memcpy(&r, &v, 16);
@@ -73,8 +87,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
             const int m = m0 + row, n = n0 + row;
             rh[i] = rl[i] = rw[i] = make_uint4(0, 0, 0, 0);
             if (kin && m < M) {
-                rh[i] = *reinterpret_cast<const uint4 *>(a.a_hi + (size_t)m * a.lda + k);
-                rl[i] = *reinterpret_cast<const uint4 *>(a.a_lo + (size_t)m * a.lda + k);
+                const uint16_t *p = a.a + (size_t)m * a.lda + pair_at(k);
+                rh[i] = *reinterpret_cast<const uint4 *>(p);
+                rl[i] = *reinterpret_cast<const uint4 *>(p + 32);
             }
             if (kin && n < N) rw[i] = *reinterpret_cast<const uint4 *>(W + (size_t)n * K + k);
         }
@@ -179,11 +194,15 @@ __device__ __forceinline__ void wait_lgkm() {
 // Each wavefront computes WB x WB blocks of 32 x 32, so a workgroup tile is 64 WB square: WB = 2
 // gives the 128 x 128 tile, WB = 4 the 256 x 256 tile (16 accumulator blocks per wavefront, one
 // wavefront per SIMD), which reads half as many operand bytes per product from L2 and LDS.
-// An operand tile in LDS is row-major, four 16-byte k segments per row (BK = 32), segment s of row
+// The weight tile in LDS is row-major, four 16-byte k segments per row (BK = 32), segment s of row
 // r stored at slot 4 r + (s ^ ((r >> 2) & 3)): each DMA instruction then copies 16 rows x 64
 // contiguous bytes (lane l: row 16 q + l / 4 of instruction q), and the 32 x 32 fragment reads
 // (lane l: row l % 32, segment 2 step + l / 32) touch every LDS bank once per 16 lanes.  (Loading
-// in fragment order instead, 32 rows x 32 bytes per instruction, took 1.3-1.6x as long.)
+// in fragment order instead, 32 rows x 32 bytes per instruction, took 1.3-1.6x as long.)  The
+// activation tile holds a row's whole 128-byte k block (hi segments 0-3, lo segments 4-7),
+// segment g of row r at slot 8 r + (g ^ ((r >> 1) & 7)): one DMA instruction copies 8 rows x 128
+// contiguous bytes (full cache lines; 16 rows x 64 bytes of hi and of lo took 5-15% longer per
+// GEMM), and the fragment reads again meet every bank once per 16 lanes.
 //
 // With one wavefront per SIMD (WB = 4) nothing else hides the latency of a fragment read or of the
 // barrier, so that loop is software-pipelined (K >= 64): the fragments of the next k step are
@@ -195,10 +214,11 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     constexpr int S = 3;
     constexpr int TILE = 64 * WB;                 // workgroup tile rows of each operand
     constexpr int SLOTS = TILE * (BK / 8);        // 16-byte slots per operand tile (4 per row)
-    constexpr int PER_TILE = 3 * WB;              // load instructions per wavefront per k tile
-    static_assert(SLOTS == 4 * WB * 64, "each wavefront loads WB instructions of each operand");
-    static_assert(BK == 32, "the segment swizzle assumes four 16-byte k segments per row");
-    __shared__ uint4 lds[S][3][SLOTS];
+    constexpr int AI = 2 * WB;                    // activation copies per wavefront per k tile
+    constexpr int PER_TILE = AI + WB;             // load instructions per wavefront per k tile
+    static_assert(SLOTS == 4 * WB * 64, "each wavefront loads WB instructions of the weight tile");
+    static_assert(BK == 32, "the segment swizzles assume 32-wide k tiles");
+    __shared__ uint4 lds[S][3][SLOTS];            // per stage: activation tile (2 SLOTS), weight tile
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4 *)&lds[0][0][0];
     const int wm = wave >> 1, wn = wave & 1;
@@ -206,17 +226,20 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
     const uint16_t *W = a.w[blockIdx.z];
     const int M = a.M, N = a.N, K = a.K, nk = K / BK;
 
-    // instruction q = wave * WB + i of an operand: lane l copies row 16 q + l / 4, k segment
-    // (l % 4) ^ ((row >> 2) & 3) into slot 64 q + l; rows past M or N are clamped (in bounds),
-    // their results are never stored
-    // SWIGLU: the tile's 32-row blocks alternate between Wg and Wu rows n0 / 2 + 32 (b / 2) ..
-    const uint16_t *src_hi[WB], *src_lo[WB], *src_w[WB];
+    // activation copy qa = wave * AI + i: lane l copies segment (l % 8) ^ ((row >> 1) & 7) of the
+    // 128-byte k block of row 8 qa + l / 8 into slot 64 qa + l; weight copy q = wave * WB + i: lane
+    // l copies row 16 q + l / 4, k segment (l % 4) ^ ((row >> 2) & 3) into slot 64 q + l.  Rows past
+    // M or N are clamped (in bounds), their results are never stored.
+    // SWIGLU: the weight tile's 32-row blocks alternate between Wg and Wu rows n0 / 2 + 32 (b / 2) ..
+    const uint16_t *src_a[AI], *src_w[WB];
+#pragma unroll
+    for (int i = 0; i < AI; ++i) {
+        const int r = 8 * (wave * AI + i) + (lane >> 3), g = (lane & 7) ^ ((r >> 1) & 7);
+        src_a[i] = a.a + (size_t)min(m0 + r, M - 1) * a.lda + 8 * g;
+    }
 #pragma unroll
     for (int i = 0; i < WB; ++i) {
         const int q = wave * WB + i, r = 16 * q + (lane >> 2), seg = (lane & 3) ^ ((r >> 2) & 3);
-        const int m = min(m0 + r, M - 1);
-        src_hi[i] = a.a_hi + (size_t)m * a.lda + 8 * seg;
-        src_lo[i] = a.a_lo + (size_t)m * a.lda + 8 * seg;
         if (MODE == GEMM_SWIGLU) {
             const int b = r >> 5, n = min(n0 / 2 + 32 * (b >> 1) + (r & 31), N - 1);
             src_w[i] = a.w[b & 1] + (size_t)n * K + 8 * seg;
@@ -224,12 +247,12 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
             src_w[i] = W + (size_t)min(n0 + r, N - 1) * K + 8 * seg;
         }
     }
-    // this wavefront's share of tile t: instruction i of each operand
+    // this wavefront's share of tile t, part i: activation copies 2 i and 2 i + 1, weight copy i
     auto issue_part = [&](int t, int i) {
-        const int st = t % S, k0 = t * BK, q = wave * WB + i;
-        dma16(src_hi[i] + k0, lds_base + ((st * 3 + 0) * SLOTS + q * 64) * 16);
-        dma16(src_lo[i] + k0, lds_base + ((st * 3 + 1) * SLOTS + q * 64) * 16);
-        dma16(src_w[i] + k0, lds_base + ((st * 3 + 2) * SLOTS + q * 64) * 16);
+        const int st = t % S, q = wave * WB + i, qa = wave * AI + 2 * i;
+        dma16(src_a[2 * i] + 64 * t, lds_base + ((st * 3) * SLOTS + qa * 64) * 16);
+        dma16(src_a[2 * i + 1] + 64 * t, lds_base + ((st * 3) * SLOTS + (qa + 1) * 64) * 16);
+        dma16(src_w[i] + BK * t, lds_base + ((st * 3 + 2) * SLOTS + q * 64) * 16);
     };
     auto issue = [&](int t) {
 #pragma unroll
@@ -252,10 +275,10 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
 #pragma unroll
         for (int b = 0; b < WB; ++b) {
             const int ra = 32 * (wm * WB + b) + fr, rb = 32 * (wn * WB + b) + fr;
-            const int sa = 4 * ra + (seg ^ ((ra >> 2) & 3));
+            const int sw = (ra >> 1) & 7;
             const int sb = 4 * rb + (seg ^ ((rb >> 2) & 3));
-            ah[b] = as_bf16x8(L[sa]);
-            al[b] = as_bf16x8(L[SLOTS + sa]);
+            ah[b] = as_bf16x8(L[8 * ra + (seg ^ sw)]);
+            al[b] = as_bf16x8(L[8 * ra + ((4 + seg) ^ sw)]);
             bw[b] = as_bf16x8(L[2 * SLOTS + sb]);
         }
     };
@@ -336,8 +359,8 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
                     const int m = m0 + wm * 32 * WB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                     if (m >= M) continue;
                     const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-                    const size_t o = (size_t)m * a.ldo + n;
-                    split(gt / (1.f + expf(-gt)) * up, a.out_hi[o], a.out_lo[o]);
+                    const size_t o = (size_t)m * a.ldo + pair_at(n);
+                    split(gt / (1.f + expf(-gt)) * up, a.out_pair[o], a.out_pair[o + 32]);
                 }
             }
         return;
@@ -362,9 +385,9 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
         }
 }
 
-// y = x / sqrt(mean(x^2) + eps) * g, written as a bf16 hi/lo pair.  One workgroup per row.
+// y = x / sqrt(mean(x^2) + eps) * g, written as a pair (row stride ld).  One workgroup per row.
 __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, const uint16_t *g, float eps, int H,
-                                                             uint16_t *hi, uint16_t *lo) {
+                                                             uint16_t *pair, long ld) {
     const int row = blockIdx.x;
     const float *xr = x + (size_t)row * H;
     float ss = 0.f;
@@ -376,26 +399,39 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, cons
     __syncthreads();
     const float tot = ((red[0] + red[1]) + red[2]) + red[3];
     const float scale = 1.f / sqrtf(tot / (float)H + eps);
-    for (int i = threadIdx.x; i < H; i += 256) {
-        const float y = xr[i] * scale * __uint_as_float((uint32_t)g[i] << 16);
-        split(y, hi[(size_t)row * H + i], lo[(size_t)row * H + i]);
+    // four elements per thread (H % 4 == 0): one 16-byte load, 8-byte stores of their hi and lo
+    for (int i = 4 * threadIdx.x; i < H; i += 1024) {
+        const float4 v = *reinterpret_cast<const float4 *>(xr + i);
+        const uint2 gg = *reinterpret_cast<const uint2 *>(g + i);
+        store_pair4(pair + (size_t)row * ld + pair_at(i),
+                    make_float4(v.x * scale * __uint_as_float(gg.x << 16), v.y * scale * __uint_as_float(gg.x & 0xFFFF0000u),
+                                v.z * scale * __uint_as_float(gg.y << 16), v.w * scale * __uint_as_float(gg.y & 0xFFFF0000u)));
     }
 }
 
-// hi/lo pair of an fp32 matrix [rows, n] (row stride n).
-__global__ __launch_bounds__(256) void split_kernel(const float *x, size_t count, uint16_t *hi, uint16_t *lo) {
-    for (size_t i = blockIdx.x * 256ull + threadIdx.x; i < count; i += (size_t)gridDim.x * 256)
-        split(x[i], hi[i], lo[i]);
+// The pair (row stride ld) of an fp32 matrix [rows, n] (row stride n, n % 4 == 0), four elements
+// per thread.
+__global__ __launch_bounds__(256) void split_kernel(const float *x, int rows, int n, uint16_t *pair, long ld) {
+    const size_t quads = (size_t)rows * n / 4;
+    for (size_t q = blockIdx.x * 256ull + threadIdx.x; q < quads; q += (size_t)gridDim.x * 256) {
+        const size_t r = 4 * q / n;
+        const int c = (int)(4 * q % n);
+        store_pair4(pair + r * ld + pair_at(c), *reinterpret_cast<const float4 *>(x + 4 * q));
+    }
 }
 
-// h = silu(gate) * up from gu [rows, 2F] (gate columns first), written as a hi/lo pair [rows, F].
-__global__ __launch_bounds__(256) void swiglu_split_kernel(const float *gu, int F, size_t rows, uint16_t *hi,
-                                                            uint16_t *lo) {
-    const size_t count = rows * F;
-    for (size_t i = blockIdx.x * 256ull + threadIdx.x; i < count; i += (size_t)gridDim.x * 256) {
-        const size_t r = i / F, f = i % F;
-        const float gt = gu[r * 2 * F + f], up = gu[r * 2 * F + F + f];
-        split(gt / (1.f + expf(-gt)) * up, hi[i], lo[i]);
+// h = silu(gate) * up from gu [rows, 2F] (gate columns first), written as a pair [rows, F] (row
+// stride ld; F % 4 == 0), four elements per thread.
+__global__ __launch_bounds__(256) void swiglu_split_kernel(const float *gu, int F, int rows, uint16_t *pair,
+                                                            long ld) {
+    const size_t quads = (size_t)rows * F / 4;
+    for (size_t q = blockIdx.x * 256ull + threadIdx.x; q < quads; q += (size_t)gridDim.x * 256) {
+        const size_t r = 4 * q / F;
+        const int f = (int)(4 * q % F);
+        const float4 g4 = *reinterpret_cast<const float4 *>(gu + r * 2 * F + f);
+        const float4 u4 = *reinterpret_cast<const float4 *>(gu + r * 2 * F + F + f);
+        auto sw = [](float gt, float up) { return gt / (1.f + expf(-gt)) * up; };
+        store_pair4(pair + r * ld + pair_at(f), make_float4(sw(g4.x, u4.x), sw(g4.y, u4.y), sw(g4.z, u4.z), sw(g4.w, u4.w)));
     }
 }
 
@@ -428,8 +464,9 @@ void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) {
     if (a.M <= 0) return hipSuccess;
     // every variant runs the same MFMAs in the same order: the choice never changes a bit
+    if (a.lda < pair_ld(a.K)) return hipErrorInvalidValue;
     if (mode == GEMM_SWIGLU) {
-        if (a.K % BK != 0 || n_mats != 1 || !a.out_hi || !a.out_lo) return hipErrorInvalidValue;
+        if (a.K % BK != 0 || n_mats != 1 || !a.out_pair || a.ldo < pair_ld(a.N)) return hipErrorInvalidValue;
         launch_gemm_mode<GEMM_SWIGLU>(a, 1, st);
     } else if (mode == GEMM_RESIDUAL) {
         launch_gemm_mode<GEMM_RESIDUAL>(a, n_mats, st);
@@ -439,22 +476,27 @@ hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st) 
     return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *hi,
-                                uint16_t *lo, hipStream_t st) {
+hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *pair,
+                                long ld, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
-    STG_LAUNCH(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, hi, lo);
+    if (ld < pair_ld(H) || H % 4 != 0) return hipErrorInvalidValue;
+    STG_LAUNCH(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, pair, ld);
     return hipGetLastError();
 }
 
-hipError_t launch_split(const float *x, size_t count, uint16_t *hi, uint16_t *lo, hipStream_t st) {
-    if (count == 0) return hipSuccess;
-    STG_LAUNCH(split_kernel, dim3(grid_for(count)), dim3(256), 0, st, x, count, hi, lo);
+hipError_t launch_split(const float *x, int rows, int n, uint16_t *pair, long ld, hipStream_t st) {
+    if (rows <= 0 || n <= 0) return hipSuccess;
+    if (ld < pair_ld(n)) return hipErrorInvalidValue;
+    if (n % 4 != 0) return hipErrorInvalidValue;
+    STG_LAUNCH(split_kernel, dim3(grid_for((size_t)rows * n / 4)), dim3(256), 0, st, x, rows, n, pair, ld);
     return hipGetLastError();
 }
 
-hipError_t launch_swiglu_split(const float *gu, int F, size_t rows, uint16_t *hi, uint16_t *lo, hipStream_t st) {
-    if (rows == 0) return hipSuccess;
-    STG_LAUNCH(swiglu_split_kernel, dim3(grid_for(rows * F)), dim3(256), 0, st, gu, F, rows, hi, lo);
+hipError_t launch_swiglu_split(const float *gu, int F, int rows, uint16_t *pair, long ld, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    if (ld < pair_ld(F)) return hipErrorInvalidValue;
+    if (F % 4 != 0) return hipErrorInvalidValue;
+    STG_LAUNCH(swiglu_split_kernel, dim3(grid_for((size_t)rows * F / 4)), dim3(256), 0, st, gu, F, rows, pair, ld);
     return hipGetLastError();
 }
 

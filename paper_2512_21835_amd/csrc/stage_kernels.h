@@ -82,11 +82,19 @@ hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start
 
 enum GemmMode { GEMM_STORE = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2 };
 
-// Prefill projection on the matrix cores: out[m, out_col + n] (+)= sum_k (a_hi + a_lo)[m, k] W[n, k].
+// A prefill GEMM operand is an fp32 matrix X [M, K] held as the exact-sum pair X = hi + lo of two
+// bf16 matrices, interleaved by 32-wide k blocks: row m holds, for each block b, the 32 hi values
+// of k = 32 b .. 32 b + 31 and then their 32 lo values, so element k of the row has its hi at
+// 64 (k / 32) + k % 32 and its lo 32 further.  Row stride pair_ld(K) (K rounded up to a whole
+// block; a partial last block's padding is never read).
+constexpr long pair_ld(long k) { return 2 * ((k + 31) / 32 * 32); }
+__host__ __device__ constexpr long pair_at(long k) { return 2 * (k & ~31L) + (k & 31); }
+
+// Prefill projection on the matrix cores: out[m, out_col + n] (+)= sum_k (hi + lo)[m, k] W[n, k].
 // SWIGLU (K a multiple of 32, n_mats = 1): w[0] = Wg, w[1] = Wu, both [N, K]; writes
-// h = silu(Wg a) * (Wu a) as a bf16 hi/lo pair out_hi/out_lo [M, N] with row stride ldo.
+// h = silu(Wg a) * (Wu a) as a pair [M, N] to out_pair with row stride ldo.
 struct GemmArgs {
-    const uint16_t *a_hi, *a_lo;  // [M, K] bf16 pair of the fp32 activation, row stride lda
+    const uint16_t *a;            // [M, lda] pair of the fp32 activation (lda >= pair_ld(K))
     long lda;
     const uint16_t *w[2];         // [N, K] bf16; grid z selects the matrix
     float *out;                   // row stride ldo
@@ -94,16 +102,16 @@ struct GemmArgs {
     long ldo;
     int out_col[2];               // output column offset of each matrix
     int M, N, K;
-    uint16_t *out_hi, *out_lo;    // SWIGLU output pair
+    uint16_t *out_pair;           // SWIGLU output pair (row stride ldo >= pair_ld(N))
 };
 hipError_t launch_gemm(int mode, const GemmArgs &a, int n_mats, hipStream_t st);
-// y = rmsnorm(x) * g as a bf16 hi/lo pair [rows, H].
-hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *hi,
-                                uint16_t *lo, hipStream_t st);
-// bf16 hi/lo pair of `count` fp32 values.
-hipError_t launch_split(const float *x, size_t count, uint16_t *hi, uint16_t *lo, hipStream_t st);
-// silu(gate) * up of gu [rows, 2F] (gate columns first) as a bf16 hi/lo pair [rows, F].
-hipError_t launch_swiglu_split(const float *gu, int F, size_t rows, uint16_t *hi, uint16_t *lo, hipStream_t st);
+// y = rmsnorm(x) * g as a pair [rows, H] (row stride ld).
+hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, int rows, int H, uint16_t *pair,
+                                long ld, hipStream_t st);
+// The pair [rows, n] (row stride ld) of an fp32 matrix [rows, n].
+hipError_t launch_split(const float *x, int rows, int n, uint16_t *pair, long ld, hipStream_t st);
+// silu(gate) * up of gu [rows, 2F] (gate columns first) as a pair [rows, F] (row stride ld).
+hipError_t launch_swiglu_split(const float *gu, int F, int rows, uint16_t *pair, long ld, hipStream_t st);
 
 struct RopeKvArgs {
     const float *qkv;  // [rows, (Hq + 2 Hkv) d]: q heads, then k heads, then v heads

@@ -106,7 +106,7 @@ struct LaneState {
     CallMeta *d_meta = nullptr;
     size_t ws_rows = 0, part_rows = 0;
     float *ws_qkv = nullptr, *ws_q = nullptr, *ws_attn = nullptr, *ws_h = nullptr;
-    uint16_t *ws_hi = nullptr, *ws_lo = nullptr;
+    uint16_t *ws_pair = nullptr;
     float *ws_part_o = nullptr, *ws_part_ml = nullptr;
     float *ws_split = nullptr, *ws_split_ss = nullptr;
 };
@@ -147,7 +147,7 @@ struct stage {
 
     size_t ws_rows = 0;
     float *ws_qkv = nullptr, *ws_q = nullptr, *ws_attn = nullptr, *ws_h = nullptr;
-    uint16_t *ws_hi = nullptr, *ws_lo = nullptr;  // bf16 hi/lo pair of a prefill GEMM operand
+    uint16_t *ws_pair = nullptr;  // interleaved bf16 hi/lo pair of a prefill GEMM operand
     size_t part_rows = 0;
     int max_splits = 0;
     float *ws_part_o = nullptr, *ws_part_ml = nullptr;
@@ -270,8 +270,7 @@ void swap_workspaces(stage *s, LaneState &o) {
     std::swap(s->ws_q, o.ws_q);
     std::swap(s->ws_attn, o.ws_attn);
     std::swap(s->ws_h, o.ws_h);
-    std::swap(s->ws_hi, o.ws_hi);
-    std::swap(s->ws_lo, o.ws_lo);
+    std::swap(s->ws_pair, o.ws_pair);
     std::swap(s->ws_part_o, o.ws_part_o);
     std::swap(s->ws_part_ml, o.ws_part_ml);
     std::swap(s->ws_split, o.ws_split);
@@ -499,18 +498,16 @@ int ensure_workspace(stage *s, size_t rows, bool split_attention) {
     int rc = sync_all(s);
     if (rc) return rc;
     if (rows > s->ws_rows) {
-        for (void *p : {(void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
-                        (void *)s->ws_hi, (void *)s->ws_lo})
+        for (void *p : {(void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h, (void *)s->ws_pair})
             if (p) (void)hipFree(p);
         s->ws_qkv = s->ws_q = s->ws_attn = s->ws_h = nullptr;
-        s->ws_hi = s->ws_lo = nullptr;
+        s->ws_pair = nullptr;
         s->ws_rows = 0;
         const size_t qd = (size_t)s->Hq * s->D;
         const size_t wide = std::max<size_t>(s->qkv_rows, 2 * (size_t)s->F);
-        const size_t pair = std::max<size_t>(std::max<size_t>(s->H, qd), s->F);
+        const size_t pair = (size_t)pair_ld(std::max<size_t>(std::max<size_t>(s->H, qd), s->F));
         if (hipMalloc(&s->ws_qkv, rows * wide * sizeof(float)) != hipSuccess ||
-            hipMalloc(&s->ws_hi, rows * pair * sizeof(uint16_t)) != hipSuccess ||
-            hipMalloc(&s->ws_lo, rows * pair * sizeof(uint16_t)) != hipSuccess ||
+            hipMalloc(&s->ws_pair, rows * pair * sizeof(uint16_t)) != hipSuccess ||
             hipMalloc(&s->ws_q, rows * qd * sizeof(float)) != hipSuccess ||
             hipMalloc(&s->ws_attn, rows * qd * sizeof(float)) != hipSuccess ||
             hipMalloc(&s->ws_h, rows * (size_t)s->F * sizeof(float)) != hipSuccess) {
@@ -778,9 +775,9 @@ int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int 
     const int H = s->H, F = s->F, qd = s->Hq * s->D;
     const float eps = s->cfg.rms_eps;
 
-    HIP_TRY(launch_rmsnorm_split(x_src, base + s->off_g1 / 2, eps, rows, H, s->ws_hi, s->ws_lo, s->cs));
+    HIP_TRY(launch_rmsnorm_split(x_src, base + s->off_g1 / 2, eps, rows, H, s->ws_pair, pair_ld(H), s->cs));
     GemmArgs q{};
-    q.a_hi = s->ws_hi; q.a_lo = s->ws_lo; q.lda = H;
+    q.a = s->ws_pair; q.lda = pair_ld(H);
     q.w[0] = base + s->off_wqkv / 2;
     q.out = s->ws_qkv; q.ldo = s->qkv_rows;
     q.M = rows; q.N = s->qkv_rows; q.K = H;
@@ -810,10 +807,10 @@ int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int 
     at.rows_per_seq = T;
     at.meta = meta;
     HIP_TRY(launch_attention(at, s->cs));
-    HIP_TRY(launch_split(s->ws_attn, (size_t)rows * qd, s->ws_hi, s->ws_lo, s->cs));
+    HIP_TRY(launch_split(s->ws_attn, rows, qd, s->ws_pair, pair_ld(qd), s->cs));
 
     GemmArgs o{};
-    o.a_hi = s->ws_hi; o.a_lo = s->ws_lo; o.lda = qd;
+    o.a = s->ws_pair; o.lda = pair_ld(qd);
     o.w[0] = base + s->off_wo / 2;
     o.out = x_dst; o.res = x_src; o.ldo = H;
     o.M = rows; o.N = H; o.K = qd;
@@ -822,31 +819,29 @@ int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int 
     base = w.mlp;
     int rc = mlp_boundary(s, layer, w);
     if (rc) return rc;
-    HIP_TRY(launch_rmsnorm_split(x_dst, base + s->off_g2 / 2, eps, rows, H, s->ws_hi, s->ws_lo, s->cs));
+    HIP_TRY(launch_rmsnorm_split(x_dst, base + s->off_g2 / 2, eps, rows, H, s->ws_pair, pair_ld(H), s->cs));
     GemmArgs gu{};
-    gu.a_hi = s->ws_hi; gu.a_lo = s->ws_lo; gu.lda = H;
+    gu.a = s->ws_pair; gu.lda = pair_ld(H);
     gu.w[0] = base + s->off_wg / 2;
     gu.w[1] = base + s->off_wu / 2;
     gu.M = rows; gu.N = F; gu.K = H;
-    const uint16_t *h_hi = s->ws_hi, *h_lo = s->ws_lo;   // h = silu(Wg y) * (Wu y) as a bf16 pair
+    const uint16_t *h = s->ws_pair;   // h = silu(Wg y) * (Wu y) as a bf16 pair
     if (H % 32 == 0) {
         // SwiGLU and the hi/lo split in the GEMM's epilogue; the GEMM still reads the pair of y
-        // from ws_hi / ws_lo, so h goes to the (fp32-sized) QKV workspace
-        gu.out_hi = reinterpret_cast<uint16_t *>(s->ws_qkv);
-        gu.out_lo = gu.out_hi + (size_t)rows * F;
-        gu.ldo = F;
+        // from ws_pair, so h goes to the (fp32-sized) QKV workspace
+        gu.out_pair = reinterpret_cast<uint16_t *>(s->ws_qkv);
+        gu.ldo = pair_ld(F);
         HIP_TRY(launch_gemm(GEMM_SWIGLU, gu, 1, s->cs));
-        h_hi = gu.out_hi;
-        h_lo = gu.out_lo;
+        h = gu.out_pair;
     } else {
         gu.out = s->ws_qkv; gu.ldo = 2 * (long)F;
         gu.out_col[0] = 0; gu.out_col[1] = F;
         HIP_TRY(launch_gemm(GEMM_STORE, gu, 2, s->cs));
-        HIP_TRY(launch_swiglu_split(s->ws_qkv, F, rows, s->ws_hi, s->ws_lo, s->cs));
+        HIP_TRY(launch_swiglu_split(s->ws_qkv, F, rows, s->ws_pair, pair_ld(F), s->cs));
     }
 
     GemmArgs dn{};
-    dn.a_hi = h_hi; dn.a_lo = h_lo; dn.lda = F;
+    dn.a = h; dn.lda = pair_ld(F);
     dn.w[0] = base + s->off_wd / 2;
     dn.out = x_dst; dn.res = x_dst; dn.ldo = H;
     dn.M = rows; dn.N = H; dn.K = F;
@@ -1403,7 +1398,7 @@ int stage_destroy(stage *s) {
         if (p) (void)hipHostFree(p);
     for (void *p : {(void *)s->kv_pool, (void *)s->d_table, (void *)s->d_meta, (void *)s->d_cos, (void *)s->d_sin,
                     (void *)s->ws_qkv, (void *)s->ws_q, (void *)s->ws_attn, (void *)s->ws_h,
-                    (void *)s->ws_hi, (void *)s->ws_lo,
+                    (void *)s->ws_pair,
                     (void *)s->ws_part_o, (void *)s->ws_part_ml, (void *)s->ws_split, (void *)s->ws_split_ss,
                     s->ws_dense, (void *)s->d_slot_tags, (void *)s->d_slot_rec})
         if (p) (void)hipFree(p);
@@ -1411,7 +1406,7 @@ int stage_destroy(stage *s) {
     if (s->own_xs && s->xs) (void)hipStreamDestroy(s->xs);
     for (LaneState &ln : s->lanes) {
         for (void *p : {(void *)ln.d_meta, (void *)ln.ws_qkv, (void *)ln.ws_q, (void *)ln.ws_attn, (void *)ln.ws_h,
-                        (void *)ln.ws_hi, (void *)ln.ws_lo, (void *)ln.ws_part_o, (void *)ln.ws_part_ml,
+                        (void *)ln.ws_pair, (void *)ln.ws_part_o, (void *)ln.ws_part_ml,
                         (void *)ln.ws_split, (void *)ln.ws_split_ss})
             if (p) (void)hipFree(p);
         if (ln.own_cs && ln.cs) (void)hipStreamDestroy(ln.cs);
