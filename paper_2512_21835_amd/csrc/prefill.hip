@@ -68,6 +68,30 @@ __device__ __forceinline__ int frag_slot(int row, int ch) {
     return ((row >> 5) * (BK / 16) + (ch >> 1)) * 64 + (row & 31) + 32 * (ch & 1);
 }
 
+// Stores one 32 x 32 accumulator block (rows mb .. mb + 31, this lane's column c): register r of
+// lane l is row mb + 8 (r / 4) + 4 (l / 32) + r % 4.  RESIDUAL: for a block inside M all 16
+// residual values are loaded before any sum is stored, in straight-line code, so their loads are in
+// flight together and the stores wait for nothing (out may alias res: each element is read and
+// written by this lane only, read first).  A block crossing M stores element by element.
+template <int MODE>
+__device__ __forceinline__ void store_block(const GemmArgs &a, const f32x16 &acc, int mb, int M, int c, int lane) {
+    const size_t o0 = (size_t)(mb + 4 * (lane >> 5)) * a.ldo + c;
+    auto off = [&](int r) { return o0 + (size_t)(8 * (r >> 2) + (r & 3)) * a.ldo; };
+    if (mb + 32 <= M) {   // the same for the whole wavefront
+        float rv[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) rv[r] = MODE == GEMM_RESIDUAL ? a.res[off(r)] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) a.out[off(r)] = MODE == GEMM_RESIDUAL ? rv[r] + acc[r] : acc[r];
+        return;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int m = mb + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (m < M) a.out[off(r)] = MODE == GEMM_RESIDUAL ? a.res[off(r)] + acc[r] : acc[r];
+    }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
     __shared__ uint4 lds[2][3][kFrag];
@@ -151,16 +175,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         for (int j = 0; j < 2; ++j) {
             const int n = n0 + wn * 64 + j * 32 + (lane & 31);
             if (n >= N) continue;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (m >= M) continue;
-                const size_t o = (size_t)m * a.ldo + col_off + n;
-                if (MODE == GEMM_RESIDUAL)
-                    a.out[o] = a.res[o] + acc[i][j][r];
-                else
-                    a.out[o] = acc[i][j][r];
-            }
+            store_block<MODE>(a, acc[i][j], m0 + wm * 64 + i * 32, M, col_off + n, lane);
         }
 }
 
@@ -372,16 +387,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
         for (int j = 0; j < WB; ++j) {
             const int n = n0 + wn * 32 * WB + j * 32 + (lane & 31);
             if (n >= N) continue;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * 32 * WB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (m >= M) continue;
-                const size_t o = (size_t)m * a.ldo + col_off + n;
-                if (MODE == GEMM_RESIDUAL)
-                    a.out[o] = a.res[o] + acc[i][j][r];
-                else
-                    a.out[o] = acc[i][j][r];
-            }
+            store_block<MODE>(a, acc[i][j], m0 + wm * 32 * WB + i * 32, M, col_off + n, lane);
         }
 }
 
