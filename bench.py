@@ -476,14 +476,16 @@ def c1_leg(K: int = 256, W: int = 16):
             "steps": runs * steps, "weight_bytes": 2 * shape.layer_bytes(), "bound": "latency (weights fit in L2)"}
 
 
-def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False, prefill: bool = True):
+def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False, prefill: bool = True, slots: int = 2,
+                decode: bool = True):
     """The 70B-shaped stage with 4 resident layers and 12 streamed through 2 HBM slots from pinned
     host memory (the library's own copy stream), 4 micro-batches.  Without zero copy: a prefill of
     4 x `ctx` tokens in one call (the regime where compute and copies are of the same order), then
     decode calls carrying all four micro-batches (streamed layers loaded once per call); both timed
     with events on the copy and compute streams.  With `zero_copy` the contexts are filled through
     stage_kv_append and the decode kernels of the 12 offloaded layers read their pinned host blobs
-    directly (no slot copies); the report gives the call time and the host-link rate of those reads."""
+    directly (no slot copies); the report gives the call time and the host-link rate of those reads.
+    `slots`: streaming slots; `decode=False` returns after the prefill."""
     import torch
 
     import synth
@@ -494,7 +496,7 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False, prefill: b
     cstream = torch.cuda.current_stream(dev)
     n_mb, L = 4, shape.n_layers
     cfg = P.config_for(shape, max_microbatches=n_mb, max_batch=1, max_context=ctx + calls + 2, n_resident_max=4,
-                       n_stream_slots=2, compute_stream=cstream.cuda_stream, zero_copy=zero_copy)
+                       n_stream_slots=slots, compute_stream=cstream.cuda_stream, zero_copy=zero_copy)
     h = P.stage_init(cfg)
     gen = torch.Generator(device=dev).manual_seed(2512)
     res = {}
@@ -531,6 +533,8 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False, prefill: b
             res["prefill"] = dict(ov, tokens=n_mb * ctx, tokens_per_s=n_mb * ctx / wall,
                                   link_GBs=streamed / (ov["ms_per_call"] * 1e-3) / 1e9)
             del xp, yp
+            if not decode:
+                return {"slots": slots, "prefill": res["prefill"]}
         else:
             for m in range(n_mb):
                 kv = random_kv(shape, ctx, gen, dev)
@@ -568,7 +572,7 @@ def offload_leg(calls: int, ctx: int = 2048, zero_copy: bool = False, prefill: b
     ov = overlap(seg)
     res.update({
         "workload": f"llama70b_offload: 16 layers (hidden 8192, 64/8 heads, ffn 28672), 4 resident + 12 streamed "
-                    f"through 2 HBM slots from pinned host memory on the library's copy stream, 4 micro-batches of "
+                    f"through {slots} HBM slots from pinned host memory on the library's copy stream, 4 micro-batches of "
                     f"batch 1 per call; prefill {ctx} tokens each in one call, then decode calls at context {ctx}",
         "tokens_per_s": n_mb * calls / wall, "streamed_GB_per_call": streamed / 1e9,
         "link_GBs": streamed / (ov["ms_per_call"] * 1e-3) / 1e9, "h2d_peak_GBs": h2d_gbs,
@@ -951,6 +955,10 @@ def main() -> int:
         out["planner"] = planner_leg(args.planner_calls)
     if args.offload_calls > 0:
         out["offload"] = offload_leg(args.offload_calls)
+        # the same prefill with more streaming slots: the copy engine no longer waits for a slot
+        # while the resident layers compute
+        out["offload"]["prefill_more_slots"] = {str(S): offload_leg(0, slots=S, decode=False)["prefill"]
+                                                for S in (3, 4)}
         out["offload_zero_copy"] = offload_leg(args.offload_calls, zero_copy=True)
         if "resident70b" in out:
             out["allocation"] = allocation_report(out["resident70b"]["4_in_one_call"]["ms_per_call"], out["offload"])
