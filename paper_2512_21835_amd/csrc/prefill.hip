@@ -396,8 +396,17 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, cons
                                                              uint16_t *pair, long ld) {
     const int row = blockIdx.x;
     const float *xr = x + (size_t)row * H;
+    // sum of squares: four elements per thread and step (H % 4 == 0), the loads of four steps
+    // issued before their products
     float ss = 0.f;
-    for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+#pragma unroll 4
+    for (int i = 4 * threadIdx.x; i < H; i += 1024) {
+        const float4 v = *reinterpret_cast<const float4 *>(xr + i);
+        ss = fmaf(v.x, v.x, ss);
+        ss = fmaf(v.y, v.y, ss);
+        ss = fmaf(v.z, v.z, ss);
+        ss = fmaf(v.w, v.w, ss);
+    }
     __shared__ float red[4];
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) ss += lane_xor(ss, o);
