@@ -41,8 +41,8 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": 940190062,
-                                "source_sha256": "c944ce07e06d83ea35c0a12c5b37c315c7603c2b6b3cd7119b2955b4d12d40f2"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940189726,
+                                "source_sha256": "19a64dafd7ff31193f7ff71c108e8ddf366b8ade233cea0093a708ff28bb7350"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 

@@ -431,7 +431,9 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
 }
 
 // Adds the k ranges of a split matrix-core launch in ascending order and applies the epilogue:
-// one thread per (row, unit).
+// one thread per (row, unit).  Every load (each range's partials and sums of squares, indices past
+// the last range clamped to it, then the epilogue inputs) is issued before the first sum, so the
+// partials cost one round trip to memory.
 template <int MODE>
 __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int splits) {
     constexpr bool kNorm = Shape<MODE>::kNorm;
@@ -440,20 +442,31 @@ __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int split
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= a.rows * units) return;
     const int m = e / units, u = e % units;
+    float p[NW][kGemvMaxSplits], q[kGemvMaxSplits];
+#pragma unroll
+    for (int sp = 0; sp < kGemvMaxSplits; ++sp) {
+        const int c = min(sp, splits - 1);
+#pragma unroll
+        for (int w = 0; w < NW; ++w) p[w][sp] = a.split_part[(((size_t)c * NW + w) * kMfmaRows + m) * units + u];
+        if (kNorm) q[sp] = a.split_ss[c * kMfmaRows + m];
+    }
+    const EpiIn epi = epi_load<MODE>(a, u, m);   // (RoPE/KV: dependent metadata loads, after the partials')
     float t[NW];
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-        float acc = a.split_part[((size_t)w * kMfmaRows + m) * units + u];
-        for (int sp = 1; sp < splits; ++sp) acc += a.split_part[(((size_t)sp * NW + w) * kMfmaRows + m) * units + u];
+        float acc = p[w][0];
+#pragma unroll
+        for (int sp = 1; sp < kGemvMaxSplits; ++sp) acc = sp < splits ? acc + p[w][sp] : acc;
         t[w] = acc;
     }
     float scale = 1.f;
     if (kNorm) {
-        float sq = a.split_ss[m];
-        for (int sp = 1; sp < splits; ++sp) sq += a.split_ss[sp * kMfmaRows + m];
+        float sq = q[0];
+#pragma unroll
+        for (int sp = 1; sp < kGemvMaxSplits; ++sp) sq = sp < splits ? sq + q[sp] : sq;
         scale = 1.f / sqrtf(sq / (float)a.K + a.eps);
     }
-    epi_store<MODE>(a, epi_load<MODE>(a, u, m), u, m, t[0] * scale, t[NW - 1] * scale);
+    epi_store<MODE>(a, epi, u, m, t[0] * scale, t[NW - 1] * scale);
 }
 
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
