@@ -504,7 +504,9 @@ int ensure_workspace(stage *s, size_t rows, bool split_attention) {
         s->ws_pair = nullptr;
         s->ws_rows = 0;
         const size_t qd = (size_t)s->Hq * s->D;
-        const size_t wide = std::max<size_t>(s->qkv_rows, 2 * (size_t)s->F);
+        // ws_qkv holds the prefill QKV rows, the gate and up halves side by side, or the pair of h
+        const size_t wide = std::max<size_t>(std::max<size_t>(s->qkv_rows, 2 * (size_t)s->F),
+                                             (size_t)pair_ld(s->F) / 2);
         const size_t pair = (size_t)pair_ld(std::max<size_t>(std::max<size_t>(s->H, qd), s->F));
         if (hipMalloc(&s->ws_qkv, rows * wide * sizeof(float)) != hipSuccess ||
             hipMalloc(&s->ws_pair, rows * pair * sizeof(uint16_t)) != hipSuccess ||

@@ -255,20 +255,48 @@ ROWS_SHAPE = synth.StageShape("rows-1L-h256", 5, 1, 256, 4, 2, 64, 512)
 @pytest.mark.parametrize("rows", [1, 2, 3, 4, 5, 7, 8, 9, 16, 17, 40])
 def test_decode_rows_on_both_engines(rows):
     _gpu()
+    _decode_rows(ROWS_SHAPE, rows)
+
+
+# A stage whose widths are off the 32 grid (hidden 200, ffn 440, four heads of 64): in prefill the
+# QKV, gate/up and down GEMMs take the register-staged kernel (K % 32 != 0), gate/up stores both
+# halves and a separate pass applies SwiGLU and writes the pair, and the O GEMM (K = 256) runs on
+# the LDS-copy kernel with a ragged last column tile; in decode the vector GEMVs take K = 200 and
+# 440 (not whole 512-wide steps), and at 6 rows the O projection runs on the matrix cores with a
+# ragged last 64-unit block.
+ODD_SHAPE = synth.StageShape("odd-2L-h200", 7, 2, 200, 4, 2, 64, 440)
+
+
+@pytest.mark.parametrize("kv_fp32", [False, True])
+def test_widths_off_the_32_grid(kv_fp32):
+    _gpu()
+    plan = [("prefill", 70), ("decode", 1), ("decode", 1)]
+    _check(f"{ODD_SHAPE.name} kv_fp32={kv_fp32}", _run(ODD_SHAPE, plan, kv_fp32, 8, 80))
+
+
+@pytest.mark.parametrize("rows", [2, 6])
+def test_widths_off_the_32_grid_several_rows(rows):
+    _gpu()
+    _decode_rows(ODD_SHAPE, rows)
+
+
+def _decode_rows(shape, rows):
+    """Prefills `rows` sequences of ragged lengths one by one, then decodes all of them in one
+    call; every row against the oracle."""
     import torch
     import paper_2512_21835_amd as P
     from oracle.stage_oracle import OracleStage
 
-    shape = ROWS_SHAPE
     w = weights_of(shape)
-    H = shape.hidden
+    L, H = shape.n_layers, shape.hidden
     orc = OracleStage(shape, w, kv_dtype="bf16")
     with compute_stream() as cs:
-        cfg = P.config_for(shape, max_microbatches=40, max_batch=1, max_context=64, n_resident_max=1,
+        cfg = P.config_for(shape, max_microbatches=40, max_batch=1, max_context=64, n_resident_max=L,
                            compute_stream=cs.handle)
         h = P.stage_init(cfg)
         try:
-            P.stage_load_layer(h, 0, w(0), 1)
+            for l in range(L):
+                P.stage_load_layer(h, l, w(l), 1)
             for m in range(rows):
                 n = 20 + m % 23   # ragged histories
                 x = synth.normal_f32(synth.seed_of(0xE9, m, n), (n, H))
