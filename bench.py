@@ -42,7 +42,7 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # reported as null.
 GATEUP_TRAFFIC = {
     "llama3.3-70b-shaped-16L": {"bytes": 940189726,
-                                "source_sha256": "19a64dafd7ff31193f7ff71c108e8ddf366b8ade233cea0093a708ff28bb7350"},
+                                "source_sha256": "7b0ae265bc5c8a51344e2a66331e4391a818ef72a6ef67f1667813c9fde377d6"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 

@@ -26,15 +26,16 @@
 // the square O projection), where the vector kernel falls behind (one multiply-add per row per
 // weight element): the rows are the A operand of v_mfma_f32_16x16x32_bf16 (padded to 16, the
 // fp32 activation as a bf16 hi + lo pair, two MFMAs), 16 weight rows the B operand.  A workgroup owns 64 units, each
-// wavefront 16 of them over the workgroup's K range, in chunks of 128 k.  The B layout wants 16
-// rows x 64 bytes per load instruction, which streams HBM poorly (~4 TB/s), so a wavefront loads
-// its chunk as 4 rows x 256 contiguous bytes per instruction, stores it in its own LDS tile (the
-// 16-byte k segments XOR-swizzled by row, so the stores are contiguous and the MFMA-layout reads
-// are free of bank conflicts) and reads it back as B fragments.  The A fragments of a chunk are
-// converted once per workgroup (one per thread) into a double-buffered LDS tile, one barrier per
-// chunk; the next chunk's weights and activations are loaded before the current one is used.
-// Per output element: MFMA accumulation over the chunks in ascending k.  Where the grid would not
-// cover the GPU, K is cut into up to 8 ranges across workgroups (partial products to a
+// wavefront 16 of them over the workgroup's K range, in chunks of 128 k taken two at a time.  The
+// B layout wants 16 rows x 64 bytes per load instruction, which streams HBM poorly (~4 TB/s; 4
+// rows x 256 bytes ~5.7 TB/s), so a wavefront loads a pair of chunks as 2 rows x 512 contiguous
+// bytes per instruction, stores both chunks in its own LDS tiles (the 16-byte k segments
+// XOR-swizzled by row, so the stores are contiguous and the MFMA-layout reads are free of bank
+// conflicts) and reads them back as B fragments.  The A fragments of a pair are converted once per
+// workgroup (two per thread) into an LDS tile; two barriers per pair.  The next pair's weights and
+// activations are loaded before the current pair is multiplied.  Per output element: MFMA
+// accumulation over the chunks in ascending k.  K is cut into up to 8 ranges of whole chunk pairs
+// across workgroups where the grid would leave compute units idle (partial products to a
 // workspace) and a second launch adds the ranges in ascending order and applies the epilogue.
 // Which of the two runs depends on the layer shape only, so results are independent of the row
 // count; they differ in rounding from the vector kernel's (by ~1e-5 relative).
@@ -300,14 +301,16 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
 
 // One workgroup: units 64 blockIdx.x .. + 63 (wavefront w: 16 of them) for up to 16 activation
 // rows.  SPLIT: k chunks [blockIdx.y * cps, (blockIdx.y + 1) * cps) only, partial products and
-// sums of squares to the workspace [split][w][m][units], [split][m].
+// sums of squares to the workspace [split][w][m][units], [split][m].  LDS: 80 KB with two weight
+// rows per unit (two workgroups per compute unit), 48 KB with one (three).
 template <int MODE, bool SPLIT>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     constexpr bool kNorm = Shape<MODE>::kNorm;
     constexpr int NW = Shape<MODE>::NW;
-    __shared__ uint4 bt[kWaves][NW][256];   // wavefront B tile: row r, k segment s at 16 r + (s ^ r)
-    __shared__ uint4 at[2][4][2][64];       // A fragments [buffer][k step][hi, lo][lane]
-    __shared__ float ssp[kWaves][64];
+    // wavefront B tiles of a chunk pair: [wave][matrix][chunk], row r, k segment s at 16 r + (s ^ r)
+    __shared__ uint4 bt[kWaves][NW][2][256];
+    __shared__ uint4 at[2][4][2][64];       // A fragments [chunk][k step][hi, lo][lane]
+    float *const ssp = reinterpret_cast<float *>(&at[0][0][0][0]);   // [wave][lane], after the k loop
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int units = n_units<MODE>(a);
     const int u0 = blockIdx.x * 64 + 16 * wave;
@@ -315,19 +318,18 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     const int c_beg = SPLIT ? blockIdx.y * cps : 0;
     const int c_end = SPLIT ? min(c_beg + cps, chunks) : chunks;
 
-    // load instruction i of matrix w: lane l reads row 4 i + l / 16 of the block, k segment
-    // (l % 16) ^ row (8 bf16), i.e. 256 contiguous bytes per row; rows past the last unit are
-    // clamped to it (in bounds, results dropped)
+    // load instruction i of matrix w: lane l reads row 2 i + l / 32 of the block, 16-byte k
+    // segment l % 16 of chunk (l / 16) % 2 of the pair, i.e. 512 contiguous bytes per row; rows
+    // past the last unit are clamped to it, and a missing second chunk of a range to its first
+    // (in bounds, results dropped)
+    const int pr = lane >> 5, ph = (lane >> 4) & 1, ps = lane & 15;
     const int lr = lane >> 4, lk = lane & 15;
-    const uint16_t *wp[NW][4];
+    const uint16_t *wp[NW][8];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = 4 * i + lr;
-            wp[w][i] = unit_row<MODE>(a, min(u0 + r, units - 1), w) + 8 * (lk ^ r);
-        }
-    // this thread's A fragment: k step `wave` of the chunk, lane `lane` (row l % 16, k 8 (l / 16))
+        for (int i = 0; i < 8; ++i) wp[w][i] = unit_row<MODE>(a, min(u0 + 2 * i + pr, units - 1), w) + 8 * ps;
+    // this thread's A fragments: k step `wave` of each chunk, lane `lane` (row l % 16, k 8 (l / 16))
     const int am = lane & 15, ak = 32 * wave + 8 * (lane >> 4);
     const bool avalid = am < rows;
     const float *xp = a.act + (size_t)(avalid ? am : 0) * a.act_ld + ak;
@@ -338,26 +340,30 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     for (int w = 0; w < NW; ++w) d[w] = f32x4{0.f, 0.f, 0.f, 0.f};
     float ss = 0.f;
 
-    struct Chunk {
-        uint4 w[NW][4];
-        float4 x0, x1;
-        uint4 g;
+    struct Pair {
+        uint4 w[NW][8];
+        float4 x[2][2];
+        uint4 g[2];
     };
-    auto load = [&](int c, Chunk &b) {
-        const int k = c * kChunkK;
+    auto load = [&](int c, Pair &b) {
+        const int kc = kChunkK * min(c + ph, c_end - 1);
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) b.w[w][i] = load_stream16(wp[w][i] + k);
-        b.x0 = *reinterpret_cast<const float4 *>(xp + k);
-        b.x1 = *reinterpret_cast<const float4 *>(xp + k + 4);
-        if (kNorm) b.g = *reinterpret_cast<const uint4 *>(gp + k);
+            for (int i = 0; i < 8; ++i) b.w[w][i] = load_stream16(wp[w][i] + kc);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int k = kChunkK * min(c + h, c_end - 1);
+            b.x[h][0] = *reinterpret_cast<const float4 *>(xp + k);
+            b.x[h][1] = *reinterpret_cast<const float4 *>(xp + k + 4);
+            if (kNorm) b.g[h] = *reinterpret_cast<const uint4 *>(gp + k);
+        }
     };
-    auto compute = [&](int c, const Chunk &b) {
-        const int buf = c & 1;
-        const float x[8] = {b.x0.x, b.x0.y, b.x0.z, b.x0.w, b.x1.x, b.x1.y, b.x1.z, b.x1.w};
+    auto convert = [&](const Pair &b, int h) {
+        const float x[8] = {b.x[h][0].x, b.x[h][0].y, b.x[h][0].z, b.x[h][0].w,
+                            b.x[h][1].x, b.x[h][1].y, b.x[h][1].z, b.x[h][1].w};
         float g[8];
-        if (kNorm) unpack8(b.g, g);
+        if (kNorm) unpack8(b.g[h], g);
         bf16x8 xh, xl;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -372,44 +378,51 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
         uint4 h4, l4;
         __builtin_memcpy(&h4, &xh, 16);
         __builtin_memcpy(&l4, &xl, 16);
-        at[buf][wave][0][lane] = h4;
-        at[buf][wave][1][lane] = l4;
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) bt[wave][w][64 * i + lane] = b.w[w][i];
-        // A tile complete for every wavefront; the buffer written next chunk was last read
-        // before this barrier
-        __syncthreads();
+        at[h][wave][0][lane] = h4;
+        at[h][wave][1][lane] = l4;
+    };
+    auto multiply = [&](int h) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            const bf16x8 ah = as_bf16x8(at[buf][t][0][lane]);
-            const bf16x8 al = as_bf16x8(at[buf][t][1][lane]);
+            const bf16x8 ah = as_bf16x8(at[h][t][0][lane]);
+            const bf16x8 al = as_bf16x8(at[h][t][1][lane]);
 #pragma unroll
             for (int w = 0; w < NW; ++w) {
-                const bf16x8 bw = as_bf16x8(bt[wave][w][16 * lk + ((4 * t + lr) ^ lk)]);
+                const bf16x8 bw = as_bf16x8(bt[wave][w][h][16 * lk + ((4 * t + lr) ^ lk)]);
                 d[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw, d[w], 0, 0, 0);
                 d[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, d[w], 0, 0, 0);
             }
         }
     };
-    Chunk b0, b1;
-    if (c_beg < c_end) load(c_beg, b0);
+    Pair b;
+    if (c_beg < c_end) load(c_beg, b);
     for (int c = c_beg; c < c_end; c += 2) {
-        if (c + 1 < c_end) load(c + 1, b1);
-        compute(c, b0);
-        if (c + 1 >= c_end) break;
-        if (c + 2 < c_end) load(c + 2, b0);
-        compute(c + 1, b1);
+        const bool two = c + 1 < c_end;
+        convert(b, 0);
+        if (two) convert(b, 1);
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int r = 2 * i + pr;
+                bt[wave][w][ph][16 * r + (ps ^ r)] = b.w[w][i];
+            }
+        if (c + 2 < c_end) load(c + 2, b);
+        // A tiles complete for every wavefront (each wavefront reads only its own B tiles)
+        __syncthreads();
+        multiply(0);
+        if (two) multiply(1);
+        // the A tiles and the sums-of-squares array are written next by other wavefronts
+        __syncthreads();
     }
 
     // a row's sum of squares: 16 thread partials (4 k steps x 4 k blocks) in a fixed order
-    if (kNorm) ssp[wave][lane] = ss;
+    if (kNorm) ssp[wave * 64 + lane] = ss;
     __syncthreads();
     auto row_ss = [&](int m) {
         float t = 0.f;
         for (int w = 0; w < kWaves; ++w)
-            for (int q = 0; q < 4; ++q) t += ssp[w][16 * q + m];
+            for (int q = 0; q < 4; ++q) t += ssp[w * 64 + 16 * q + m];
         return t;
     };
     if (SPLIT && kNorm && blockIdx.x == 0 && threadIdx.x < kMfmaRows)
@@ -471,29 +484,21 @@ __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int split
 
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
 
-// K ranges: about 640 workgroups in all, at most 8 ranges and at least 2 chunks per range (swept
-// on the 8B- and 70B-shaped projections at 5, 8 and 16 rows: 70B gate/up runs unsplit with 448
-// workgroups, the 8B gate/up in 3 ranges, the O and down projections in 5-8).  Without a
-// workspace, unsplit.
+// K ranges of whole chunk pairs, at most 8 and at most one per four chunks, as many as keep the
+// grid within one even layer of workgroups: 512 (two per compute unit) with one weight row per
+// unit, 300 (about one per compute unit) with two, whose 80 KB of LDS leave room for two but whose
+// split epilogue costs more than a second, partial layer gains.  Swept at 4, 8 and 16 rows on the
+// 8B- and 70B-shaped layers (16 rows, with the epilogue): 70B gate/up unsplit (448 workgroups)
+// 155 us against 165 with 4 ranges; 70B QKV 3 ranges 36.7 us, 4 ranges 44.6, 6 ranges 39.7; 70B
+// down 4 ranges 78 us against 92 for 8 and 95 for 2; 70B O 4 ranges 28 us against 31 for 8; 8B
+// gate/up unsplit 48.7 us against 52.1 with 2 ranges; 8B QKV 6 ranges 17.4 us against 18.1 for 4;
+// 8B down and O 8 ranges.  Without a workspace, unsplit.
 template <int MODE>
 void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int units = host_units(MODE, c), chunks = c.K / kChunkK;
     const int blocks = (units + 63) / 64;
-    // about 640 workgroups, preferring a whole number per compute unit (256 of them) between 512
-    // and 768, larger on a tie (measured on the 8B- and 70B-shaped layers; 70B down projection at
-    // 16 rows: 5 splits 92.8 us, 6 splits 84.5 us)
-    const int max_splits = max(1, min(kGemvMaxSplits, chunks / 2));
-    int splits = max(1, min((640 + blocks / 2) / blocks, max_splits));
-    for (int sp = 1, best = 1 << 30; sp <= max_splits; ++sp) {
-        const int g = blocks * sp, d = abs(g - 640);
-        if (g % 256 == 0 && g >= 512 && g <= 768 && d <= best) {
-            best = d;
-            splits = sp;
-        }
-    }
-    // QKV (two weight rows per unit, RoPE epilogue): at most 6 ranges (70B shape at 16 rows: 39.6 us
-    // against 42.4 us for 8; 8B: 19.4 against 20.7)
-    if (MODE == GEMV_NORM_ROPE_KV) splits = min(splits, 6);
+    const int grid_max = Shape<MODE>::NW == 1 ? 512 : 300;
+    int splits = max(1, min(min(kGemvMaxSplits, chunks / 4), grid_max / blocks));
     if (!c.split_part || !c.split_ss) splits = 1;
     if (splits == 1) {
         if (e0 || e1)
@@ -502,7 +507,7 @@ void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
             STG_LAUNCH((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, c, 0);
         return;
     }
-    const int cps = (chunks + splits - 1) / splits;
+    const int cps = ((chunks + splits - 1) / splits + 1) & ~1;   // whole chunk pairs
     splits = (chunks + cps - 1) / cps;  // no empty range
     if (e0)
         STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,

@@ -246,16 +246,32 @@ def test_every_attention_group_and_head_width(g, d, kv_fp32):
 
 # Decode calls of 1 to 40 rows on one small layer whose projections can run on either engine
 # (K a multiple of 128): the vector kernel's 1-, 2-, 4- and 8-row instances, the matrix-core
-# engine from 3 rows (5 for the O projection), its split and unsplit launches, and calls of more
+# engine from 3 rows (5 for the O projection), its unsplit launches and the down projection's K
+# cut into two ranges, and calls of more
 # than 16 rows cut into several launches (17: 16 + 1; 40: 16 + 16 + 8); every row against the
 # oracle.
-ROWS_SHAPE = synth.StageShape("rows-1L-h256", 5, 1, 256, 4, 2, 64, 512)
+ROWS_SHAPE = synth.StageShape("rows-1L-h256", 5, 1, 256, 4, 2, 64, 1024)
 
 
 @pytest.mark.parametrize("rows", [1, 2, 3, 4, 5, 7, 8, 9, 16, 17, 40])
 def test_decode_rows_on_both_engines(rows):
     _gpu()
     _decode_rows(ROWS_SHAPE, rows)
+
+
+# Matrix-core launches over an odd number of 128-wide k chunks (the engine takes them in pairs):
+# hidden 384 and ffn 1152 leave the QKV, O and gate/up projections unsplit over 3 chunks and cut
+# the down projection into ranges of 6 and 3 chunks; hidden 1152 cuts the QKV (RoPE epilogue) and
+# gate/up projections, normalised over ranges, into 6 and 3 chunks.
+ODD_CHUNKS = [synth.StageShape("chunks-1L-h384", 9, 1, 384, 6, 6, 64, 1152),
+              synth.StageShape("chunks-1L-h1152", 10, 1, 1152, 2, 2, 64, 256)]
+
+
+@pytest.mark.parametrize("rows", [3, 5, 16])
+@pytest.mark.parametrize("shape", ODD_CHUNKS, ids=["h384", "h1152"])
+def test_matrix_core_odd_chunk_counts(shape, rows):
+    _gpu()
+    _decode_rows(shape, rows)
 
 
 # A stage whose widths are off the 32 grid (hidden 200, ffn 440, four heads of 64): in prefill the
