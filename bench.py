@@ -41,8 +41,8 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": 940189726,
-                                "source_sha256": "7b0ae265bc5c8a51344e2a66331e4391a818ef72a6ef67f1667813c9fde377d6"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940173582,
+                                "source_sha256": "178c3510c3976a77aa27a5dbdfee763a986bbe60b077a7e5ce8a5941f37b3348"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 

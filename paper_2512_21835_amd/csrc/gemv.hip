@@ -299,12 +299,14 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
     return r;
 }
 
-// One workgroup: units 64 blockIdx.x .. + 63 (wavefront w: 16 of them) for up to 16 activation
-// rows.  SPLIT: k chunks [blockIdx.y * cps, (blockIdx.y + 1) * cps) only, partial products and
-// sums of squares to the workspace [split][w][m][units], [split][m].  LDS: 80 KB with two weight
-// rows per unit (two workgroups per compute unit), 48 KB with one (three).
-template <int MODE, bool SPLIT>
+// One workgroup: units 4 UW blockIdx.x .. + 4 UW - 1 (wavefront w: UW <= 16 of them, the MFMA's
+// other B columns unused) for up to 16 activation rows.  SPLIT: k chunks [blockIdx.y * cps,
+// (blockIdx.y + 1) * cps) only, partial products and sums of squares to the workspace
+// [split][w][m][units], [split][m].  LDS: 80 KB with two weight rows per unit (two workgroups per
+// compute unit), 48 KB with one (three).
+template <int MODE, bool SPLIT, int UW>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
+    static_assert(UW % 2 == 0 && UW >= 2 && UW <= 16, "units per wavefront: an even number up to 16");
     constexpr bool kNorm = Shape<MODE>::kNorm;
     constexpr int NW = Shape<MODE>::NW;
     // wavefront B tiles of a chunk pair: [wave][matrix][chunk], row r, k segment s at 16 r + (s ^ r)
@@ -313,12 +315,12 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
     float *const ssp = reinterpret_cast<float *>(&at[0][0][0][0]);   // [wave][lane], after the k loop
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int units = n_units<MODE>(a);
-    const int u0 = blockIdx.x * 64 + 16 * wave;
+    const int u0 = blockIdx.x * 4 * UW + UW * wave;
     const int K = a.K, chunks = K / kChunkK, rows = a.rows;
     const int c_beg = SPLIT ? blockIdx.y * cps : 0;
     const int c_end = SPLIT ? min(c_beg + cps, chunks) : chunks;
 
-    // load instruction i of matrix w: lane l reads row 2 i + l / 32 of the block, 16-byte k
+    // load instruction i < UW / 2 of matrix w: lane l reads row 2 i + l / 32 of the block, 16-byte k
     // segment l % 16 of chunk (l / 16) % 2 of the pair, i.e. 512 contiguous bytes per row; rows
     // past the last unit are clamped to it, and a missing second chunk of a range to its first
     // (in bounds, results dropped)
@@ -350,7 +352,8 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int i = 0; i < 8; ++i) b.w[w][i] = load_stream16(wp[w][i] + kc);
+            for (int i = 0; i < 8; ++i)
+                if (2 * i < UW) b.w[w][i] = load_stream16(wp[w][i] + kc);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int k = kChunkK * min(c + h, c_end - 1);
@@ -405,7 +408,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int r = 2 * i + pr;
-                bt[wave][w][ph][16 * r + (ps ^ r)] = b.w[w][i];
+                if (2 * i < UW) bt[wave][w][ph][16 * r + (ps ^ r)] = b.w[w][i];
             }
         if (c + 2 < c_end) load(c + 2, b);
         // A tiles complete for every wavefront (each wavefront reads only its own B tiles)
@@ -431,7 +434,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(GemvArgs a, int cps) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int m = 4 * lr + i, u = u0 + lk;
-        if (m >= rows || u >= units) continue;
+        if (m >= rows || lk >= UW || u >= units) continue;
         if (SPLIT) {
 #pragma unroll
             for (int w = 0; w < NW; ++w)
@@ -493,6 +496,20 @@ int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ?
 // down 4 ranges 78 us against 92 for 8 and 95 for 2; 70B O 4 ranges 28 us against 31 for 8; 8B
 // gate/up unsplit 48.7 us against 52.1 with 2 ranges; 8B QKV 6 ranges 17.4 us against 18.1 for 4;
 // 8B down and O 8 ranges.  Without a workspace, unsplit.
+//
+// An unsplit launch of the SwiGLU or residual form takes 14 units per wavefront instead of 16
+// where that leaves the most loaded compute unit fewer units (ceil(workgroups / 256) x units per
+// wavefront): the 70B gate/up projection (F = 28672 = 7 x 2^12) then runs 512 workgroups, two on
+// every compute unit, where 16 leaves 448 and a quarter of the compute units half idle (153 ->
+// 143 us at 4 to 16 rows); the 8B one (F = 14336) 256 workgroups instead of 224 (48.5 -> 46.7
+// us).  12 units per wavefront (597 and 299 workgroups) took 171 and 56 us.
+constexpr int kComputeUnits = 256;
+
+bool fewer_units_per_wave(int units) {
+    const long b16 = (units + 63) / 64, b14 = (units + 55) / 56;
+    return (b14 + kComputeUnits - 1) / kComputeUnits * 14 < (b16 + kComputeUnits - 1) / kComputeUnits * 16;
+}
+
 template <int MODE>
 void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int units = host_units(MODE, c), chunks = c.K / kChunkK;
@@ -500,20 +517,30 @@ void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1
     const int grid_max = Shape<MODE>::NW == 1 ? 512 : 300;
     int splits = max(1, min(min(kGemvMaxSplits, chunks / 4), grid_max / blocks));
     if (!c.split_part || !c.split_ss) splits = 1;
+    if constexpr (MODE != GEMV_NORM_ROPE_KV) {
+        if (splits == 1 && fewer_units_per_wave(units)) {
+            const dim3 grid((units + 55) / 56);
+            if (e0 || e1)
+                STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, false, 14>), grid, dim3(256), 0, st, e0, e1, 0, c, 0);
+            else
+                STG_LAUNCH((gemv_mfma_kernel<MODE, false, 14>), grid, dim3(256), 0, st, c, 0);
+            return;
+        }
+    }
     if (splits == 1) {
         if (e0 || e1)
-            STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, c, 0);
+            STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, false, 16>), dim3(blocks), dim3(256), 0, st, e0, e1, 0, c, 0);
         else
-            STG_LAUNCH((gemv_mfma_kernel<MODE, false>), dim3(blocks), dim3(256), 0, st, c, 0);
+            STG_LAUNCH((gemv_mfma_kernel<MODE, false, 16>), dim3(blocks), dim3(256), 0, st, c, 0);
         return;
     }
     const int cps = ((chunks + splits - 1) / splits + 1) & ~1;   // whole chunk pairs
     splits = (chunks + cps - 1) / cps;  // no empty range
     if (e0)
-        STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr, 0,
-                              c, cps);
+        STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, true, 16>), dim3(blocks, splits), dim3(256), 0, st, e0, nullptr,
+                              0, c, cps);
     else
-        STG_LAUNCH((gemv_mfma_kernel<MODE, true>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
+        STG_LAUNCH((gemv_mfma_kernel<MODE, true, 16>), dim3(blocks, splits), dim3(256), 0, st, c, cps);
     const int eg = (c.rows * units + 255) / 256;
     if (e1)
         STG_EXT_LAUNCH((gemv_split_epilogue<MODE>), dim3(eg), dim3(256), 0, st, nullptr, e1, 0, c, splits);

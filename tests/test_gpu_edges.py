@@ -259,16 +259,18 @@ def test_decode_rows_on_both_engines(rows):
     _decode_rows(ROWS_SHAPE, rows)
 
 
-# Matrix-core launches over an odd number of 128-wide k chunks (the engine takes them in pairs):
+# Matrix-core launch forms: an odd number of 128-wide k chunks (the engine takes them in pairs):
 # hidden 384 and ffn 1152 leave the QKV, O and gate/up projections unsplit over 3 chunks and cut
 # the down projection into ranges of 6 and 3 chunks; hidden 1152 cuts the QKV (RoPE epilogue) and
-# gate/up projections, normalised over ranges, into 6 and 3 chunks.
+# gate/up projections, normalised over ranges, into 6 and 3 chunks.  Units per wavefront: small
+# unsplit launches take 14, and ffn 16384 (256 workgroups of 64 gate/up units) keeps 16.
 ODD_CHUNKS = [synth.StageShape("chunks-1L-h384", 9, 1, 384, 6, 6, 64, 1152),
-              synth.StageShape("chunks-1L-h1152", 10, 1, 1152, 2, 2, 64, 256)]
+              synth.StageShape("chunks-1L-h1152", 10, 1, 1152, 2, 2, 64, 256),
+              synth.StageShape("wide-ffn-1L-h128", 11, 1, 128, 2, 2, 64, 16384)]
 
 
 @pytest.mark.parametrize("rows", [3, 5, 16])
-@pytest.mark.parametrize("shape", ODD_CHUNKS, ids=["h384", "h1152"])
+@pytest.mark.parametrize("shape", ODD_CHUNKS, ids=["h384", "h1152", "f16384"])
 def test_matrix_core_odd_chunk_counts(shape, rows):
     _gpu()
     _decode_rows(shape, rows)
