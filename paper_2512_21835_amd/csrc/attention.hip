@@ -458,7 +458,11 @@ template <int G, int D, bool FINAL>
 __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
     static_assert(D == 128 && G <= 16, "one 128-wide head, up to 16 query heads per KV head");
     constexpr int VROW = D + 8;                     // V tile row stride in bf16 (272 bytes)
-    __shared__ uint16_t vs[kChunk][VROW];
+    // one LDS area for the K tile (until the first barrier: each wavefront reads only its own 16
+    // keys) and then the V tile
+    __shared__ uint4 kv_tile[kChunk * VROW * 2 / 16];
+    uint4 (*const ks)[D / 8] = reinterpret_cast<uint4 (*)[D / 8]>(kv_tile);    // [key][chunk ^ key % 16]
+    uint16_t (*const vs)[VROW] = reinterpret_cast<uint16_t (*)[VROW]>(kv_tile);
     __shared__ uint4 pf[2][2][64];                  // P A-fragments [key step][hi, lo][lane]
     __shared__ float wm[4][16], wl[4][16];
     const int split = blockIdx.x, g = blockIdx.y, row = blockIdx.z;
@@ -487,17 +491,19 @@ __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
     const int blk = a.kv.block_table[(size_t)slot * a.kv.max_blocks + (kbeg + min(16 * wave, n - 1)) / kBlockTokens];
     const uint16_t *kb = pool + (size_t)blk * blk_stride + (size_t)g * kBlockTokens * D;
     const uint16_t *vb = pool + (size_t)blk * blk_stride + (size_t)(hkv + g) * kBlockTokens * D;
-    // K fragments: key 16 wave + l16 of the split (clamped into the split), d 32 s + 8 lq
-    const int kkey = kbeg + min(16 * wave + l16, n - 1);
-    const uint16_t *kp = kb + (size_t)(kkey % kBlockTokens) * D + 8 * lq;
-    uint4 kf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) kf[s] = *reinterpret_cast<const uint4 *>(kp + 32 * s);
-    // V rows: instruction i, lane l: key 16 wave + 4 i + lq, d 8 l16
+    // K and V rows, 4 keys x 256 contiguous bytes per load instruction (16 keys x 64 bytes, the
+    // MFMA fragment layout read straight from memory, streams poorly): instruction i, lane l: key
+    // 16 wave + 4 i + lq of the split (clamped into it); K: 16-byte d chunk l16 ^ (4 i + lq),
+    // stored in the K tile at [key][l16]; V: chunk l16
+    auto krow = [&](int i) {
+        const int key = kbeg + min(16 * wave + 4 * i + lq, n - 1);
+        return *reinterpret_cast<const uint4 *>(kb + (size_t)(key % kBlockTokens) * D + 8 * (l16 ^ (4 * i + lq)));
+    };
     auto vrow = [&](int i) {
         const int key = kbeg + min(16 * wave + 4 * i + lq, n - 1);
         return *reinterpret_cast<const uint4 *>(vb + (size_t)(key % kBlockTokens) * D + 8 * l16);
     };
+    const uint4 kr0 = krow(0), kr1 = krow(1), kr2 = krow(2), kr3 = krow(3);
     const uint4 vr0 = vrow(0), vr1 = vrow(1), vr2 = vrow(2), vr3 = vrow(3);
     // every K and V load in flight before any is used (left alone, the scheduler issues half of
     // them after the first products, a second round trip to memory)
@@ -514,15 +520,18 @@ __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
         for (int j = 0; j < 8; ++j) x[j] = l16 < G ? q8[j] * scale : 0.f;
         split8(x, qh[s], ql[s]);
     }
-    *reinterpret_cast<uint4 *>(&vs[16 * wave + lq][8 * l16]) = vr0;
-    *reinterpret_cast<uint4 *>(&vs[16 * wave + 4 + lq][8 * l16]) = vr1;
-    *reinterpret_cast<uint4 *>(&vs[16 * wave + 8 + lq][8 * l16]) = vr2;
-    *reinterpret_cast<uint4 *>(&vs[16 * wave + 12 + lq][8 * l16]) = vr3;
+    ks[16 * wave + lq][l16] = kr0;
+    ks[16 * wave + 4 + lq][l16] = kr1;
+    ks[16 * wave + 8 + lq][l16] = kr2;
+    ks[16 * wave + 12 + lq][l16] = kr3;
+    // K fragments: key 16 wave + l16, d 32 s + 8 lq, i.e. chunk 4 s + lq (the tile holds chunk c of
+    // key k at c ^ k % 16: every 16 lanes of a read meet distinct banks)
     f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(kf[s]), qh[s], sc, 0, 0, 0);
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(kf[s]), ql[s], sc, 0, 0, 0);
+        const bf16x8_t kf = as_bf(ks[16 * wave + l16][(4 * s + lq) ^ l16]);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[s], sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[s], sc, 0, 0, 0);
     }
     // sc[i]: score of key 16 wave + 4 lq + i for head l16
     float mx = -INFINITY;
@@ -534,7 +543,11 @@ __global__ __launch_bounds__(256) void attn_decode_mfma(AttnArgs a) {
     mx = fmaxf(mx, lane_xor(mx, 16));
     mx = fmaxf(mx, lane_xor(mx, 32));
     if (lane < 16) wm[wave][lane] = mx;
-    __syncthreads();
+    __syncthreads();   // every wavefront's K reads done: the tile takes V
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + lq][8 * l16]) = vr0;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 4 + lq][8 * l16]) = vr1;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 8 + lq][8 * l16]) = vr2;
+    *reinterpret_cast<uint4 *>(&vs[16 * wave + 12 + lq][8 * l16]) = vr3;
     const float mh = fmaxf(fmaxf(wm[0][l16], wm[1][l16]), fmaxf(wm[2][l16], wm[3][l16]));
     float p[4], ls = 0.f;
 #pragma unroll
