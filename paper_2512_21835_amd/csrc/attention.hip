@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include "lanes.h"
+#include "pair.h"
 #include "stage_kernels.h"
 
 namespace stg {
@@ -789,8 +790,20 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma(AttnArgs a) {
     }
     if (!qvalid) return;
     // O^T[d = 32 b + 8 (i / 4) + 4 half + i % 4][query col]
-    float *orow = a.out + qrow * q_ld + (size_t)(g * G + hh) * D;
     const float inv = 1.f / l_run;
+    if (a.out_pair) {   // four consecutive d of one 32-wide block per store
+        uint16_t *prow = a.out_pair + qrow * a.out_pair_ld;
+        const int k0 = (g * G + hh) * D;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                store_pair4(prow + pair_at(k0 + 32 * b + 8 * j + 4 * half),
+                            make_float4(o[b][4 * j] * inv, o[b][4 * j + 1] * inv, o[b][4 * j + 2] * inv,
+                                        o[b][4 * j + 3] * inv));
+        return;
+    }
+    float *orow = a.out + qrow * q_ld + (size_t)(g * G + hh) * D;
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll

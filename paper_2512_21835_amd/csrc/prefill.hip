@@ -22,6 +22,7 @@
 #include <type_traits>
 
 #include "lanes.h"
+#include "pair.h"
 #include "stage_kernels.h"
 
 namespace stg {
@@ -32,30 +33,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 32;
 constexpr int kFrag = (BM / 32) * (BK / 16) * 64;  // 16-byte fragment slots per operand tile (512)
-
-__device__ __forceinline__ uint16_t to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ void split(float v, uint16_t &hi, uint16_t &lo) {
-    hi = to_bf16(v);
-    lo = to_bf16(v - __uint_as_float((uint32_t)hi << 16));
-}
-
-// The hi and lo of four consecutive elements of a 32-wide block (p: the first one's hi, 8-byte
-// aligned): two 8-byte stores, the lo 32 elements further.
-__device__ __forceinline__ void store_pair4(uint16_t *p, float4 v) {
-    uint16_t h[4], l[4];
-    split(v.x, h[0], l[0]);
-    split(v.y, h[1], l[1]);
-    split(v.z, h[2], l[2]);
-    split(v.w, h[3], l[3]);
-    *reinterpret_cast<uint2 *>(p) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-    *reinterpret_cast<uint2 *>(p + 32) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
-}
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &v) {
     bf16x8 r;
@@ -375,7 +352,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a) {
                     if (m >= M) continue;
                     const float gt = acc[i][j][r], up = acc[i][j + 1][r];
                     const size_t o = (size_t)m * a.ldo + pair_at(n);
-                    split(gt / (1.f + expf(-gt)) * up, a.out_pair[o], a.out_pair[o + 32]);
+                    split_pair(gt / (1.f + expf(-gt)) * up, a.out_pair[o], a.out_pair[o + 32]);
                 }
             }
         return;

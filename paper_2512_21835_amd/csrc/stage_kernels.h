@@ -128,6 +128,10 @@ hipError_t launch_rope_kv_store(const RopeKvArgs &a, hipStream_t st);
 struct AttnArgs {
     const float *q;      // [rows, Hq d] rotated
     float *out;          // [rows, Hq d]
+    // prefill with the bf16 cache: when set, the output goes here instead of `out`, as the hi/lo
+    // pair the O projection GEMM reads ([rows, out_pair_ld], pair_at layout)
+    uint16_t *out_pair;
+    long out_pair_ld;
     float *part_o;       // [rows, Hq, max_splits, d] unnormalised partial outputs
     float *part_ml;      // [rows, Hq, max_splits, 2] partial max and sum
     KvView kv;

@@ -808,8 +808,12 @@ int run_layer_prefill(stage *s, int layer, const LayerWeights &w, int rows, int 
     at.n_seqs = rows / T;
     at.rows_per_seq = T;
     at.meta = meta;
+    if (!s->cfg.kv_fp32) {   // the matrix-core kernel writes the O projection's operand pair itself
+        at.out_pair = s->ws_pair;
+        at.out_pair_ld = pair_ld(qd);
+    }
     HIP_TRY(launch_attention(at, s->cs));
-    HIP_TRY(launch_split(s->ws_attn, rows, qd, s->ws_pair, pair_ld(qd), s->cs));
+    if (s->cfg.kv_fp32) HIP_TRY(launch_split(s->ws_attn, rows, qd, s->ws_pair, pair_ld(qd), s->cs));
 
     GemmArgs o{};
     o.a = s->ws_pair; o.lda = pair_ld(qd);
