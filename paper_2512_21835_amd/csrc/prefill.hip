@@ -401,6 +401,43 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float *x, cons
     }
 }
 
+// The same for H = 1024 NV (NV <= 8): a thread's NV float4 of the row stay in registers between
+// the sum of squares and the output, so the row is read once (same arithmetic in the same order:
+// identical results).
+template <int NV>
+__global__ __launch_bounds__(256) void rmsnorm_split_rows_kernel(const float *x, const uint16_t *g, float eps,
+                                                                 uint16_t *pair, long ld) {
+    constexpr int H = 1024 * NV;
+    const int row = blockIdx.x;
+    const float *xr = x + (size_t)row * H + 4 * threadIdx.x;
+    float4 v[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) v[j] = *reinterpret_cast<const float4 *>(xr + 1024 * j);
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        ss = fmaf(v[j].x, v[j].x, ss);
+        ss = fmaf(v[j].y, v[j].y, ss);
+        ss = fmaf(v[j].z, v[j].z, ss);
+        ss = fmaf(v[j].w, v[j].w, ss);
+    }
+    __shared__ float red[4];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += lane_xor(ss, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float tot = ((red[0] + red[1]) + red[2]) + red[3];
+    const float scale = 1.f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int i = 4 * threadIdx.x + 1024 * j;
+        const uint2 gg = *reinterpret_cast<const uint2 *>(g + i);
+        store_pair4(pair + (size_t)row * ld + pair_at(i),
+                    make_float4(v[j].x * scale * __uint_as_float(gg.x << 16), v[j].y * scale * __uint_as_float(gg.x & 0xFFFF0000u),
+                                v[j].z * scale * __uint_as_float(gg.y << 16), v[j].w * scale * __uint_as_float(gg.y & 0xFFFF0000u)));
+    }
+}
+
 // The pair (row stride ld) of an fp32 matrix [rows, n] (row stride n, n % 4 == 0), four elements
 // per thread.
 __global__ __launch_bounds__(256) void split_kernel(const float *x, int rows, int n, uint16_t *pair, long ld) {
@@ -472,7 +509,11 @@ hipError_t launch_rmsnorm_split(const float *x, const uint16_t *g, float eps, in
                                 long ld, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     if (ld < pair_ld(H) || H % 4 != 0) return hipErrorInvalidValue;
-    STG_LAUNCH(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, pair, ld);
+    switch (H) {
+        case 4096: STG_LAUNCH(rmsnorm_split_rows_kernel<4>, dim3(rows), dim3(256), 0, st, x, g, eps, pair, ld); break;
+        case 8192: STG_LAUNCH(rmsnorm_split_rows_kernel<8>, dim3(rows), dim3(256), 0, st, x, g, eps, pair, ld); break;
+        default: STG_LAUNCH(rmsnorm_split_kernel, dim3(rows), dim3(256), 0, st, x, g, eps, H, pair, ld);
+    }
     return hipGetLastError();
 }
 
