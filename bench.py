@@ -41,10 +41,10 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": 940174029,
-                                "source_sha256": "33306cf25c340d5f57741db15f3c8280c27aa2fda926082c5a7df3e530f1e163"},
-    "llama3-8b-shaped-8L": {"bytes": 235246761,
-                            "source_sha256": "33306cf25c340d5f57741db15f3c8280c27aa2fda926082c5a7df3e530f1e163"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940174477,
+                                "source_sha256": "d2437c39790525d57fb9667183942733c2ed15d88a9f1ed83bf36bc00b3a514d"},
+    "llama3-8b-shaped-8L": {"bytes": 235246873,
+                            "source_sha256": "d2437c39790525d57fb9667183942733c2ed15d88a9f1ed83bf36bc00b3a514d"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 

@@ -42,6 +42,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "lanes.h"
 #include "stage_kernels.h"
 
@@ -488,9 +490,9 @@ __global__ __launch_bounds__(256) void gemv_split_epilogue(GemvArgs a, int split
 int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ? a.N / 2 : a.N; }
 
 // K ranges of whole chunk pairs, at most 8 and at most one per four chunks, as many as keep the
-// grid within one even layer of workgroups: 512 (two per compute unit) with one weight row per
-// unit, 300 (about one per compute unit) with two, whose 80 KB of LDS leave room for two but whose
-// split epilogue costs more than a second, partial layer gains.  Swept at 4, 8 and 16 rows on the
+// grid within one even layer of workgroups: two per compute unit (512 on MI355X) with one weight
+// row per unit, 7/6 per compute unit (298) with two, whose 80 KB of LDS leave room for two but
+// whose split epilogue costs more than a second, partial layer gains.  Swept at 4, 8 and 16 rows on the
 // 8B- and 70B-shaped layers (16 rows, with the epilogue): 70B gate/up unsplit (448 workgroups)
 // 155 us against 165 with 4 ranges; 70B QKV 3 ranges 36.7 us, 4 ranges 44.6, 6 ranges 39.7; 70B
 // down 4 ranges 78 us against 92 for 8 and 95 for 2; 70B O 4 ranges 28 us against 31 for 8; 8B
@@ -498,27 +500,26 @@ int host_units(int mode, const GemvArgs &a) { return mode == GEMV_NORM_ROPE_KV ?
 // 8B down and O 8 ranges.  Without a workspace, unsplit.
 //
 // An unsplit launch of the SwiGLU or residual form takes 14 units per wavefront instead of 16
-// where that leaves the most loaded compute unit fewer units (ceil(workgroups / 256) x units per
-// wavefront): the 70B gate/up projection (F = 28672 = 7 x 2^12) then runs 512 workgroups, two on
+// where that leaves the most loaded compute unit fewer units (ceil(workgroups / compute units) x
+// units per wavefront): the 70B gate/up projection (F = 28672 = 7 x 2^12) then runs 512 workgroups, two on
 // every compute unit, where 16 leaves 448 and a quarter of the compute units half idle (153 ->
 // 143 us at 4 to 16 rows); the 8B one (F = 14336) 256 workgroups instead of 224 (48.5 -> 46.7
 // us).  12 units per wavefront (597 and 299 workgroups) took 171 and 56 us.
-constexpr int kComputeUnits = 256;
-
-bool fewer_units_per_wave(int units) {
+bool fewer_units_per_wave(int units, int cus) {
     const long b16 = (units + 63) / 64, b14 = (units + 55) / 56;
-    return (b14 + kComputeUnits - 1) / kComputeUnits * 14 < (b16 + kComputeUnits - 1) / kComputeUnits * 16;
+    return (b14 + cus - 1) / cus * 14 < (b16 + cus - 1) / cus * 16;
 }
 
 template <int MODE>
 void launch_mfma(const GemvArgs &c, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     const int units = host_units(MODE, c), chunks = c.K / kChunkK;
     const int blocks = (units + 63) / 64;
-    const int grid_max = Shape<MODE>::NW == 1 ? 512 : 300;
+    const int cus = device_compute_units();
+    const int grid_max = Shape<MODE>::NW == 1 ? 2 * cus : cus * 7 / 6;
     int splits = max(1, min(min(kGemvMaxSplits, chunks / 4), grid_max / blocks));
     if (!c.split_part || !c.split_ss) splits = 1;
     if constexpr (MODE != GEMV_NORM_ROPE_KV) {
-        if (splits == 1 && fewer_units_per_wave(units)) {
+        if (splits == 1 && fewer_units_per_wave(units, cus)) {
             const dim3 grid((units + 55) / 56);
             if (e0 || e1)
                 STG_EXT_LAUNCH((gemv_mfma_kernel<MODE, false, 14>), grid, dim3(256), 0, st, e0, e1, 0, c, 0);
@@ -618,6 +619,25 @@ hipError_t launch_mode(const GemvArgs &a, hipStream_t st, hipEvent_t ev_start, h
 }
 
 }  // namespace
+
+// (256, the count of a whole MI355X, if the runtime cannot tell)
+int device_compute_units() {
+    constexpr int kDevices = 64;
+    static std::atomic<int> cached[kDevices];
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) {
+        (void)hipGetLastError();   // a failed query must not surface as a launch error
+        return 256;
+    }
+    n = cached[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+        (void)hipGetLastError();
+        return 256;
+    }
+    cached[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
 
 hipError_t launch_gemv(int mode, GemvArgs a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (a.rows <= 0) return hipSuccess;

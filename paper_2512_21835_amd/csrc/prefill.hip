@@ -482,7 +482,7 @@ void launch_gemm_mode(const GemmArgs &a, int n_mats, hipStream_t st) {
         }
     }
     // the wide tiles when they still fill every compute unit (their pipelined loop takes K >= 64)
-    if ((long)wide.x * wide.y * wide.z >= 256 && a.K >= 2 * BK)
+    if ((long)wide.x * wide.y * wide.z >= device_compute_units() && a.K >= 2 * BK)
         STG_LAUNCH((gemm_dma_kernel<MODE, 4>), wide, dim3(256), 0, st, a);
     else
         STG_LAUNCH((gemm_dma_kernel<MODE, 2>), grid, dim3(256), 0, st, a);

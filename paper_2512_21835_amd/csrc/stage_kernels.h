@@ -74,6 +74,10 @@ struct GemvArgs {
 };
 constexpr int kGemvMaxSplits = 8;
 
+// Compute units of the current device (256 on a whole MI355X; fewer on a partitioned one), read
+// once per device.  Launch shapes that aim at one or two workgroups per compute unit use it.
+int device_compute_units();
+
 // y = W x for `rows` activation rows (any number; launched in chunks of up to 8 rows).  K must be a
 // multiple of 8.  Non-null events are recorded at the start of the first and the end of the last
 // launch (kernel timestamps, no extra stream packets).
