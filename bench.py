@@ -41,10 +41,10 @@ OVERLAP_TARGET = 0.8    # hidden-shorter fraction the offloaded stage should rea
 # in the same run).  Valid for the GEMV source it was taken on: with any other source the field is
 # reported as null.
 GATEUP_TRAFFIC = {
-    "llama3.3-70b-shaped-16L": {"bytes": 940174477,
-                                "source_sha256": "d2437c39790525d57fb9667183942733c2ed15d88a9f1ed83bf36bc00b3a514d"},
-    "llama3-8b-shaped-8L": {"bytes": 235246873,
-                            "source_sha256": "d2437c39790525d57fb9667183942733c2ed15d88a9f1ed83bf36bc00b3a514d"},
+    "llama3.3-70b-shaped-16L": {"bytes": 940172778,
+                                "source_sha256": "b86a279723f17c625b0331b91585831d31090808d9141c423fd3f7f5a4f43d1b"},
+    "llama3-8b-shaped-8L": {"bytes": 235246452,
+                            "source_sha256": "b86a279723f17c625b0331b91585831d31090808d9141c423fd3f7f5a4f43d1b"},
 }
 KERNEL_SOURCES = ("paper_2512_21835_amd/csrc/gemv.hip", "paper_2512_21835_amd/csrc/stage_kernels.h")
 

@@ -25,8 +25,9 @@
 // Matrix-core engine (gemv_mfma_kernel), for launches of 3 to 16 activation rows (5 to 16 for
 // the square O projection), where the vector kernel falls behind (one multiply-add per row per
 // weight element): the rows are the A operand of v_mfma_f32_16x16x32_bf16 (padded to 16, the
-// fp32 activation as a bf16 hi + lo pair, two MFMAs), 16 weight rows the B operand.  A workgroup owns 64 units, each
-// wavefront 16 of them over the workgroup's K range, in chunks of 128 k taken two at a time.  The
+// fp32 activation as a bf16 hi + lo pair, two MFMAs), up to 16 weight rows the B operand.  A workgroup
+// of four wavefronts owns 4 x 16 units (4 x 14 in unsplit launches where that evens out the grid),
+// each wavefront its share over the workgroup's K range, in chunks of 128 k taken two at a time.  The
 // B layout wants 16 rows x 64 bytes per load instruction, which streams HBM poorly (~4 TB/s; 4
 // rows x 256 bytes ~5.7 TB/s), so a wavefront loads a pair of chunks as 2 rows x 512 contiguous
 // bytes per instruction, stores both chunks in its own LDS tiles (the 16-byte k segments
